@@ -1,0 +1,324 @@
+"""Pins for the fp64 oracle (CPU only).
+
+Each test checks the oracle against something other than itself: the plain
+dense definition Y = X W^T that PIFA reproduces losslessly (Sec. 3.2), the
+closed-form coefficient matrix C = U[I^c] U[I]^-1, LAPACK's QR with column
+pivoting (dgeqp3, run through scipy, not copied), least squares through
+numpy, the parameter count of Sec. 3.3, hand-derived worked examples in
+tests/golden/, and brute force on tiny inputs.  The mutation tests at the end
+plant plausible mistakes in oracle outputs and check that the pins catch them.
+"""
+import itertools
+import json
+import os
+
+import numpy as np
+import pytest
+import scipy.linalg
+
+import oracle
+from paper_2501_19090_amd import inputs
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _layer(d_out, d_in, r, seed=1):
+    U, V = inputs.lowrank_factors(d_out, d_in, r, seed)
+    return U, V, U @ V
+
+
+def _rel(a, b):
+    nb = np.linalg.norm(b)
+    return np.linalg.norm(a - b) / (nb if nb > 0 else 1.0)
+
+
+# ---------------------------------------------------------------- brute force
+def _triple_loop_dense(X, W):
+    M, K = X.shape
+    N = W.shape[0]
+    Y = [[0.0] * N for _ in range(M)]
+    for m in range(M):
+        for n in range(N):
+            s = 0.0
+            for k in range(K):
+                s += float(X[m, k]) * float(W[n, k])
+            Y[m][n] = s
+    return np.array(Y)
+
+
+@pytest.mark.parametrize("d_out,d_in", [(1, 1), (4, 4), (5, 3), (3, 6), (8, 8), (12, 7), (7, 16), (16, 16)])
+def test_tiny_bruteforce_every_rank(d_out, d_in):
+    """PIFA build + forward equals a triple-loop X W^T for every admissible r."""
+    for r in range(1, min(d_out, d_in) + 1):
+        U, V, W = _layer(d_out, d_in, r, seed=100 + r)
+        b = oracle.build_pifa(W, r)
+        X = inputs.activations(3, d_in, seed=r)
+        Y = oracle.pifa_forward(X, b["pivot_idx"], b["nonpivot_idx"], b["Wp"], b["C"])
+        Yref = _triple_loop_dense(X, W)
+        assert _rel(Y, Yref) <= 1e-12, (d_out, d_in, r)
+
+
+# ---------------------------------------------------------------- build invariants
+SHAPES = [(64, 48, 16), (48, 64, 16), (256, 256, 128), (96, 96, 1), (80, 120, 80),
+          (120, 80, 80), (333, 200, 150), (1024, 1024, 512), (2752, 1024, 512), (1024, 2752, 512)]
+
+
+@pytest.mark.parametrize("d_out,d_in,r", SHAPES)
+def test_build_lossless_and_partition(d_out, d_in, r):
+    U, V, W = _layer(d_out, d_in, r)
+    b = oracle.build_pifa(W, r)
+    piv, npiv = b["pivot_idx"], b["nonpivot_idx"]
+    # exactly r pivots; I and I^c partition [0, d_out), both sorted
+    assert piv.size == r and npiv.size == d_out - r
+    assert np.all(np.diff(piv) > 0) and (npiv.size < 2 or np.all(np.diff(npiv) > 0))
+    assert np.array_equal(np.sort(np.concatenate([piv, npiv])), np.arange(d_out))
+    # W_p is W'[I, :] exactly (eq. separate)
+    assert np.array_equal(b["Wp"], W[piv])
+    # lossless: P[W_p; C W_p] == W (eq. wnp)
+    assert oracle.reconstruction_error(W, piv, npiv, b["Wp"], b["C"]) <= 1e-10
+    # numpy's own product for the same check (library, not the oracle's loops)
+    if npiv.size:
+        assert _rel(b["C"] @ b["Wp"], W[npiv]) <= 1e-10
+    # rank certification recorded
+    assert b["report"][3] == 1.0
+
+
+@pytest.mark.parametrize("d_out,d_in,r", SHAPES)
+def test_parameter_count(d_out, d_in, r):
+    """Stored values r*d_in + (d_out-r)*r; with the r indices this is the
+    paper's r(m+n) - r^2 + r (Sec. 3.3), and it meets the degrees-of-freedom
+    count r(m+n) - (r^2 - r) of Sec. 3.1."""
+    _, _, W = _layer(d_out, d_in, r)
+    b = oracle.build_pifa(W, r)
+    n_values = b["Wp"].size + b["C"].size
+    assert n_values == r * (d_in + d_out - r)
+    assert n_values + b["pivot_idx"].size == r * (d_out + d_in) - r * r + r
+    assert n_values + b["pivot_idx"].size == r * (d_out + d_in) - (r * r - r)
+
+
+@pytest.mark.parametrize("d_out,d_in,r", [s for s in SHAPES if s[0] > s[2]])
+def test_coefficients_match_closed_form(d_out, d_in, r):
+    """C = U[I^c] U[I]^-1 (V has full row rank), and C is the least-squares
+    solution of W_p^T C^T = W_np^T (numpy lstsq)."""
+    U, V, W = _layer(d_out, d_in, r)
+    b = oracle.build_pifa(W, r)
+    piv, npiv = b["pivot_idx"], b["nonpivot_idx"]
+    C_closed = np.linalg.solve(U[piv].T, U[npiv].T).T
+    assert _rel(b["C"], C_closed) <= 1e-9
+    C_lsq = np.linalg.lstsq(W[piv].T, W[npiv].T, rcond=None)[0].T
+    assert _rel(b["C"], C_lsq) <= 1e-9
+
+
+@pytest.mark.parametrize("d_out,d_in,r,seed", [(64, 48, 16, 1), (48, 64, 16, 2), (256, 256, 128, 3),
+                                               (300, 200, 120, 4), (1024, 1024, 512, 5), (2752, 1024, 512, 6)])
+def test_pivots_match_lapack_dgeqp3(d_out, d_in, r, seed):
+    """The pivot sequence is Businger-Golub's: LAPACK dgeqp3 on W^T selects
+    the same first r columns, in the same order."""
+    _, _, W = _layer(d_out, d_in, r, seed)
+    b = oracle.build_pifa(W, r)
+    _, _, P = scipy.linalg.qr(W.T, pivoting=True, mode="economic")
+    assert np.array_equal(P[:r], b["select_order"])
+    assert np.array_equal(np.sort(P[:r]), b["pivot_idx"])
+
+
+def test_selection_order_is_not_sorted():
+    """The QRCP selection order is generally unsorted, so sorting I is a real step."""
+    _, _, W = _layer(256, 256, 128)
+    b = oracle.build_pifa(W, 128)
+    assert not np.all(np.diff(b["select_order"]) > 0)
+
+
+def test_lapack_pivot_set_also_lossless():
+    """A second, independently chosen pivot set (LAPACK's) also gives a
+    lossless layer: the paper allows any r independent rows."""
+    U, V, W = _layer(300, 200, 120, 9)
+    _, _, P = scipy.linalg.qr(W.T, pivoting=True, mode="economic")
+    piv = np.sort(P[:120])
+    npiv = np.setdiff1d(np.arange(300), piv)
+    C = np.linalg.lstsq(W[piv].T, W[npiv].T, rcond=None)[0].T
+    assert oracle.reconstruction_error(W, piv, npiv, W[piv], C) <= 1e-10
+
+
+# ---------------------------------------------------------------- golden worked examples
+def _golden():
+    with open(os.path.join(GOLDEN, "qrcp_worked_examples.json")) as f:
+        return json.load(f)["examples"]
+
+
+@pytest.mark.parametrize("ex", _golden(), ids=lambda e: e["name"])
+def test_worked_examples(ex):
+    W = np.array(ex["W"], dtype=np.float64)
+    b = oracle.build_pifa(W, ex["r"])
+    assert b["select_order"].tolist() == ex["select_order"]
+    assert b["pivot_idx"].tolist() == ex["pivot_idx"]
+    assert b["nonpivot_idx"].tolist() == ex["nonpivot_idx"]
+    np.testing.assert_array_equal(b["Wp"], np.array(ex["Wp"], dtype=np.float64))
+    np.testing.assert_allclose(b["C"], np.array(ex["C"], dtype=np.float64), rtol=0, atol=1e-14)
+
+
+# ---------------------------------------------------------------- degenerate inputs
+def test_rank_too_low_is_rejected():
+    """U with a repeated column makes rank(W') = r - 1 < r."""
+    U, V = inputs.lowrank_factors(64, 64, 8, 3)
+    U[:, 1] = U[:, 0]
+    V[1] = V[0]
+    with pytest.raises(oracle.OracleRankError):
+        oracle.build_pifa(U @ V, 8)
+
+
+def test_rank_too_high_is_rejected():
+    W = np.random.default_rng(0).standard_normal((40, 30))
+    with pytest.raises(oracle.OracleRankError):
+        oracle.build_pifa(W, 10)
+
+
+def test_zero_matrix_is_rejected():
+    with pytest.raises(oracle.OracleRankError):
+        oracle.build_pifa(np.zeros((5, 4)), 1)
+
+
+def test_full_rank_r_equals_d_out():
+    """r = d_out: C is empty and Y is a column permutation of X W_p^T."""
+    U, V, W = _layer(32, 48, 32)
+    b = oracle.build_pifa(W, 32)
+    assert b["C"].shape == (0, 32) and b["nonpivot_idx"].size == 0
+    X = inputs.activations(4, 48, 5)
+    Y = oracle.pifa_forward(X, b["pivot_idx"], b["nonpivot_idx"], b["Wp"], b["C"])
+    assert _rel(Y, X @ W.T) <= 1e-12
+
+
+def test_integer_matrix_build_is_exact():
+    """A rank-2 integer matrix whose rows are small integer combinations of two
+    rows: C comes out with those integer coefficients."""
+    base = np.array([[1.0, 2.0, 0.0, -1.0], [0.0, 1.0, 3.0, 1.0]])
+    coeffs = np.array([[1, 0], [0, 1], [2, -1], [-3, 1], [1, 1]], dtype=np.float64)
+    W = coeffs @ base
+    b = oracle.build_pifa(W, 2)
+    # reconstruct coefficients for every row from the chosen pivots
+    piv = b["pivot_idx"]
+    Cfull = np.linalg.lstsq(W[piv].T, W.T, rcond=None)[0].T
+    np.testing.assert_allclose(b["C"], Cfull[b["nonpivot_idx"]], atol=1e-12)
+    assert oracle.reconstruction_error(W, piv, b["nonpivot_idx"], b["Wp"], b["C"]) <= 1e-14
+
+
+# ---------------------------------------------------------------- forward and baselines
+def test_forward_layout_probe_exact():
+    """W_p = [I_r | 0] and one-hot C give Y[:, I[j]] = X[:, j] and
+    Y[:, I^c[k]] = X[:, (7k+3) mod r], exactly."""
+    d_in, d_out, r, M = 40, 56, 24, 6
+    Wp, C = inputs.layout_probe_layer(d_in, d_out, r)
+    piv, npiv = inputs.random_partition(d_out, r, 3)
+    X = inputs.layout_probe_activations(M, d_in, 1)
+    Y = oracle.pifa_forward(X, piv, npiv, Wp, C)
+    assert np.array_equal(Y[:, piv], X[:, :r])
+    k = np.arange(d_out - r)
+    assert np.array_equal(Y[:, npiv], X[:, (7 * k + 3) % r])
+
+
+def test_forward_uses_given_index_order():
+    """Alg. PIFA Layer writes Y_p's column j to output column I[j]: an
+    unsorted partition must be honoured as given."""
+    d_in, d_out, r = 10, 9, 4
+    Wp, C = inputs.layout_probe_layer(d_in, d_out, r)
+    piv = np.array([7, 0, 5, 2], np.int32)
+    npiv = np.array([8, 1, 6, 3, 4], np.int32)
+    X = inputs.layout_probe_activations(3, d_in, 2)
+    Y = oracle.pifa_forward(X, piv, npiv, Wp, C)
+    assert np.array_equal(Y[:, piv], X[:, :r])
+
+
+def test_dense_and_lowrank_match_numpy():
+    rng = np.random.default_rng(5)
+    X = rng.standard_normal((7, 33))
+    U = rng.standard_normal((29, 5))
+    V = rng.standard_normal((5, 33))
+    W = U @ V
+    assert _rel(oracle.dense_forward(X, W), X @ W.T) <= 1e-13
+    assert _rel(oracle.lowrank_forward(X, U, V), (X @ V.T) @ U.T) <= 1e-13
+
+
+def test_config_a_matches_dense():
+    """fp32 256x256, r = 128 layer: the PIFA forward on the built layer equals
+    dense X W^T in fp64 (the losslessness claim of Sec. 3.2)."""
+    U, V = inputs.lowrank_factors(256, 256, 128, inputs.config_seed(0))
+    W = U @ V
+    b = oracle.build_pifa(W, 128)
+    X = inputs.activations(32, 256, inputs.config_seed(0))
+    Y = oracle.pifa_forward(X, b["pivot_idx"], b["nonpivot_idx"], b["Wp"], b["C"])
+    assert _rel(Y, oracle.dense_forward(X, W)) <= 1e-12
+    assert _rel(Y, oracle.lowrank_forward(X, U, V)) <= 1e-12
+
+
+def test_forward_is_pivot_set_invariant():
+    """Two different valid pivot sets of the same W' give the same Y."""
+    U, V, W = _layer(120, 90, 40, 4)
+    b = oracle.build_pifa(W, 40)
+    # a second pivot set: the last 40 rows (generic U makes them independent)
+    piv2 = np.arange(80, 120, dtype=np.int32)
+    npiv2 = np.arange(0, 80, dtype=np.int32)
+    C2 = np.linalg.solve(U[piv2].T, U[npiv2].T).T
+    X = inputs.activations(5, 90, 8)
+    Y1 = oracle.pifa_forward(X, b["pivot_idx"], b["nonpivot_idx"], b["Wp"], b["C"])
+    Y2 = oracle.pifa_forward(X, piv2, npiv2, W[piv2], C2)
+    assert _rel(Y1, Y2) <= 1e-10
+
+
+def test_threads_do_not_change_results():
+    U, V, W = _layer(200, 150, 60, 12)
+    b1 = oracle.build_pifa(W, 60, threads=1)
+    b4 = oracle.build_pifa(W, 60, threads=4)
+    assert np.array_equal(b1["pivot_idx"], b4["pivot_idx"])
+    assert np.array_equal(b1["C"], b4["C"])
+    X = inputs.activations(9, 150, 1)
+    y1 = oracle.pifa_forward(X, b1["pivot_idx"], b1["nonpivot_idx"], b1["Wp"], b1["C"], threads=1)
+    y4 = oracle.pifa_forward(X, b1["pivot_idx"], b1["nonpivot_idx"], b1["Wp"], b1["C"], threads=4)
+    assert np.array_equal(y1, y4)
+
+
+# ---------------------------------------------------------------- planted mistakes
+def _pins_fail(W, U, piv, npiv, Wp, C):
+    """True if any of the pins used above rejects this (mutated) layer."""
+    X = inputs.activations(4, W.shape[1], 77)
+    bad_forward = _rel(oracle.pifa_forward(X, piv, npiv, Wp, C), X @ W.T) > 1e-10
+    bad_recon = oracle.reconstruction_error(W, piv, npiv, Wp, C) > 1e-10
+    closed = np.linalg.solve(U[piv].T, U[npiv].T).T
+    bad_closed = _rel(C, closed) > 1e-9
+    return bad_forward and bad_recon and bad_closed
+
+
+def test_planted_mistakes_are_caught():
+    U, V, W = _layer(64, 64, 32, 21)
+    b = oracle.build_pifa(W, 32)
+    piv, npiv, Wp, C = b["pivot_idx"], b["nonpivot_idx"], b["Wp"], b["C"]
+    assert not _pins_fail(W, U, piv, npiv, Wp, C)
+    # transposed coefficient matrix (square case)
+    assert _pins_fail(W, U, piv, npiv, Wp, C.T.copy())
+    # sign error in one column of C
+    Cs = C.copy(); Cs[:, 3] *= -1
+    assert _pins_fail(W, U, piv, npiv, Wp, Cs)
+    # C columns in selection order instead of sorted order
+    order = b["select_order"]
+    pos = {int(p): i for i, p in enumerate(piv)}
+    Csel = C[:, [pos[int(p)] for p in order]]
+    assert _pins_fail(W, U, piv, npiv, Wp, Csel)
+    # dropped term: C missing its largest-magnitude column
+    Cd = C.copy(); Cd[:, np.argmax(np.abs(C).sum(0))] = 0
+    assert _pins_fail(W, U, piv, npiv, Wp, Cd)
+    # off-by-one in the non-pivot index set
+    npiv_shift = np.roll(npiv, 1)
+    X = inputs.activations(4, 64, 77)
+    assert _rel(oracle.pifa_forward(X, piv, npiv_shift, Wp, C), X @ W.T) > 1e-3
+
+
+# ---------------------------------------------------------------- input rounding
+def test_bf16_rounding_matches_torch():
+    """The generator's fp32 -> bf16 rounding is round-to-nearest-even, as
+    torch's conversion is."""
+    import torch
+    rng = np.random.default_rng(3)
+    x = np.concatenate([rng.standard_normal(10000).astype(np.float32),
+                        np.array([1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -1.0 - 2 ** -8, 0.0, -0.0,
+                                  np.inf, -np.inf, 3.0e38], dtype=np.float32)])
+    ours = inputs.f32_bits_to_bf16_bits(x)
+    ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(ours, ref)
