@@ -1,0 +1,167 @@
+/*
+ * libpifa -- PIFA (Pivoting Factorization) linear layer forward on MI355X.
+ *
+ * Method: Zhao, Zhang & Cannistraci, "Pivoting Factorization: A Compact Meta
+ * Low-Rank Representation of Sparsity for Efficient Inference in Large
+ * Language Models", arXiv 2501.19090.
+ *
+ * A rank-r weight W (d_out x d_in) is stored as its r pivot rows W_p
+ * (r x d_in), the coefficient matrix C ((d_out - r) x r) with non-pivot rows
+ * W_np = C W_p (Sec. 3.2, eq. wnp), and the pivot / non-pivot row index sets
+ * I and I^c.  The layer forward (Algorithm "PIFA Layer") is
+ *     Y_p = X W_p^T,   Y_np = Y_p C^T,   Y[:, I] = Y_p,   Y[:, I^c] = Y_np
+ * written here for row-major activations X (M x d_in) and outputs Y
+ * (M x d_out): the paper's row index sets of W become column positions of Y.
+ *
+ * Conventions for every entry point:
+ *   - Matrices are dense, row-major, contiguous, with no padding between rows.
+ *   - "device" pointers are HIP device memory on the current device;
+ *     "host" pointers are ordinary host memory.
+ *   - Element type is given by a pifa_dtype: PIFA_BF16 (bfloat16 storage,
+ *     fp32 accumulation) or PIFA_F32.  X, Y and the weights share the dtype.
+ *   - bf16 requires d_in to be a multiple of 8 (16-byte rows); f32 accepts
+ *     any d_in.
+ *   - `stream` is a hipStream_t passed as void*; NULL means the default stream.
+ *   - No entry point throws.  Arguments are validated synchronously and a
+ *     status is returned; a kernel fault surfaces at the caller's next
+ *     synchronisation.  NaN and Inf in the inputs propagate to the outputs.
+ *   - Indices are 0-based int32 (the paper's are 1-based sets).
+ */
+#ifndef PIFA_H
+#define PIFA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { PIFA_F32 = 0, PIFA_BF16 = 1 } pifa_dtype;
+
+typedef enum {
+    PIFA_OK = 0,
+    PIFA_ERR_INVALID_ARG = -1, /* null pointer, bad size or dtype        */
+    PIFA_ERR_BAD_INDEX = -2,   /* index out of range, duplicate, or the  */
+                               /* two sets do not partition [0, d_out)   */
+    PIFA_ERR_UNSUPPORTED = -3, /* a shape or alignment this build lacks  */
+    PIFA_ERR_HIP = -4,         /* a HIP runtime call or launch failed    */
+    PIFA_ERR_OOM = -5          /* device memory allocation failed        */
+} pifa_status;
+
+/* Layer shape: W is d_out x d_in with rank r, 1 <= r <= min(d_in, d_out)
+ * (Sec. 3.3 assumes r < min(m, n) for the memory saving; r = d_out is
+ * accepted and gives an empty C). */
+typedef struct {
+    int64_t d_in;
+    int64_t d_out;
+    int64_t r;
+} pifa_dims;
+
+typedef struct pifa_layer* pifa_handle;
+typedef struct lowrank_layer* lowrank_handle;
+
+/* Human-readable name of a status code (static storage, never NULL). */
+const char* pifa_status_string(pifa_status s);
+
+/*
+ * Host-only check that pivot_idx (r entries) and nonpivot_idx (d_out - r
+ * entries) are in range, free of duplicates and together cover [0, d_out)
+ * exactly (Algorithm "Pivoting Factorization": I^c = {1..m} \ I).  Any order
+ * is accepted.  Needs no GPU.  Returns PIFA_OK, PIFA_ERR_INVALID_ARG (bad
+ * dims or null pointer) or PIFA_ERR_BAD_INDEX.
+ */
+pifa_status pifa_validate_partition(const int32_t* pivot_idx, const int32_t* nonpivot_idx,
+                                    pifa_dims dims);
+
+/*
+ * Create a PIFA layer from the output of Algorithm "Pivoting Factorization".
+ *   W_p           device, r x d_in, dtype.  Row j is the weight row that
+ *                 produces output column pivot_idx[j].
+ *   C             device, (d_out - r) x r, dtype; may be NULL when r = d_out.
+ *                 Row k produces output column nonpivot_idx[k]; its columns
+ *                 follow the row order of W_p.
+ *   pivot_idx     host, r entries; nonpivot_idx host, d_out - r entries
+ *                 (may be NULL when r = d_out).  Validated as by
+ *                 pifa_validate_partition.
+ * The layer copies everything it needs into memory it owns (W_p padded to a
+ * multiple of 64 rows; for bf16, C converted exactly to fp16 with a
+ * power-of-two scale), so the caller may free its buffers on return.
+ * Synchronises the device.  On success *out holds the handle.
+ */
+pifa_status pifa_layer_create(const void* W_p, const void* C, const int32_t* pivot_idx,
+                              const int32_t* nonpivot_idx, pifa_dims dims, pifa_dtype dtype,
+                              pifa_handle* out);
+
+/* Release a layer and its device memory (synchronises the device). NULL is OK. */
+pifa_status pifa_layer_destroy(pifa_handle h);
+
+/*
+ * Pre-size the layer's workspace for forwards of up to max_M rows, so that
+ * later pifa_forward calls allocate nothing.  Synchronises the device.
+ */
+pifa_status pifa_layer_reserve(pifa_handle h, int64_t max_M);
+
+/*
+ * Algorithm "PIFA Layer": Y[:, I] = X W_p^T and Y[:, I^c] = (X W_p^T) C^T.
+ *   X  device, M x d_in, dtype, borrowed (read only).
+ *   Y  device, M x d_out, dtype; every element is written.
+ * M = 0 returns PIFA_OK without launching.  Asynchronous on `stream`.
+ * The layer's workspace holds the intermediate Y_p, so calls on one handle
+ * must not overlap (use one handle per concurrent stream).  If M exceeds the
+ * reserved size the workspace grows, which synchronises `stream`.
+ * bf16: Y_p is handed from the first to the second product as fp16 times
+ * 2^s (s = 0 unless set by pifa_layer_set_intermediate_scale); a |Y_p * 2^s|
+ * above 65504 cannot be represented, is counted (pifa_layer_overflow_count)
+ * and produces non-finite outputs in that row.
+ */
+pifa_status pifa_forward(pifa_handle h, const void* X, void* Y, int64_t M, void* stream);
+
+/* Bytes of weights and indices a forward must read: r*d_in + (d_out-r)*r
+ * elements of the dtype plus d_out int32 indices (Sec. 3.3 memory cost). */
+size_t pifa_layer_weight_bytes(pifa_handle h);
+
+/* Set the power-of-two exponent s applied to Y_p before its fp16 hand-off
+ * (bf16 layers only; -30 <= s <= 30). */
+pifa_status pifa_layer_set_intermediate_scale(pifa_handle h, int log2_scale);
+
+/* Number of Y_p elements that overflowed fp16 since creation (synchronises
+ * the device).  Always 0 for f32 layers. */
+pifa_status pifa_layer_overflow_count(pifa_handle h, int64_t* count);
+
+/*
+ * Dense baseline (Sec. 3.3, 2 m n b FLOPs): Y = X W^T.
+ *   W device d_out x d_in; X device M x d_in; Y device M x d_out.
+ * Uses the library's shared workspace for M <= 16: calls on different
+ * streams must not overlap.
+ */
+pifa_status dense_forward(const void* W, const void* X, void* Y, int64_t M, int64_t d_in,
+                          int64_t d_out, pifa_dtype dtype, void* stream);
+
+/*
+ * Low-rank baseline (Sec. 3.3, 2 b r (m + n) FLOPs): Y = (X V^T) U^T, i.e. the
+ * paper's U (V^T X) for row-major activations.
+ *   U device d_out x r; V device r x d_in; X device M x d_in; Y device M x d_out.
+ * The intermediate X V^T goes through the library's shared workspace (calls
+ * on different streams must not overlap).  bf16 requires r to be a multiple
+ * of 8 here (PIFA_ERR_UNSUPPORTED otherwise); lowrank_layer_create accepts
+ * any r.
+ */
+pifa_status lowrank_uv_forward(const void* U, const void* V, const void* X, void* Y, int64_t M,
+                               pifa_dims dims, pifa_dtype dtype, void* stream);
+
+/* Low-rank baseline with weights prepacked once (U padded to a multiple of 64
+ * columns), the like-for-like counterpart of pifa_layer_create.  U and V are
+ * device buffers as for lowrank_uv_forward; they are copied. */
+pifa_status lowrank_layer_create(const void* U, const void* V, pifa_dims dims, pifa_dtype dtype,
+                                 lowrank_handle* out);
+pifa_status lowrank_layer_forward(lowrank_handle h, const void* X, void* Y, int64_t M,
+                                  void* stream);
+pifa_status lowrank_layer_reserve(lowrank_handle h, int64_t max_M);
+pifa_status lowrank_layer_destroy(lowrank_handle h);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PIFA_H */

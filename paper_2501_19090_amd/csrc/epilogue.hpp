@@ -1,0 +1,85 @@
+// Epilogues shared by every GEMM/GEMV kernel.
+//
+// A kernel produces fp32 values acc(m, n) of a product with N columns and
+// hands each one to the epilogue, which
+//   * writes round(acc * out_scale) to out[m * ldo + idx[n]] for n < n_out
+//     (idx == nullptr means the identity map) -- this is the pivot /
+//     non-pivot assignment of Algorithm "PIFA Layer" (its last two steps),
+//     fused into the producing kernel so there is no separate permutation pass;
+//   * optionally keeps a workspace copy ws[m * ldws + n] for n < n_ws, as fp16
+//     times ws_scale (the bf16 path's Y_p hand-off) or as fp32.
+#pragma once
+
+#include "common.hpp"
+
+namespace pifa {
+
+enum WsKind { kWsNone = 0, kWsF16 = 1, kWsF32 = 2 };
+
+template <typename TOut, int WS>
+struct ScatterEpi {
+    TOut* out;
+    int64_t ldo;
+    const int32_t* idx;  // nullptr: column n goes to output column n
+    int64_t n_out;
+    float out_scale;
+    void* ws;
+    int64_t ldws;
+    int64_t n_ws;
+    float ws_scale;
+    int* overflow;  // fp16 hand-off overflow counter
+    int64_t M;
+
+    struct Col {
+        int64_t n;
+        int64_t dst;
+        bool out_ok;
+        bool ws_ok;
+    };
+
+    __device__ __forceinline__ Col col(int64_t n) const {
+        Col c;
+        c.n = n;
+        c.out_ok = n < n_out;
+        c.dst = c.out_ok ? (idx ? (int64_t)idx[n] : n) : 0;
+        c.ws_ok = (WS != kWsNone) && n < n_ws;
+        return c;
+    }
+
+    __device__ __forceinline__ void store(int64_t m, const Col& c, float v) const {
+        if (m >= M) return;
+        if (c.out_ok) Store<TOut>::put(out + m * ldo + c.dst, v * out_scale);
+        if constexpr (WS == kWsF16) {
+            if (c.ws_ok) {
+                const float s = v * ws_scale;
+                const f16 h = (f16)s;
+                if (!__builtin_isfinite((float)h) && __builtin_isfinite(s)) atomicAdd(overflow, 1);
+                reinterpret_cast<f16*>(ws)[m * ldws + c.n] = h;
+            }
+        } else if constexpr (WS == kWsF32) {
+            if (c.ws_ok) reinterpret_cast<float*>(ws)[m * ldws + c.n] = v;
+        }
+    }
+};
+
+template <typename TOut, int WS>
+__host__ inline ScatterEpi<TOut, WS> make_epi(TOut* out, int64_t ldo, const int32_t* idx,
+                                              int64_t n_out, float out_scale, void* ws,
+                                              int64_t ldws, int64_t n_ws, float ws_scale,
+                                              int* overflow, int64_t M) {
+    ScatterEpi<TOut, WS> e;
+    e.out = out;
+    e.ldo = ldo;
+    e.idx = idx;
+    e.n_out = n_out;
+    e.out_scale = out_scale;
+    e.ws = ws;
+    e.ldws = ldws;
+    e.n_ws = n_ws;
+    e.ws_scale = ws_scale;
+    e.overflow = overflow;
+    e.M = M;
+    return e;
+}
+
+}  // namespace pifa

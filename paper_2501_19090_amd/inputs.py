@@ -157,3 +157,24 @@ def integer_layer(d_in: int, d_out: int, r: int, M: int, seed: int, density: flo
         cols = rng.choice(r, size=nnz_c, replace=False)
         C[k, cols] = rng.choice([-1.0, 1.0], size=nnz_c)
     return X, Wp, C
+
+
+# --------------------------------------------------------------------------
+# the workloads: LLaMA layer shapes with synthetic values
+# --------------------------------------------------------------------------
+# name -> (config index, layer index, d_in, d_out, r, dtype, M values, layer kind)
+# layer kind "built": (I, W_p, C) come from the PIFA build of U V;
+#            "direct": drawn by direct_layer (shapes whose build takes minutes).
+RANK_SWEEP = (0.1, 0.2, 0.3, 0.4, 0.5, 0.6, 0.7, 0.8, 0.9)
+
+CONFIGS = {
+    "A_f32_256": (0, 0, 256, 256, 128, "f32", (32,), "built"),
+    "B_attn_4096": (1, 0, 4096, 4096, 2048, "bf16", (1, 16, 128, 2048, 4096), "built"),
+    "C_mlp_up_4096x11008": (2, 0, 4096, 11008, 2048, "bf16", (1, 4096), "built"),
+    "C_mlp_down_11008x4096": (2, 1, 11008, 4096, 2048, "bf16", (1, 4096), "built"),
+    "D_70b_sq_8192": (3, 0, 8192, 8192, 4096, "bf16", (1, 4096), "direct"),
+    "D_70b_up_8192x28672": (3, 1, 8192, 28672, 4096, "bf16", (1, 4096), "direct"),
+}
+for _i, _rho in enumerate(RANK_SWEEP):
+    CONFIGS["E_sweep_r%02d" % round(100 * _rho)] = (4, _i, 4096, 4096, int(round(_rho * 4096)), "bf16",
+                                                    (1, 4096), "built")

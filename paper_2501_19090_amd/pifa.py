@@ -1,0 +1,260 @@
+"""Thin ctypes binding of libpifa (include/pifa.h).
+
+Argument marshalling only: every function has the name of the C entry point
+it calls, takes torch tensors for device buffers (or numpy arrays for host
+index arrays) and raises :class:`PifaError` on a non-OK status.  All compute
+runs in the HIP library; if it is missing, loading raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+import threading
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libpifa.so")
+HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "pifa.h")
+
+PIFA_F32 = 0
+PIFA_BF16 = 1
+
+PIFA_OK = 0
+PIFA_ERR_INVALID_ARG = -1
+PIFA_ERR_BAD_INDEX = -2
+PIFA_ERR_UNSUPPORTED = -3
+PIFA_ERR_HIP = -4
+PIFA_ERR_OOM = -5
+
+
+class pifa_dims(ctypes.Structure):
+    _fields_ = [("d_in", ctypes.c_int64), ("d_out", ctypes.c_int64), ("r", ctypes.c_int64)]
+
+
+class PifaError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        self.status = status
+        super().__init__("%s failed: %s" % (fn, pifa_status_string(status)))
+
+
+_lock = threading.Lock()
+_lib = None
+
+_vp = ctypes.c_void_p
+_i64 = ctypes.c_int64
+_i32p = ctypes.POINTER(ctypes.c_int32)
+_st = ctypes.c_int
+
+_SIGNATURES = {
+    "pifa_status_string": (ctypes.c_char_p, [_st]),
+    "pifa_validate_partition": (_st, [_i32p, _i32p, pifa_dims]),
+    "pifa_layer_create": (_st, [_vp, _vp, _i32p, _i32p, pifa_dims, ctypes.c_int, ctypes.POINTER(_vp)]),
+    "pifa_layer_destroy": (_st, [_vp]),
+    "pifa_layer_reserve": (_st, [_vp, _i64]),
+    "pifa_forward": (_st, [_vp, _vp, _vp, _i64, _vp]),
+    "pifa_layer_weight_bytes": (ctypes.c_size_t, [_vp]),
+    "pifa_layer_set_intermediate_scale": (_st, [_vp, ctypes.c_int]),
+    "pifa_layer_overflow_count": (_st, [_vp, ctypes.POINTER(_i64)]),
+    "dense_forward": (_st, [_vp, _vp, _vp, _i64, _i64, _i64, ctypes.c_int, _vp]),
+    "lowrank_uv_forward": (_st, [_vp, _vp, _vp, _vp, _i64, pifa_dims, ctypes.c_int, _vp]),
+    "lowrank_layer_create": (_st, [_vp, _vp, pifa_dims, ctypes.c_int, ctypes.POINTER(_vp)]),
+    "lowrank_layer_forward": (_st, [_vp, _vp, _vp, _i64, _vp]),
+    "lowrank_layer_reserve": (_st, [_vp, _i64]),
+    "lowrank_layer_destroy": (_st, [_vp]),
+}
+
+
+def lib():
+    """Open libpifa.so (raises if it has not been built)."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise RuntimeError("libpifa.so not built: run `python -m paper_2501_19090_amd.build`")
+            handle = ctypes.CDLL(LIB_PATH)
+            for name, (res, args) in _SIGNATURES.items():
+                fn = getattr(handle, name)
+                fn.restype = res
+                fn.argtypes = args
+            _lib = handle
+        return _lib
+
+
+def declared_symbols(header: str = HEADER_PATH):
+    """Function names declared in include/pifa.h."""
+    with open(header) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b([a-z_][a-z0-9_]*)\s*\(", text)) - {"defined"})
+
+
+# ---------------------------------------------------------------- marshalling
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.bfloat16:
+        return PIFA_BF16
+    if t.dtype == torch.float32:
+        return PIFA_F32
+    raise TypeError("unsupported dtype %s (bf16 or fp32)" % t.dtype)
+
+
+def _dev_ptr(t, name: str) -> int | None:
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("%s must be a device tensor" % name)
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    return t.data_ptr()
+
+
+def _host_i32(a):
+    if a is None:
+        return None, None
+    arr = np.ascontiguousarray(np.asarray(a), dtype=np.int32)
+    return arr, arr.ctypes.data_as(_i32p)
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    return int(getattr(stream, "cuda_stream", stream))
+
+
+def _check(fn: str, status: int):
+    if status != PIFA_OK:
+        raise PifaError(fn, status)
+
+
+# ---------------------------------------------------------------- entry points
+def pifa_status_string(status: int) -> str:
+    return lib().pifa_status_string(int(status)).decode()
+
+
+def pifa_validate_partition(pivot_idx, nonpivot_idx, dims) -> int:
+    """Returns the status code (no exception): PIFA_OK or the error."""
+    piv, pp = _host_i32(pivot_idx)
+    npv, npp = _host_i32(nonpivot_idx)
+    return int(lib().pifa_validate_partition(pp, npp, pifa_dims(*dims)))
+
+
+def pifa_layer_create(W_p, C, pivot_idx, nonpivot_idx, dims, dtype: int | None = None) -> int:
+    """dims = (d_in, d_out, r); returns an opaque handle."""
+    dt = _dtype_code(W_p) if dtype is None else int(dtype)
+    piv, pp = _host_i32(pivot_idx)
+    npv, npp = _host_i32(nonpivot_idx)
+    out = _vp()
+    _check("pifa_layer_create", lib().pifa_layer_create(
+        _dev_ptr(W_p, "W_p"), _dev_ptr(C, "C"), pp, npp, pifa_dims(*dims), dt, ctypes.byref(out)))
+    return out.value
+
+
+def pifa_layer_destroy(handle: int) -> None:
+    _check("pifa_layer_destroy", lib().pifa_layer_destroy(handle))
+
+
+def pifa_layer_reserve(handle: int, max_M: int) -> None:
+    _check("pifa_layer_reserve", lib().pifa_layer_reserve(handle, int(max_M)))
+
+
+def pifa_forward(handle: int, X, Y, M: int | None = None, stream=None) -> None:
+    M = X.shape[0] if M is None else int(M)
+    _check("pifa_forward", lib().pifa_forward(handle, _dev_ptr(X, "X"), _dev_ptr(Y, "Y"), M,
+                                              _stream(stream)))
+
+
+def pifa_layer_weight_bytes(handle: int) -> int:
+    return int(lib().pifa_layer_weight_bytes(handle))
+
+
+def pifa_layer_set_intermediate_scale(handle: int, log2_scale: int) -> None:
+    _check("pifa_layer_set_intermediate_scale",
+           lib().pifa_layer_set_intermediate_scale(handle, int(log2_scale)))
+
+
+def pifa_layer_overflow_count(handle: int) -> int:
+    out = _i64()
+    _check("pifa_layer_overflow_count", lib().pifa_layer_overflow_count(handle, ctypes.byref(out)))
+    return int(out.value)
+
+
+def dense_forward(W, X, Y, M: int | None = None, d_in: int | None = None, d_out: int | None = None,
+                  dtype: int | None = None, stream=None) -> None:
+    M = X.shape[0] if M is None else int(M)
+    d_in = W.shape[1] if d_in is None else int(d_in)
+    d_out = W.shape[0] if d_out is None else int(d_out)
+    dt = _dtype_code(W) if dtype is None else int(dtype)
+    _check("dense_forward", lib().dense_forward(_dev_ptr(W, "W"), _dev_ptr(X, "X"), _dev_ptr(Y, "Y"),
+                                                M, d_in, d_out, dt, _stream(stream)))
+
+
+def lowrank_uv_forward(U, V, X, Y, M: int | None = None, dims=None, dtype: int | None = None,
+                       stream=None) -> None:
+    M = X.shape[0] if M is None else int(M)
+    dims = (V.shape[1], U.shape[0], U.shape[1]) if dims is None else dims
+    dt = _dtype_code(U) if dtype is None else int(dtype)
+    _check("lowrank_uv_forward", lib().lowrank_uv_forward(
+        _dev_ptr(U, "U"), _dev_ptr(V, "V"), _dev_ptr(X, "X"), _dev_ptr(Y, "Y"), M, pifa_dims(*dims),
+        dt, _stream(stream)))
+
+
+def lowrank_layer_create(U, V, dims=None, dtype: int | None = None) -> int:
+    dims = (V.shape[1], U.shape[0], U.shape[1]) if dims is None else dims
+    dt = _dtype_code(U) if dtype is None else int(dtype)
+    out = _vp()
+    _check("lowrank_layer_create", lib().lowrank_layer_create(
+        _dev_ptr(U, "U"), _dev_ptr(V, "V"), pifa_dims(*dims), dt, ctypes.byref(out)))
+    return out.value
+
+
+def lowrank_layer_forward(handle: int, X, Y, M: int | None = None, stream=None) -> None:
+    M = X.shape[0] if M is None else int(M)
+    _check("lowrank_layer_forward", lib().lowrank_layer_forward(
+        handle, _dev_ptr(X, "X"), _dev_ptr(Y, "Y"), M, _stream(stream)))
+
+
+def lowrank_layer_reserve(handle: int, max_M: int) -> None:
+    _check("lowrank_layer_reserve", lib().lowrank_layer_reserve(handle, int(max_M)))
+
+
+def lowrank_layer_destroy(handle: int) -> None:
+    _check("lowrank_layer_destroy", lib().lowrank_layer_destroy(handle))
+
+
+# ---------------------------------------------------------------- convenience
+class PifaLayer:
+    """Owns a pifa_handle; ``layer(X)`` allocates Y and runs pifa_forward."""
+
+    def __init__(self, W_p, C, pivot_idx, nonpivot_idx, d_out: int):
+        self.d_in = int(W_p.shape[1])
+        self.r = int(W_p.shape[0])
+        self.d_out = int(d_out)
+        self.dtype = W_p.dtype
+        self.handle = pifa_layer_create(W_p, C, pivot_idx, nonpivot_idx, (self.d_in, self.d_out, self.r))
+
+    def __call__(self, X, Y=None, stream=None):
+        import torch
+        if Y is None:
+            Y = torch.empty((X.shape[0], self.d_out), dtype=X.dtype, device=X.device)
+        pifa_forward(self.handle, X, Y, X.shape[0], stream)
+        return Y
+
+    def close(self):
+        if self.handle:
+            pifa_layer_destroy(self.handle)
+            self.handle = 0
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,126 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol the
+header declares, and rejects bad arguments before touching the device."""
+import ctypes
+
+import numpy as np
+import pytest
+
+from paper_2501_19090_amd import pifa
+
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
+
+
+def test_library_exports_every_declared_symbol():
+    declared = pifa.declared_symbols()
+    assert "pifa_layer_create" in declared and "pifa_forward" in declared
+    assert "dense_forward" in declared and "lowrank_uv_forward" in declared
+    lib = pifa.lib()
+    missing = [s for s in declared if not hasattr(lib, s)]
+    assert not missing, missing
+    # the binding wraps every declared entry point under the same name
+    assert not [s for s in declared if not hasattr(pifa, s)]
+
+
+def test_status_strings():
+    for code, name in [(0, "PIFA_OK"), (-1, "PIFA_ERR_INVALID_ARG"), (-2, "PIFA_ERR_BAD_INDEX"),
+                       (-3, "PIFA_ERR_UNSUPPORTED"), (-4, "PIFA_ERR_HIP"), (-5, "PIFA_ERR_OOM")]:
+        assert pifa.pifa_status_string(code) == name
+    assert pifa.pifa_status_string(7) == "PIFA_ERR_UNKNOWN"
+
+
+def _perm_split(d_out, r, seed=0):
+    perm = np.random.default_rng(seed).permutation(d_out).astype(np.int32)
+    return perm[:r], perm[r:]
+
+
+def test_validate_partition_accepts_any_order():
+    piv, npiv = _perm_split(50, 20)
+    assert pifa.pifa_validate_partition(piv, npiv, (30, 50, 20)) == pifa.PIFA_OK
+    assert pifa.pifa_validate_partition(np.sort(piv), np.sort(npiv), (30, 50, 20)) == pifa.PIFA_OK
+    # r = d_out: empty complement
+    assert pifa.pifa_validate_partition(np.arange(8), None, (8, 8, 8)) == pifa.PIFA_OK
+
+
+@pytest.mark.parametrize("mutate", ["dup", "range_hi", "range_lo", "overlap"])
+def test_validate_partition_rejects_bad_indices(mutate):
+    piv, npiv = _perm_split(40, 15, 3)
+    piv, npiv = piv.copy(), npiv.copy()
+    if mutate == "dup":
+        piv[1] = piv[0]
+    elif mutate == "range_hi":
+        npiv[0] = 40
+    elif mutate == "range_lo":
+        piv[2] = -1
+    elif mutate == "overlap":
+        npiv[0] = piv[0]
+    assert pifa.pifa_validate_partition(piv, npiv, (16, 40, 15)) == pifa.PIFA_ERR_BAD_INDEX
+
+
+@pytest.mark.parametrize("dims", [(0, 10, 1), (10, 0, 1), (10, 10, 0), (10, 10, 11), (5, 10, 6),
+                                  (10, 5, 6), (-1, 4, 1)])
+def test_validate_partition_rejects_bad_dims(dims):
+    piv = np.arange(max(dims[2], 1), dtype=np.int32)
+    assert pifa.pifa_validate_partition(piv, piv, dims) == pifa.PIFA_ERR_INVALID_ARG
+
+
+def test_validate_partition_null_pointers():
+    lib = pifa.lib()
+    assert lib.pifa_validate_partition(None, None, pifa.pifa_dims(4, 4, 2)) == pifa.PIFA_ERR_INVALID_ARG
+    piv = np.arange(4, dtype=np.int32)
+    # r = d_out needs no complement
+    assert lib.pifa_validate_partition(piv.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), None,
+                                       pifa.pifa_dims(4, 4, 4)) == pifa.PIFA_OK
+
+
+def _create(Wp, C, piv, npiv, dims, dtype):
+    out = ctypes.c_void_p()
+    pp = None if piv is None else np.ascontiguousarray(piv, np.int32).ctypes.data_as(
+        ctypes.POINTER(ctypes.c_int32))
+    npp = None if npiv is None else np.ascontiguousarray(npiv, np.int32).ctypes.data_as(
+        ctypes.POINTER(ctypes.c_int32))
+    st = pifa.lib().pifa_layer_create(Wp, C, pp, npp, pifa.pifa_dims(*dims), dtype, ctypes.byref(out))
+    return st, out.value
+
+
+def test_create_rejects_before_device_work():
+    piv, npiv = _perm_split(64, 16)
+    ok_dims = (64, 64, 16)
+    # null output handle pointer
+    assert pifa.lib().pifa_layer_create(FAKE, FAKE, None, None, pifa.pifa_dims(*ok_dims),
+                                        pifa.PIFA_BF16, None) == pifa.PIFA_ERR_INVALID_ARG
+    # bad dtype
+    assert _create(FAKE, FAKE, piv, npiv, ok_dims, 7)[0] == pifa.PIFA_ERR_INVALID_ARG
+    # null weights / missing C with r < d_out
+    assert _create(None, FAKE, piv, npiv, ok_dims, pifa.PIFA_BF16)[0] == pifa.PIFA_ERR_INVALID_ARG
+    assert _create(FAKE, None, piv, npiv, ok_dims, pifa.PIFA_BF16)[0] == pifa.PIFA_ERR_INVALID_ARG
+    # bf16 rows must be 16-byte multiples
+    assert _create(FAKE, FAKE, piv, npiv, (60, 64, 16), pifa.PIFA_BF16)[0] == pifa.PIFA_ERR_UNSUPPORTED
+    # bad partition
+    bad = npiv.copy(); bad[0] = piv[0]
+    st, h = _create(FAKE, FAKE, piv, bad, ok_dims, pifa.PIFA_BF16)
+    assert st == pifa.PIFA_ERR_BAD_INDEX and h is None
+    # rank larger than a dimension
+    assert _create(FAKE, FAKE, piv, npiv, (8, 64, 16), pifa.PIFA_F32)[0] == pifa.PIFA_ERR_INVALID_ARG
+
+
+def test_forward_and_baselines_reject_bad_args():
+    lib = pifa.lib()
+    assert lib.pifa_forward(None, FAKE, FAKE, 4, None) == pifa.PIFA_ERR_INVALID_ARG
+    assert lib.pifa_layer_destroy(None) == pifa.PIFA_OK
+    assert lib.pifa_layer_weight_bytes(None) == 0
+    assert lib.dense_forward(FAKE, FAKE, FAKE, -1, 8, 8, pifa.PIFA_BF16, None) == pifa.PIFA_ERR_INVALID_ARG
+    assert lib.dense_forward(FAKE, FAKE, FAKE, 4, 8, 8, 9, None) == pifa.PIFA_ERR_INVALID_ARG
+    assert lib.dense_forward(None, FAKE, FAKE, 4, 8, 8, pifa.PIFA_BF16, None) == pifa.PIFA_ERR_INVALID_ARG
+    assert lib.dense_forward(FAKE, FAKE, FAKE, 4, 12, 8, pifa.PIFA_BF16, None) == pifa.PIFA_ERR_UNSUPPORTED
+    # M = 0 is a no-op that succeeds without a device
+    assert lib.dense_forward(FAKE, FAKE, FAKE, 0, 8, 8, pifa.PIFA_BF16, None) == pifa.PIFA_OK
+    assert lib.lowrank_uv_forward(FAKE, FAKE, FAKE, FAKE, 0, pifa.pifa_dims(8, 8, 4), pifa.PIFA_BF16,
+                                  None) == pifa.PIFA_OK
+    assert lib.lowrank_uv_forward(FAKE, FAKE, FAKE, FAKE, 4, pifa.pifa_dims(8, 8, 9), pifa.PIFA_BF16,
+                                  None) == pifa.PIFA_ERR_INVALID_ARG
+    assert lib.lowrank_uv_forward(FAKE, FAKE, FAKE, FAKE, 4, pifa.pifa_dims(16, 16, 4), pifa.PIFA_BF16,
+                                  None) == pifa.PIFA_ERR_UNSUPPORTED
+    assert lib.lowrank_layer_forward(None, FAKE, FAKE, 4, None) == pifa.PIFA_ERR_INVALID_ARG
+    assert lib.lowrank_layer_destroy(None) == pifa.PIFA_OK
+    assert lib.pifa_layer_set_intermediate_scale(None, 0) == pifa.PIFA_ERR_INVALID_ARG
+    assert lib.pifa_layer_overflow_count(None, None) == pifa.PIFA_ERR_INVALID_ARG
