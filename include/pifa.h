@@ -60,6 +60,7 @@ typedef struct {
 
 typedef struct pifa_layer* pifa_handle;
 typedef struct lowrank_layer* lowrank_handle;
+typedef struct dense_layer* dense_handle;
 
 /* Human-readable name of a status code (static storage, never NULL). */
 const char* pifa_status_string(pifa_status s);
@@ -84,9 +85,10 @@ pifa_status pifa_validate_partition(const int32_t* pivot_idx, const int32_t* non
  *   pivot_idx     host, r entries; nonpivot_idx host, d_out - r entries
  *                 (may be NULL when r = d_out).  Validated as by
  *                 pifa_validate_partition.
- * The layer copies everything it needs into memory it owns (W_p padded to a
- * multiple of 64 rows; for bf16, C converted exactly to fp16 with a
- * power-of-two scale), so the caller may free its buffers on return.
+ * The layer copies everything it needs into memory it owns, so the caller may
+ * free its buffers on return.  bf16 layers reorder W_p and C into 16 x 128
+ * blocks in MFMA operand order (rows padded to a multiple of 64 with zeros)
+ * and convert C exactly to fp16 with a power-of-two scale.
  * Synchronises the device.  On success *out holds the handle.
  */
 pifa_status pifa_layer_create(const void* W_p, const void* C, const int32_t* pivot_idx,
@@ -132,11 +134,19 @@ pifa_status pifa_layer_overflow_count(pifa_handle h, int64_t* count);
 /*
  * Dense baseline (Sec. 3.3, 2 m n b FLOPs): Y = X W^T.
  *   W device d_out x d_in; X device M x d_in; Y device M x d_out.
- * Uses the library's shared workspace for M <= 16: calls on different
- * streams must not overlap.
+ * Reads the caller's row-major W directly (no workspace).
  */
 pifa_status dense_forward(const void* W, const void* X, void* Y, int64_t M, int64_t d_in,
                           int64_t d_out, pifa_dtype dtype, void* stream);
+
+/* Dense baseline with W prepacked once into the same weight layout the PIFA
+ * layer uses (the like-for-like counterpart of pifa_layer_create).  W is a
+ * device buffer as for dense_forward; it is copied.  Synchronises on create
+ * and destroy. */
+pifa_status dense_layer_create(const void* W, int64_t d_in, int64_t d_out, pifa_dtype dtype,
+                               dense_handle* out);
+pifa_status dense_layer_forward(dense_handle h, const void* X, void* Y, int64_t M, void* stream);
+pifa_status dense_layer_destroy(dense_handle h);
 
 /*
  * Low-rank baseline (Sec. 3.3, 2 b r (m + n) FLOPs): Y = (X V^T) U^T, i.e. the
@@ -150,8 +160,9 @@ pifa_status dense_forward(const void* W, const void* X, void* Y, int64_t M, int6
 pifa_status lowrank_uv_forward(const void* U, const void* V, const void* X, void* Y, int64_t M,
                                pifa_dims dims, pifa_dtype dtype, void* stream);
 
-/* Low-rank baseline with weights prepacked once (U padded to a multiple of 64
- * columns), the like-for-like counterpart of pifa_layer_create.  U and V are
+/* Low-rank baseline with weights prepacked once into the PIFA layer's weight
+ * layout (r padded to a multiple of 64), the like-for-like counterpart of
+ * pifa_layer_create.  U and V are
  * device buffers as for lowrank_uv_forward; they are copied. */
 pifa_status lowrank_layer_create(const void* U, const void* V, pifa_dims dims, pifa_dtype dtype,
                                  lowrank_handle* out);
@@ -159,6 +170,21 @@ pifa_status lowrank_layer_forward(lowrank_handle h, const void* X, void* Y, int6
                                   void* stream);
 pifa_status lowrank_layer_reserve(lowrank_handle h, int64_t max_M);
 pifa_status lowrank_layer_destroy(lowrank_handle h);
+
+/*
+ * Per-kernel timing.  While enabled, every kernel the library launches for a
+ * forward is bracketed by a pair of HIP events recorded on the launch stream
+ * (they add no synchronisation).  pifa_profile_read synchronises on the
+ * recorded events and returns, per launch site, the number of launches and
+ * their summed duration in milliseconds since the last reset; sites with no
+ * launches are omitted.  names[i] points to static storage.  Returns the
+ * number of sites written through *n_sites (at most max_sites).
+ * Not thread-safe against concurrent forwards on other host threads.
+ */
+pifa_status pifa_profile_enable(int on);
+pifa_status pifa_profile_reset(void);
+pifa_status pifa_profile_read(const char** names, int64_t* launches, double* total_ms, int max_sites,
+                              int* n_sites);
 
 #ifdef __cplusplus
 }

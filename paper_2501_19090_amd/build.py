@@ -26,6 +26,18 @@ def sources():
     return [os.path.join(CSRC, "pifa.hip")]
 
 
+def source_digest() -> str:
+    """sha256 over the kernel and ABI sources (identifies a kernel version)."""
+    import hashlib
+    h = hashlib.sha256()
+    files = sorted(f for f in os.listdir(CSRC) if f.endswith((".hip", ".hpp")))
+    for f in files + ["../../include/pifa.h"]:
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(f.encode())
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
 def build(verbose: bool = False) -> str:
     """Always recompile (this is the build check); returns the library path."""
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -5,16 +5,23 @@
 // supplies 8 consecutive K values of one row.  Used for X W_p^T (bf16),
 // Y_p C^T (fp16 operands) and the dense / low-rank baselines.
 //
-// Block tile BM x BN, K step BK, staged through LDS with double buffering:
-// global loads for step k+1 are in flight while step k runs on MFMA.  Rows
-// are padded by 16 bytes in LDS so the 16-byte operand reads of 32 lanes
-// (32 rows, same K offset) spread over all banks.  Ragged M / N / K are
-// handled by buffer-resource range checks (out-of-range loads return 0) and
-// a K mask, so any M, N and any K that is a multiple of 8 work.
+// Block tile BM x BN, K step BK, staged through LDS with double buffering,
+// 8 waves (2 per SIMD) each owning a 64 x 64 sub-tile of 32x32x16 MFMAs.
+// Global loads run PGR tiles ahead through registers; the LDS write of the
+// next tile is issued right after the first MFMA group of the current one,
+// and operand fragments for MFMA step kk+1 are read from LDS while step kk
+// runs, so the matrix cores rarely wait on memory.  Rows are padded by 16
+// bytes in LDS so the 16-byte operand reads of 32 lanes (32 rows, same K
+// offset) spread over all banks (no bank conflicts were counted).  Ragged M / N / K are
+// handled by buffer-resource range checks (out-of-range loads return 0; a
+// masked lane is given an offset past the range), so any M, N and any K that
+// is a multiple of 8 work.  B is either
+// row-major (row stride ldb) or in the lane order of layout.hpp (BPACK).
 #pragma once
 
 #include "common.hpp"
 #include "epilogue.hpp"
+#include "layout.hpp"
 
 namespace pifa {
 
@@ -67,20 +74,34 @@ __device__ __forceinline__ void tile_coords(int64_t bid, int64_t tiles_m, int64_
     tn = in_band / rows;
 }
 
-template <typename T, int BM, int BN, int BK, int WM, int WN, typename Epi>
+// Offset past every buffer range: the load returns 0 without a branch.
+constexpr uint32_t kMaskedOffset = 0x80000000u;
+
+// Buffer resource whose range stays below kMaskedOffset.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc31(const void* base, int64_t bytes) {
+    const uint32_t n = bytes <= 0 ? 0u : (bytes >= 0x7FFFFFFFll ? 0x7FFFFFFFu : (uint32_t)bytes);
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, 0x00020000);
+}
+
+template <typename T, int BM, int BN, int BK, int WM, int WN, bool BPACK, int PGR, typename Epi>
 __global__ __launch_bounds__(WM* WN* kWave) void gemm_nt_mfma(const T* __restrict__ A, int64_t lda,
                                                              int64_t M, const T* __restrict__ B,
                                                              int64_t ldb, int64_t N, int64_t K,
                                                              Epi epi) {
     constexpr int NT = WM * WN * kWave;
-    constexpr int LDK = BK + 8;   // padded LDS row, in elements
-    constexpr int CPR = BK / 8;   // 16-byte chunks per tile row
+    constexpr int LDK = BK + 8;  // padded LDS row, in elements
+    constexpr int CPR = BK / 8;  // 16-byte chunks per tile row
     constexpr int A_CH = BM * CPR / NT;
     constexpr int B_CH = BN * CPR / NT;
     constexpr int WTM = BM / WM, WTN = BN / WN;
     constexpr int TM = WTM / 32, TN = WTN / 32;
+    constexpr int KK = BK / 16;
+    constexpr int CPG = 2 * BK;  // packed: chunks of one 16-row group inside a tile
+    constexpr int LPC = BK / 2;  // packed: lanes per MFMA slice inside a tile
     static_assert(BM * CPR % NT == 0 && BN * CPR % NT == 0, "tile does not split over threads");
-    static_assert(WTM % 32 == 0 && WTN % 32 == 0 && BK % 16 == 0, "bad warp tile");
+    static_assert(WTM % 32 == 0 && WTN % 32 == 0 && KK >= 2, "bad warp tile");
+    static_assert(!BPACK || ((BK == 64 || BK == 128) && BN % kPackRows == 0), "bad packed tile");
+    static_assert(PGR == 1 || PGR == 2, "prefetch depth");
 
     __shared__ __attribute__((aligned(16))) T As[2][BM * LDK];
     __shared__ __attribute__((aligned(16))) T Bs[2][BN * LDK];
@@ -90,80 +111,110 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_nt_mfma(const T* __restric
     tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn);
     const int64_t m0 = tm * BM, n0 = tn * BN;
 
-    const auto ars = make_rsrc(A + m0 * lda, ((M - m0 - 1) * lda + K) * (int64_t)sizeof(T));
-    const auto brs = make_rsrc(B + n0 * ldb, ((N - n0 - 1) * ldb + K) * (int64_t)sizeof(T));
+    const auto ars = make_rsrc31(A + m0 * lda, ((M - m0 - 1) * lda + K) * (int64_t)sizeof(T));
+    const int64_t KB = packed_kblocks(K);
+    const auto brs = BPACK ? make_rsrc31(B + (n0 / kPackRows) * KB * (kPackChunks * 8),
+                                         (packed_groups(N) - n0 / kPackRows) * KB * kPackChunks * 16)
+                           : make_rsrc31(B + n0 * ldb, ((N - n0 - 1) * ldb + K) * (int64_t)sizeof(T));
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
     const int wave = tid / kWave;
     const int wm = wave / WN, wn = wave % WN;
 
-    u32x4 ra[A_CH], rb[B_CH];
-    auto gload = [&](int64_t k0) {
+    struct Stage {
+        u32x4 a[A_CH], b[B_CH];
+        int blds[B_CH];  // LDS element offset of each B chunk
+    };
+    Stage S[PGR];
+    auto gload = [&](int64_t k0, Stage& R) {
 #pragma unroll
         for (int i = 0; i < A_CH; ++i) {
-            const int c = tid + i * NT;
-            const int row = c / CPR;
+            const int c = tid + i * NT, row = c / CPR;
             const int64_t k = k0 + (c % CPR) * 8;
-            ra[i] = k < K ? load16(ars, (uint32_t)((row * lda + k) * (int64_t)sizeof(T))) : zero16();
+            R.a[i] = load16(ars, k < K ? (uint32_t)((row * lda + k) * (int64_t)sizeof(T)) : kMaskedOffset);
         }
+        if constexpr (BPACK) {
+            const int64_t blk = k0 / kPackCols;
+            const int hsel = (int)((k0 % kPackCols) / BK);
 #pragma unroll
-        for (int i = 0; i < B_CH; ++i) {
-            const int c = tid + i * NT;
-            const int row = c / CPR;
-            const int64_t k = k0 + (c % CPR) * 8;
-            rb[i] = k < K ? load16(brs, (uint32_t)((row * ldb + k) * (int64_t)sizeof(T))) : zero16();
+            for (int i = 0; i < B_CH; ++i) {
+                const int cid = tid + i * NT, gl = cid / CPG, rem = cid % CPG;
+                const int c = rem / LPC, l = hsel * LPC + rem % LPC;
+                R.b[i] = load16(brs, (uint32_t)((((gl * KB + blk) * 4 + c) * 64 + l) * 16));
+                R.blds[i] = (gl * kPackRows + (l & 15)) * LDK + (4 * ((l >> 4) - hsel * (LPC / 16)) + c) * 8;
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < B_CH; ++i) {
+                const int c = tid + i * NT, row = c / CPR;
+                const int64_t k = k0 + (c % CPR) * 8;
+                R.b[i] = load16(brs, k < K ? (uint32_t)((row * ldb + k) * (int64_t)sizeof(T)) : kMaskedOffset);
+                R.blds[i] = row * LDK + (c % CPR) * 8;
+            }
         }
     };
-    auto sstore = [&](int buf) {
+    auto sstore = [&](int buf, const Stage& R) {
 #pragma unroll
         for (int i = 0; i < A_CH; ++i) {
             const int c = tid + i * NT;
-            *reinterpret_cast<u32x4*>(&As[buf][(c / CPR) * LDK + (c % CPR) * 8]) = ra[i];
+            *reinterpret_cast<u32x4*>(&As[buf][(c / CPR) * LDK + (c % CPR) * 8]) = R.a[i];
         }
 #pragma unroll
-        for (int i = 0; i < B_CH; ++i) {
-            const int c = tid + i * NT;
-            *reinterpret_cast<u32x4*>(&Bs[buf][(c / CPR) * LDK + (c % CPR) * 8]) = rb[i];
-        }
+        for (int i = 0; i < B_CH; ++i) *reinterpret_cast<u32x4*>(&Bs[buf][R.blds[i]]) = R.b[i];
     };
 
     f32x16 acc[TM][TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
+        for (int j = 0; j < TN; ++j) acc[i][j] = f32x16{};
+
+    // 32x32x16 operands: lane supplies row (lane % 32), K values 8*(lane/32) .. +7
+    const int frag_row = lane & 31, frag_k = (lane >> 5) * 8;
+    u32x4 fa[2][TM], fb[2][TN];
+    auto lds_frag = [&](int buf, int kk, int slot) {
+        const T* as = &As[buf][(wm * WTM + frag_row) * LDK + frag_k + kk * 16];
+        const T* bs = &Bs[buf][(wn * WTN + frag_row) * LDK + frag_k + kk * 16];
 #pragma unroll
-            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+        for (int i = 0; i < TM; ++i) fa[slot][i] = *reinterpret_cast<const u32x4*>(as + i * 32 * LDK);
+#pragma unroll
+        for (int j = 0; j < TN; ++j) fb[slot][j] = *reinterpret_cast<const u32x4*>(bs + j * 32 * LDK);
+    };
 
     const int64_t nk = ceil_div(K, BK);
-    gload(0);
-    sstore(0);
+    // Tile t is staged in S[t % PGR].  Before iteration kt the LDS buffer
+    // (kt & 1) holds tile kt and tiles kt+1 .. kt+PGR are in flight.
+    gload(0, S[0]);
+    if (PGR == 2 && nk > 1) gload(BK, S[PGR - 1]);
+    sstore(0, S[0]);
+    if (nk > PGR) gload((int64_t)PGR * BK, S[0]);
     __syncthreads();
-
-    const int frag_row = lane & 31;
-    const int frag_k = (lane >> 5) * 8;
-    for (int64_t kt = 0; kt < nk; ++kt) {
+    lds_frag(0, 0, 0);
+    auto body = [&](int64_t kt, Stage& nxt) {  // nxt = S[(kt + 1) % PGR]
         const int cur = (int)(kt & 1);
-        if (kt + 1 < nk) gload((kt + 1) * BK);
-        const T* as = &As[cur][(wm * WTM + frag_row) * LDK + frag_k];
-        const T* bs = &Bs[cur][(wn * WTN + frag_row) * LDK + frag_k];
 #pragma unroll
-        for (int kk = 0; kk < BK / 16; ++kk) {
-            u32x4 af[TM], bfr[TN];
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
-                af[i] = *reinterpret_cast<const u32x4*>(as + i * 32 * LDK + kk * 16);
-#pragma unroll
-            for (int j = 0; j < TN; ++j)
-                bfr[j] = *reinterpret_cast<const u32x4*>(bs + j * 32 * LDK + kk * 16);
+        for (int kk = 0; kk < KK; ++kk) {
+            const int slot = kk & 1;
+            if (kk + 1 < KK) lds_frag(cur, kk + 1, slot ^ 1);
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
-                for (int j = 0; j < TN; ++j) acc[i][j] = Mfma<T>::mma32(af[i], bfr[j], acc[i][j]);
+                for (int j = 0; j < TN; ++j) acc[i][j] = Mfma<T>::mma32(fa[slot][i], fb[slot][j], acc[i][j]);
+            // the other LDS buffer was last read before the previous barrier
+            if (kk == 0 && kt + 1 < nk) sstore(cur ^ 1, nxt);
+            if (kk == 1 && kt + 1 + PGR < nk) gload((kt + 1 + PGR) * BK, nxt);
         }
-        if (kt + 1 < nk) sstore(cur ^ 1);
         __syncthreads();
+        if (kt + 1 < nk) lds_frag(cur ^ 1, 0, 0);
+    };
+    if constexpr (PGR == 1) {
+        for (int64_t kt = 0; kt < nk; ++kt) body(kt, S[0]);
+    } else {
+        for (int64_t kt = 0; kt < nk; kt += 2) {
+            body(kt, S[PGR - 1]);
+            if (kt + 1 < nk) body(kt + 1, S[0]);
+        }
     }
 
     // 32x32 accumulator layout: lane holds column (lane % 32) and rows

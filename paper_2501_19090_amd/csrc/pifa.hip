@@ -23,6 +23,7 @@
 #include "gemm_f32.hpp"
 #include "gemm_mfma.hpp"
 #include "gemv_skinny.hpp"
+#include "layout.hpp"
 #include "prepack.hpp"
 
 using namespace pifa;
@@ -33,10 +34,11 @@ namespace {
 constexpr int64_t kDecodeMaxM = 16;  // M at or below this takes the skinny path
 constexpr int64_t kRowPad = 64;      // W_p rows / C columns padded to this multiple
 
-constexpr int kGemmBM = 128, kGemmBN = 128, kGemmBK = 64, kGemmWM = 2, kGemmWN = 2;
-constexpr int kSkinnyWaves = 4, kSkinnyUnroll = 2;
-constexpr int64_t kSkinnyTargetWgs = 1024;
-constexpr int64_t kSkinnyMaxSplit = 16;
+// Prefill tiles: 256 x 128 (8 waves of 64 x 64, two tiles of global
+// prefetch); 128 x 128 when the large tile would leave CUs without work.
+constexpr int kGemmBK = 64;
+constexpr int64_t kCus = 256;
+constexpr int kSkinnyWaves = 8, kSkinnyUnroll = 2;
 
 #define PIFA_HIP(call)                                  \
     do {                                                \
@@ -47,69 +49,6 @@ inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s);
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 inline size_t esize(pifa_dtype dt) { return dt == PIFA_BF16 ? 2 : 4; }
 inline bool valid_dtype(pifa_dtype dt) { return dt == PIFA_BF16 || dt == PIFA_F32; }
-
-// ------------------------------------------------------------------ skinny split
-struct SkinnyPlan {
-    int64_t groups, splits, k_split;
-};
-
-SkinnyPlan skinny_plan(int64_t N, int64_t K) {
-    SkinnyPlan p;
-    p.groups = ceil_div(N, kSkinnyRows);
-    const int64_t step = (int64_t)kSkinnyWaves * kSkinnyStepK;
-    int64_t s = ceil_div(kSkinnyTargetWgs, p.groups < 1 ? 1 : p.groups);
-    const int64_t smax = ceil_div(K, step);
-    if (s > smax) s = smax;
-    if (s > kSkinnyMaxSplit) s = kSkinnyMaxSplit;
-    if (s < 1) s = 1;
-    p.k_split = round_up(ceil_div(K, s), step);
-    p.splits = ceil_div(K, p.k_split);
-    return p;
-}
-
-size_t skinny_partial_bytes(const SkinnyPlan& p) {
-    return p.splits > 1 ? (size_t)(p.groups * p.splits) * kWave * sizeof(f32x4) : 0;
-}
-
-// Scratch for the split-K reduction of the skinny kernel.  Counters start at
-// zero and every launch leaves them at zero.
-struct SplitScratch {
-    float* partials = nullptr;
-    size_t partial_bytes = 0;
-    int* counters = nullptr;
-    size_t n_counters = 0;
-
-    pifa_status ensure(const SkinnyPlan& p, hipStream_t st) {
-        const size_t pb = skinny_partial_bytes(p);
-        const size_t nc = (size_t)p.groups;
-        if (pb <= partial_bytes && nc <= n_counters) return PIFA_OK;
-        PIFA_HIP(hipStreamSynchronize(st));
-        if (pb > partial_bytes) {
-            if (partials) PIFA_HIP(hipFree(partials));
-            partials = nullptr;
-            partial_bytes = 0;
-            if (hipMalloc(&partials, pb) != hipSuccess) return PIFA_ERR_OOM;
-            partial_bytes = pb;
-        }
-        if (nc > n_counters) {
-            if (counters) PIFA_HIP(hipFree(counters));
-            counters = nullptr;
-            n_counters = 0;
-            if (hipMalloc(&counters, nc * sizeof(int)) != hipSuccess) return PIFA_ERR_OOM;
-            PIFA_HIP(hipMemset(counters, 0, nc * sizeof(int)));
-            PIFA_HIP(hipDeviceSynchronize());
-            n_counters = nc;
-        }
-        return PIFA_OK;
-    }
-    void release() {
-        if (partials) (void)hipFree(partials);
-        if (counters) (void)hipFree(counters);
-        partials = nullptr;
-        counters = nullptr;
-        partial_bytes = n_counters = 0;
-    }
-};
 
 // A device buffer that only grows; growing waits for `st` first so no kernel
 // in flight still uses the old allocation.
@@ -133,57 +72,177 @@ struct GrowBuf {
     }
 };
 
+// ------------------------------------------------------------------ kernel timing
+enum Site {
+    kSitePifaGemm1 = 0,
+    kSitePifaGemm2,
+    kSitePifaGemv1,
+    kSitePifaGemv2,
+    kSitePifaF32Gemm1,
+    kSitePifaF32Gemm2,
+    kSiteDenseGemm,
+    kSiteDenseGemv,
+    kSiteDenseF32,
+    kSiteLowrankGemm1,
+    kSiteLowrankGemm2,
+    kSiteLowrankGemv1,
+    kSiteLowrankGemv2,
+    kSiteLowrankF32,
+    kSiteCount
+};
+
+const char* const kSiteNames[kSiteCount] = {
+    "pifa_gemm1_xwp",      "pifa_gemm2_ypc",      "pifa_gemv1_xwp",      "pifa_gemv2_ypc",
+    "pifa_f32_gemm1",      "pifa_f32_gemm2",      "dense_gemm",          "dense_gemv",
+    "dense_f32",           "lowrank_gemm1_xv",    "lowrank_gemm2_tu",    "lowrank_gemv1_xv",
+    "lowrank_gemv2_tu",    "lowrank_f32"};
+
+struct Profiler {
+    std::mutex mu;
+    bool on = false;
+    struct Rec {
+        int site;
+        hipEvent_t start, stop;
+    };
+    std::vector<Rec> pending;
+    std::vector<hipEvent_t> pool;
+    int64_t launches[kSiteCount] = {};
+    double ms[kSiteCount] = {};
+
+    hipEvent_t get() {
+        if (!pool.empty()) {
+            hipEvent_t e = pool.back();
+            pool.pop_back();
+            return e;
+        }
+        hipEvent_t e = nullptr;
+        if (hipEventCreate(&e) != hipSuccess) return nullptr;
+        return e;
+    }
+};
+
+Profiler& profiler() {
+    static Profiler p;
+    return p;
+}
+
+// Brackets one launch with events when profiling is on.
+struct TimedLaunch {
+    int site;
+    hipStream_t st;
+    hipEvent_t start = nullptr, stop = nullptr;
+    TimedLaunch(int s, hipStream_t stream) : site(s), st(stream) {
+        Profiler& p = profiler();
+        if (!p.on) return;
+        std::lock_guard<std::mutex> g(p.mu);
+        start = p.get();
+        stop = p.get();
+        if (start) (void)hipEventRecord(start, st);
+    }
+    ~TimedLaunch() {
+        if (!start || !stop) return;
+        Profiler& p = profiler();
+        (void)hipEventRecord(stop, st);
+        std::lock_guard<std::mutex> g(p.mu);
+        p.pending.push_back({site, start, stop});
+    }
+};
+
 // ------------------------------------------------------------------ launchers
-template <typename T, typename Epi>
-hipError_t launch_gemm(const T* A, int64_t lda, int64_t M, const T* B, int64_t ldb, int64_t N,
-                       int64_t K, Epi epi, hipStream_t st) {
-    const int64_t tiles = ceil_div(M, kGemmBM) * ceil_div(N, kGemmBN);
-    if (tiles == 0) return hipSuccess;
-    hipLaunchKernelGGL((gemm_nt_mfma<T, kGemmBM, kGemmBN, kGemmBK, kGemmWM, kGemmWN, Epi>),
-                       dim3((unsigned)tiles), dim3(kGemmWM * kGemmWN * kWave), 0, st, A, lda, M, B,
-                       ldb, N, K, epi);
+template <typename T, bool BPACK, typename Epi>
+hipError_t launch_gemm(int site, const T* A, int64_t lda, int64_t M, const T* B, int64_t ldb,
+                       int64_t N, int64_t K, Epi epi, hipStream_t st) {
+    if (M == 0 || N == 0) return hipSuccess;
+    TimedLaunch timed(site, st);
+    const int64_t big = ceil_div(M, 256) * ceil_div(N, 128);
+    if (big >= kCus) {
+        hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 128, kGemmBK, 4, 2, BPACK, 2, Epi>), dim3((unsigned)big),
+                           dim3(8 * kWave), 0, st, A, lda, M, B, ldb, N, K, epi);
+    } else {
+        const int64_t small = ceil_div(M, 128) * ceil_div(N, 128);
+        hipLaunchKernelGGL((gemm_nt_mfma<T, 128, 128, kGemmBK, 4, 2, BPACK, 2, Epi>), dim3((unsigned)small),
+                           dim3(8 * kWave), 0, st, A, lda, M, B, ldb, N, K, epi);
+    }
     return hipGetLastError();
 }
 
 template <typename Epi>
-hipError_t launch_gemm_f32(const float* A, int64_t lda, int64_t M, const float* B, int64_t ldb,
-                           int64_t N, int64_t K, Epi epi, hipStream_t st) {
+hipError_t launch_gemm_f32(int site, const float* A, int64_t lda, int64_t M, const float* B,
+                           int64_t ldb, int64_t N, int64_t K, Epi epi, hipStream_t st) {
     if (M == 0 || N == 0) return hipSuccess;
+    TimedLaunch timed(site, st);
     hipLaunchKernelGGL((gemm_nt_f32<Epi>), dim3((unsigned)ceil_div(N, 64), (unsigned)ceil_div(M, 64)),
                        dim3(256), 0, st, A, lda, M, B, ldb, N, K, epi);
     return hipGetLastError();
 }
 
+// B in lane order (layout.hpp), logical N x K.
 template <typename TB, typename AL, typename Epi>
-hipError_t launch_skinny(AL al, const TB* B, int64_t ldb, int64_t N, int64_t K,
-                         const SplitScratch& sc, Epi epi, hipStream_t st) {
-    const SkinnyPlan p = skinny_plan(N, K);
-    if (p.groups == 0) return hipSuccess;
-    hipLaunchKernelGGL((skinny_mfma<TB, kSkinnyWaves, kSkinnyUnroll, AL, Epi>),
-                       dim3((unsigned)p.groups, (unsigned)p.splits), dim3(kSkinnyWaves * kWave), 0, st,
-                       al, B, ldb, N, K, p.k_split, sc.partials, sc.counters, epi);
+hipError_t launch_skinny_packed(int site, AL al, const TB* B, int64_t N, int64_t K, Epi epi,
+                                hipStream_t st) {
+    const int64_t groups = packed_groups(N);
+    if (groups == 0) return hipSuccess;
+    TimedLaunch timed(site, st);
+    hipLaunchKernelGGL((skinny_packed<TB, kSkinnyWaves, kSkinnyUnroll, AL, Epi>), dim3((unsigned)groups),
+                       dim3(kSkinnyWaves * kWave), 0, st, al, B, N, K, epi);
     return hipGetLastError();
 }
 
-hipError_t launch_pack_bits(const void* src, int64_t rows, int64_t cols, int64_t ld, void* dst,
-                            int64_t rows_pad, int64_t cols_pad, size_t elem, hipStream_t st) {
-    const int64_t total = rows_pad * cols_pad;
-    if (total == 0) return hipSuccess;
-    const unsigned blocks = (unsigned)std::min<int64_t>(ceil_div(total, 256), 65536);
-    if (elem == 2)
-        hipLaunchKernelGGL((pack_pad<uint16_t>), dim3(blocks), dim3(256), 0, st,
-                           (const uint16_t*)src, rows, cols, ld, (uint16_t*)dst, rows_pad, cols_pad);
-    else
-        hipLaunchKernelGGL((pack_pad<float>), dim3(blocks), dim3(256), 0, st, (const float*)src, rows,
-                           cols, ld, (float*)dst, rows_pad, cols_pad);
+// B row-major with row stride ldb.
+template <typename TB, typename AL, typename Epi>
+hipError_t launch_skinny_rowmajor(int site, AL al, const TB* B, int64_t ldb, int64_t N, int64_t K,
+                                  Epi epi, hipStream_t st) {
+    const int64_t groups = ceil_div(N, kSkinnyRows);
+    if (groups == 0) return hipSuccess;
+    TimedLaunch timed(site, st);
+    hipLaunchKernelGGL((skinny_rowmajor<TB, kSkinnyWaves, kSkinnyUnroll, AL, Epi>), dim3((unsigned)groups),
+                       dim3(kSkinnyWaves * kWave), 0, st, al, B, ldb, N, K, epi);
     return hipGetLastError();
+}
+
+unsigned grid_for(int64_t work) { return (unsigned)std::max<int64_t>(1, std::min<int64_t>(ceil_div(work, 256), 65536)); }
+
+// Row-major copy with zero padding (fp32 layers keep row-major weights).
+hipError_t pack_rowmajor_f32(const void* src, int64_t rows, int64_t cols, void* dst, int64_t rows_pad,
+                             int64_t cols_pad) {
+    if (rows_pad * cols_pad == 0) return hipSuccess;
+    hipLaunchKernelGGL((pack_pad<float>), dim3(grid_for(rows_pad * cols_pad)), dim3(256), 0, 0,
+                       (const float*)src, rows, cols, cols, (float*)dst, rows_pad, cols_pad);
+    return hipGetLastError();
+}
+
+// bf16 rows x cols -> lane order of a rows_log x cols_log matrix (bf16).
+hipError_t pack_lane_bf16(const void* src, int64_t rows, int64_t cols, void* dst, int64_t rows_log,
+                          int64_t cols_log) {
+    const int64_t chunks = packed_groups(rows_log) * packed_kblocks(cols_log) * kPackChunks;
+    if (chunks == 0) return hipSuccess;
+    hipLaunchKernelGGL((pack_lane_order<uint16_t, uint16_t>), dim3(grid_for(chunks)), dim3(256), 0, 0,
+                       (const uint16_t*)src, rows, cols, cols, (uint16_t*)dst, rows_log, cols_log, 1.f);
+    return hipGetLastError();
+}
+
+// Largest finite |x| of a bf16 device array (synchronous).
+pifa_status absmax_bf16_host(const void* src, int64_t n, float* out) {
+    unsigned* dmax = nullptr;
+    if (hipMalloc(&dmax, sizeof(unsigned)) != hipSuccess) return PIFA_ERR_OOM;
+    unsigned bits = 0;
+    bool ok = hipMemset(dmax, 0, sizeof(unsigned)) == hipSuccess;
+    if (ok && n > 0) {
+        hipLaunchKernelGGL(absmax_bf16, dim3((unsigned)std::min<int64_t>(ceil_div(n, 256), 4096)), dim3(256),
+                           0, 0, (const uint16_t*)src, n, dmax);
+        ok = hipGetLastError() == hipSuccess;
+    }
+    ok = ok && hipMemcpy(&bits, dmax, sizeof(unsigned), hipMemcpyDeviceToHost) == hipSuccess;
+    (void)hipFree(dmax);
+    if (!ok) return PIFA_ERR_HIP;
+    *out = __builtin_bit_cast(float, bits << 16);
+    return PIFA_OK;
 }
 
 // ------------------------------------------------------------------ shared workspace
 struct DeviceScratch {
     std::mutex mu;
     GrowBuf inter;  // intermediate X V^T of the stateless low-rank baseline
-    SplitScratch split;
 };
 
 DeviceScratch& device_scratch(int dev) {
@@ -209,28 +268,35 @@ pifa_status check_rows_aligned(pifa_dtype dt, int64_t d_in) {
 }  // namespace
 
 // ===================================================================== handles
+// bf16 layers keep their weights in lane order (layout.hpp); fp32 layers keep
+// row-major copies for the vector-ALU kernels.
 struct pifa_layer {
     int device = 0;
     pifa_dtype dtype = PIFA_BF16;
     int64_t d_in = 0, d_out = 0, r = 0, n_np = 0, r_pad = 0;
-    void* Wp = nullptr;        // bf16: r_pad x d_in, rows >= r zero; f32: r x d_in
-    void* C = nullptr;         // bf16: fp16 n_np x r_pad times 2^c_log2; f32: n_np x r
+    void* Wp = nullptr;        // bf16: lane order of r_pad x d_in; f32: r x d_in
+    void* C = nullptr;         // bf16: fp16 lane order of n_np x r_pad, times 2^c_log2; f32: n_np x r
     int32_t* piv = nullptr;    // r
     int32_t* npiv = nullptr;   // n_np
     int* overflow = nullptr;
     int c_log2 = 0, y_log2 = 0;
     GrowBuf ws;                // Y_p hand-off
-    SplitScratch split;
 };
 
 struct lowrank_layer {
     int device = 0;
     pifa_dtype dtype = PIFA_BF16;
     int64_t d_in = 0, d_out = 0, r = 0, r_pad = 0;
-    void* U = nullptr;  // d_out x r_pad, columns >= r zero
-    void* V = nullptr;  // r_pad x d_in, rows >= r zero
+    void* U = nullptr;  // bf16: lane order of d_out x r_pad; f32: d_out x r
+    void* V = nullptr;  // bf16: lane order of r_pad x d_in; f32: r x d_in
     GrowBuf ws;
-    SplitScratch split;
+};
+
+struct dense_layer {
+    int device = 0;
+    pifa_dtype dtype = PIFA_BF16;
+    int64_t d_in = 0, d_out = 0;
+    void* W = nullptr;  // bf16: lane order of d_out x d_in; f32: d_out x d_in
 };
 
 namespace {
@@ -243,7 +309,6 @@ void free_layer(pifa_layer* h) {
     if (h->npiv) (void)hipFree(h->npiv);
     if (h->overflow) (void)hipFree(h->overflow);
     h->ws.release();
-    h->split.release();
     delete h;
 }
 
@@ -252,7 +317,12 @@ void free_lowrank(lowrank_layer* h) {
     if (h->U) (void)hipFree(h->U);
     if (h->V) (void)hipFree(h->V);
     h->ws.release();
-    h->split.release();
+    delete h;
+}
+
+void free_dense(dense_layer* h) {
+    if (!h) return;
+    if (h->W) (void)hipFree(h->W);
     delete h;
 }
 
@@ -262,35 +332,27 @@ size_t pifa_ws_bytes(const pifa_layer* h, int64_t M) {
     return (size_t)M * (size_t)h->r_pad * 2;
 }
 
-pifa_status pifa_prepare(pifa_layer* h, int64_t M, hipStream_t st) {
-    pifa_status s = h->ws.ensure(pifa_ws_bytes(h, M), st);
-    if (s != PIFA_OK) return s;
-    if (h->dtype == PIFA_BF16 && M <= kDecodeMaxM) {
-        s = h->split.ensure(skinny_plan(h->r_pad, h->d_in), st);
-        if (s != PIFA_OK) return s;
-        if (h->n_np > 0) s = h->split.ensure(skinny_plan(h->n_np, h->r_pad), st);
-    }
-    return s;
-}
-
 size_t lowrank_ws_bytes(pifa_dtype dt, int64_t M, int64_t r_cols) {
     if (dt == PIFA_F32 || M <= kDecodeMaxM) return (size_t)M * (size_t)r_cols * 4;
     return (size_t)M * (size_t)r_cols * 2;
 }
 
-// Y = (X V^T) U^T with V: r_cols x d_in (ldv = d_in), U: d_out x r_cols (ldu = r_cols).
+// Y = (X V^T) U^T.  V: r_cols x d_in, U: d_out x r_cols, both in lane order
+// when PACKED (bf16 handle), else row-major (stateless call, fp32).
+template <bool PACKED>
 pifa_status lowrank_run(pifa_dtype dt, const void* U, const void* V, const void* X, void* Y,
                         int64_t M, int64_t d_in, int64_t d_out, int64_t r_cols, void* T,
-                        const SplitScratch& sc, hipStream_t st) {
+                        hipStream_t st) {
     hipError_t e;
     if (dt == PIFA_F32) {
         float* t = (float*)T;
-        e = launch_gemm_f32((const float*)X, d_in, M, (const float*)V, d_in, r_cols, d_in,
+        e = launch_gemm_f32(kSiteLowrankF32, (const float*)X, d_in, M, (const float*)V, d_in, r_cols,
+                            d_in,
                             make_epi<float, kWsNone>(t, r_cols, nullptr, r_cols, 1.f, nullptr, 0, 0,
                                                      1.f, nullptr, M),
                             st);
         if (e != hipSuccess) return PIFA_ERR_HIP;
-        e = launch_gemm_f32(t, r_cols, M, (const float*)U, r_cols, d_out, r_cols,
+        e = launch_gemm_f32(kSiteLowrankF32, t, r_cols, M, (const float*)U, r_cols, d_out, r_cols,
                             make_epi<float, kWsNone>((float*)Y, d_out, nullptr, d_out, 1.f, nullptr,
                                                      0, 0, 1.f, nullptr, M),
                             st);
@@ -298,29 +360,61 @@ pifa_status lowrank_run(pifa_dtype dt, const void* U, const void* V, const void*
     }
     if (M <= kDecodeMaxM) {
         float* t = (float*)T;
-        e = launch_skinny<bf16>(ALoad16<bf16>{(const bf16*)X, d_in, M}, (const bf16*)V, d_in,
-                                r_cols, d_in, sc,
-                                make_epi<float, kWsNone>(t, r_cols, nullptr, r_cols, 1.f, nullptr,
-                                                         0, 0, 1.f, nullptr, M),
-                                st);
-        if (e != hipSuccess) return PIFA_ERR_HIP;
-        e = launch_skinny<bf16>(ASplit32<bf16>{t, r_cols, M, 1.f}, (const bf16*)U, r_cols, d_out,
-                                r_cols, sc,
-                                make_epi<bf16, kWsNone>((bf16*)Y, d_out, nullptr, d_out, 1.f,
-                                                        nullptr, 0, 0, 1.f, nullptr, M),
-                                st);
+        auto e1 = make_epi<float, kWsNone>(t, r_cols, nullptr, r_cols, 1.f, nullptr, 0, 0, 1.f, nullptr, M);
+        auto e2 = make_epi<bf16, kWsNone>((bf16*)Y, d_out, nullptr, d_out, 1.f, nullptr, 0, 0, 1.f,
+                                          nullptr, M);
+        ALoad16<bf16> a1{(const bf16*)X, d_in, M};
+        ASplit32<bf16> a2{t, r_cols, M, 1.f};
+        if constexpr (PACKED) {
+            e = launch_skinny_packed<bf16>(kSiteLowrankGemv1, a1, (const bf16*)V, r_cols, d_in, e1, st);
+            if (e != hipSuccess) return PIFA_ERR_HIP;
+            e = launch_skinny_packed<bf16>(kSiteLowrankGemv2, a2, (const bf16*)U, d_out, r_cols, e2, st);
+        } else {
+            e = launch_skinny_rowmajor<bf16>(kSiteLowrankGemv1, a1, (const bf16*)V, d_in, r_cols, d_in, e1, st);
+            if (e != hipSuccess) return PIFA_ERR_HIP;
+            e = launch_skinny_rowmajor<bf16>(kSiteLowrankGemv2, a2, (const bf16*)U, r_cols, d_out, r_cols, e2,
+                                             st);
+        }
         return e == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
     }
     bf16* t = (bf16*)T;
-    e = launch_gemm<bf16>((const bf16*)X, d_in, M, (const bf16*)V, d_in, r_cols, d_in,
-                          make_epi<bf16, kWsNone>(t, r_cols, nullptr, r_cols, 1.f, nullptr, 0, 0,
-                                                  1.f, nullptr, M),
-                          st);
+    e = launch_gemm<bf16, PACKED>(kSiteLowrankGemm1, (const bf16*)X, d_in, M, (const bf16*)V, d_in,
+                                  r_cols, d_in,
+                                  make_epi<bf16, kWsNone>(t, r_cols, nullptr, r_cols, 1.f, nullptr, 0,
+                                                          0, 1.f, nullptr, M),
+                                  st);
     if (e != hipSuccess) return PIFA_ERR_HIP;
-    e = launch_gemm<bf16>(t, r_cols, M, (const bf16*)U, r_cols, d_out, r_cols,
-                          make_epi<bf16, kWsNone>((bf16*)Y, d_out, nullptr, d_out, 1.f, nullptr, 0,
-                                                  0, 1.f, nullptr, M),
-                          st);
+    e = launch_gemm<bf16, PACKED>(kSiteLowrankGemm2, t, r_cols, M, (const bf16*)U, r_cols, d_out, r_cols,
+                                  make_epi<bf16, kWsNone>((bf16*)Y, d_out, nullptr, d_out, 1.f, nullptr,
+                                                          0, 0, 1.f, nullptr, M),
+                                  st);
+    return e == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
+}
+
+// Y = X W^T; W lane order (PACKED) or row-major.
+template <bool PACKED>
+pifa_status dense_run(pifa_dtype dt, const void* W, const void* X, void* Y, int64_t M, int64_t d_in,
+                      int64_t d_out, hipStream_t st) {
+    hipError_t e;
+    if (dt == PIFA_F32) {
+        e = launch_gemm_f32(kSiteDenseF32, (const float*)X, d_in, M, (const float*)W, d_in, d_out, d_in,
+                            make_epi<float, kWsNone>((float*)Y, d_out, nullptr, d_out, 1.f, nullptr,
+                                                     0, 0, 1.f, nullptr, M),
+                            st);
+        return e == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
+    }
+    auto epi = make_epi<bf16, kWsNone>((bf16*)Y, d_out, nullptr, d_out, 1.f, nullptr, 0, 0, 1.f,
+                                       nullptr, M);
+    if (M <= kDecodeMaxM) {
+        ALoad16<bf16> a{(const bf16*)X, d_in, M};
+        if constexpr (PACKED)
+            e = launch_skinny_packed<bf16>(kSiteDenseGemv, a, (const bf16*)W, d_out, d_in, epi, st);
+        else
+            e = launch_skinny_rowmajor<bf16>(kSiteDenseGemv, a, (const bf16*)W, d_in, d_out, d_in, epi, st);
+        return e == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
+    }
+    e = launch_gemm<bf16, PACKED>(kSiteDenseGemm, (const bf16*)X, d_in, M, (const bf16*)W, d_in, d_out,
+                                  d_in, epi, st);
     return e == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
 }
 
@@ -383,7 +477,8 @@ pifa_status pifa_layer_create(const void* W_p, const void* C, const int32_t* piv
     h->d_out = dims.d_out;
     h->r = dims.r;
     h->n_np = n_np;
-    h->r_pad = dtype == PIFA_BF16 ? round_up(dims.r, kRowPad) : dims.r;
+    const bool bf = dtype == PIFA_BF16;
+    h->r_pad = bf ? round_up(dims.r, kRowPad) : dims.r;
 
     auto fail = [&](pifa_status st) {
         free_layer(h);
@@ -391,10 +486,11 @@ pifa_status pifa_layer_create(const void* W_p, const void* C, const int32_t* piv
     };
     if (hipGetDevice(&h->device) != hipSuccess) return fail(PIFA_ERR_HIP);
     if (hipDeviceSynchronize() != hipSuccess) return fail(PIFA_ERR_HIP);
-    const size_t es = esize(dtype);
 
-    if (hipMalloc(&h->Wp, (size_t)h->r_pad * h->d_in * es) != hipSuccess) return fail(PIFA_ERR_OOM);
-    if (launch_pack_bits(W_p, h->r, h->d_in, h->d_in, h->Wp, h->r_pad, h->d_in, es, 0) != hipSuccess)
+    const size_t wp_bytes = bf ? (size_t)packed_elems(h->r_pad, h->d_in) * 2 : (size_t)h->r * h->d_in * 4;
+    if (hipMalloc(&h->Wp, wp_bytes) != hipSuccess) return fail(PIFA_ERR_OOM);
+    if ((bf ? pack_lane_bf16(W_p, h->r, h->d_in, h->Wp, h->r_pad, h->d_in)
+            : pack_rowmajor_f32(W_p, h->r, h->d_in, h->Wp, h->r, h->d_in)) != hipSuccess)
         return fail(PIFA_ERR_HIP);
 
     if (hipMalloc(&h->piv, (size_t)h->r * sizeof(int32_t)) != hipSuccess) return fail(PIFA_ERR_OOM);
@@ -408,36 +504,21 @@ pifa_status pifa_layer_create(const void* W_p, const void* C, const int32_t* piv
         if (hipMemcpy(h->npiv, nonpivot_idx, (size_t)n_np * sizeof(int32_t), hipMemcpyHostToDevice) !=
             hipSuccess)
             return fail(PIFA_ERR_HIP);
-        if (hipMalloc(&h->C, (size_t)n_np * h->r_pad * es) != hipSuccess) return fail(PIFA_ERR_OOM);
-        if (dtype == PIFA_F32) {
-            if (launch_pack_bits(C, n_np, h->r, h->r, h->C, n_np, h->r, 4, 0) != hipSuccess)
-                return fail(PIFA_ERR_HIP);
+        if (!bf) {
+            if (hipMalloc(&h->C, (size_t)n_np * h->r * 4) != hipSuccess) return fail(PIFA_ERR_OOM);
+            if (pack_rowmajor_f32(C, n_np, h->r, h->C, n_np, h->r) != hipSuccess) return fail(PIFA_ERR_HIP);
         } else {
-            unsigned* dmax = nullptr;
-            if (hipMalloc(&dmax, sizeof(unsigned)) != hipSuccess) return fail(PIFA_ERR_OOM);
-            unsigned bits = 0;
-            bool ok = hipMemset(dmax, 0, sizeof(unsigned)) == hipSuccess;
-            const int64_t n = n_np * h->r;
-            if (ok) {
-                hipLaunchKernelGGL(absmax_bf16, dim3((unsigned)std::min<int64_t>(ceil_div(n, 256), 4096)),
-                                   dim3(256), 0, 0, (const uint16_t*)C, n, dmax);
-                ok = hipGetLastError() == hipSuccess &&
-                     hipMemcpy(&bits, dmax, sizeof(unsigned), hipMemcpyDeviceToHost) == hipSuccess;
-            }
-            (void)hipFree(dmax);
-            if (!ok) return fail(PIFA_ERR_HIP);
+            float mx = 0.f;
+            s = absmax_bf16_host(C, n_np * h->r, &mx);
+            if (s != PIFA_OK) return fail(s);
             // scale so that max|C| * 2^c_log2 lies in [2^14, 2^15)
             int c_log2 = 0;
-            if (bits != 0) {
-                const float mx = __builtin_bit_cast(float, bits << 16);
-                c_log2 = 14 - (int)std::floor(std::log2((double)mx));
-                c_log2 = std::max(-30, std::min(30, c_log2));
-            }
+            if (mx > 0.f) c_log2 = std::max(-30, std::min(30, 14 - (int)std::floor(std::log2((double)mx))));
             h->c_log2 = c_log2;
-            const int64_t total = n_np * h->r_pad;
-            hipLaunchKernelGGL(bf16_to_f16_scaled,
-                               dim3((unsigned)std::min<int64_t>(ceil_div(total, 256), 65536)), dim3(256),
-                               0, 0, (const uint16_t*)C, n_np, h->r, (f16*)h->C, n_np, h->r_pad,
+            const int64_t chunks = packed_groups(n_np) * packed_kblocks(h->r_pad) * kPackChunks;
+            if (hipMalloc(&h->C, (size_t)chunks * 16) != hipSuccess) return fail(PIFA_ERR_OOM);
+            hipLaunchKernelGGL((pack_lane_order<uint16_t, f16>), dim3(grid_for(chunks)), dim3(256), 0, 0,
+                               (const uint16_t*)C, n_np, h->r, h->r, (f16*)h->C, n_np, h->r_pad,
                                std::ldexp(1.0f, c_log2));
             if (hipGetLastError() != hipSuccess) return fail(PIFA_ERR_HIP);
         }
@@ -456,8 +537,8 @@ pifa_status pifa_layer_destroy(pifa_handle h) {
 
 pifa_status pifa_layer_reserve(pifa_handle h, int64_t max_M) {
     if (!h || max_M < 0) return PIFA_ERR_INVALID_ARG;
-    pifa_status s = pifa_prepare(h, max_M, 0);
-    if (s == PIFA_OK && max_M > kDecodeMaxM) s = pifa_prepare(h, kDecodeMaxM, 0);
+    const size_t need = std::max(pifa_ws_bytes(h, max_M), pifa_ws_bytes(h, std::min<int64_t>(max_M, kDecodeMaxM)));
+    pifa_status s = h->ws.ensure(need, 0);
     if (s != PIFA_OK) return s;
     return hipDeviceSynchronize() == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
 }
@@ -489,19 +570,20 @@ pifa_status pifa_forward(pifa_handle h, const void* X, void* Y, int64_t M, void*
     if (!X || !Y) return PIFA_ERR_INVALID_ARG;
     if (h->dtype == PIFA_BF16 && !aligned16(X)) return PIFA_ERR_UNSUPPORTED;
     hipStream_t st = as_stream(stream);
-    pifa_status s = pifa_prepare(h, M, st);
+    pifa_status s = h->ws.ensure(pifa_ws_bytes(h, M), st);
     if (s != PIFA_OK) return s;
     hipError_t e;
 
     if (h->dtype == PIFA_F32) {
         float* yp = (float*)h->ws.ptr;
-        e = launch_gemm_f32((const float*)X, h->d_in, M, (const float*)h->Wp, h->d_in, h->r, h->d_in,
+        e = launch_gemm_f32(kSitePifaF32Gemm1, (const float*)X, h->d_in, M, (const float*)h->Wp, h->d_in,
+                            h->r, h->d_in,
                             make_epi<float, kWsF32>((float*)Y, h->d_out, h->piv, h->r, 1.f, yp, h->r,
                                                     h->r, 1.f, nullptr, M),
                             st);
         if (e != hipSuccess) return PIFA_ERR_HIP;
         if (h->n_np > 0) {
-            e = launch_gemm_f32(yp, h->r, M, (const float*)h->C, h->r, h->n_np, h->r,
+            e = launch_gemm_f32(kSitePifaF32Gemm2, yp, h->r, M, (const float*)h->C, h->r, h->n_np, h->r,
                                 make_epi<float, kWsNone>((float*)Y, h->d_out, h->npiv, h->n_np, 1.f,
                                                          nullptr, 0, 0, 1.f, nullptr, M),
                                 st);
@@ -514,34 +596,35 @@ pifa_status pifa_forward(pifa_handle h, const void* X, void* Y, int64_t M, void*
     const float out_scale = std::ldexp(1.0f, -(h->y_log2 + h->c_log2));
     if (M <= kDecodeMaxM) {
         float* yp = (float*)h->ws.ptr;
-        e = launch_skinny<bf16>(ALoad16<bf16>{(const bf16*)X, h->d_in, M}, (const bf16*)h->Wp, h->d_in,
-                                h->r_pad, h->d_in, h->split,
-                                make_epi<bf16, kWsF32>((bf16*)Y, h->d_out, h->piv, h->r, 1.f, yp,
-                                                       h->r_pad, h->r_pad, y_scale, h->overflow, M),
-                                st);
+        e = launch_skinny_packed<bf16>(kSitePifaGemv1, ALoad16<bf16>{(const bf16*)X, h->d_in, M},
+                                       (const bf16*)h->Wp, h->r_pad, h->d_in,
+                                       make_epi<bf16, kWsF32>((bf16*)Y, h->d_out, h->piv, h->r, 1.f, yp,
+                                                              h->r_pad, h->r_pad, y_scale, h->overflow, M),
+                                       st);
         if (e != hipSuccess) return PIFA_ERR_HIP;
         if (h->n_np > 0) {
-            e = launch_skinny<f16>(ASplit32<f16>{yp, h->r_pad, M, y_scale}, (const f16*)h->C, h->r_pad,
-                                   h->n_np, h->r_pad, h->split,
-                                   make_epi<bf16, kWsNone>((bf16*)Y, h->d_out, h->npiv, h->n_np,
-                                                           out_scale, nullptr, 0, 0, 1.f, nullptr, M),
-                                   st);
+            e = launch_skinny_packed<f16>(kSitePifaGemv2, ASplit32<f16>{yp, h->r_pad, M, y_scale},
+                                          (const f16*)h->C, h->n_np, h->r_pad,
+                                          make_epi<bf16, kWsNone>((bf16*)Y, h->d_out, h->npiv, h->n_np,
+                                                                  out_scale, nullptr, 0, 0, 1.f, nullptr, M),
+                                          st);
             if (e != hipSuccess) return PIFA_ERR_HIP;
         }
         return PIFA_OK;
     }
 
     f16* yp = (f16*)h->ws.ptr;
-    e = launch_gemm<bf16>((const bf16*)X, h->d_in, M, (const bf16*)h->Wp, h->d_in, h->r_pad, h->d_in,
-                          make_epi<bf16, kWsF16>((bf16*)Y, h->d_out, h->piv, h->r, 1.f, yp, h->r_pad,
-                                                 h->r_pad, y_scale, h->overflow, M),
-                          st);
+    e = launch_gemm<bf16, true>(kSitePifaGemm1, (const bf16*)X, h->d_in, M, (const bf16*)h->Wp, 0, h->r_pad,
+                                h->d_in,
+                                make_epi<bf16, kWsF16>((bf16*)Y, h->d_out, h->piv, h->r, 1.f, yp, h->r_pad,
+                                                       h->r_pad, y_scale, h->overflow, M),
+                                st);
     if (e != hipSuccess) return PIFA_ERR_HIP;
     if (h->n_np > 0) {
-        e = launch_gemm<f16>(yp, h->r_pad, M, (const f16*)h->C, h->r_pad, h->n_np, h->r_pad,
-                             make_epi<bf16, kWsNone>((bf16*)Y, h->d_out, h->npiv, h->n_np, out_scale,
-                                                     nullptr, 0, 0, 1.f, nullptr, M),
-                             st);
+        e = launch_gemm<f16, true>(kSitePifaGemm2, yp, h->r_pad, M, (const f16*)h->C, 0, h->n_np, h->r_pad,
+                                   make_epi<bf16, kWsNone>((bf16*)Y, h->d_out, h->npiv, h->n_np, out_scale,
+                                                           nullptr, 0, 0, 1.f, nullptr, M),
+                                   st);
         if (e != hipSuccess) return PIFA_ERR_HIP;
     }
     return PIFA_OK;
@@ -555,30 +638,52 @@ pifa_status dense_forward(const void* W, const void* X, void* Y, int64_t M, int6
     pifa_status s = check_rows_aligned(dtype, d_in);
     if (s != PIFA_OK) return s;
     if (dtype == PIFA_BF16 && (!aligned16(X) || !aligned16(W))) return PIFA_ERR_UNSUPPORTED;
-    hipStream_t st = as_stream(stream);
-    hipError_t e;
-    if (dtype == PIFA_F32) {
-        e = launch_gemm_f32((const float*)X, d_in, M, (const float*)W, d_in, d_out, d_in,
-                            make_epi<float, kWsNone>((float*)Y, d_out, nullptr, d_out, 1.f, nullptr,
-                                                     0, 0, 1.f, nullptr, M),
-                            st);
-        return e == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
-    }
-    auto epi = make_epi<bf16, kWsNone>((bf16*)Y, d_out, nullptr, d_out, 1.f, nullptr, 0, 0, 1.f,
-                                       nullptr, M);
-    if (M <= kDecodeMaxM) {
-        int dev = 0;
-        PIFA_HIP(hipGetDevice(&dev));
-        DeviceScratch& ds = device_scratch(dev);
-        std::lock_guard<std::mutex> g(ds.mu);
-        s = ds.split.ensure(skinny_plan(d_out, d_in), st);
-        if (s != PIFA_OK) return s;
-        e = launch_skinny<bf16>(ALoad16<bf16>{(const bf16*)X, d_in, M}, (const bf16*)W, d_in, d_out,
-                                d_in, ds.split, epi, st);
-        return e == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
-    }
-    e = launch_gemm<bf16>((const bf16*)X, d_in, M, (const bf16*)W, d_in, d_out, d_in, epi, st);
-    return e == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
+    return dense_run<false>(dtype, W, X, Y, M, d_in, d_out, as_stream(stream));
+}
+
+pifa_status dense_layer_create(const void* W, int64_t d_in, int64_t d_out, pifa_dtype dtype,
+                               dense_handle* out) {
+    if (!out) return PIFA_ERR_INVALID_ARG;
+    *out = nullptr;
+    if (!valid_dtype(dtype) || d_in < 1 || d_out < 1 || !W) return PIFA_ERR_INVALID_ARG;
+    if (d_in > INT32_MAX || d_out > INT32_MAX) return PIFA_ERR_UNSUPPORTED;
+    pifa_status s = check_rows_aligned(dtype, d_in);
+    if (s != PIFA_OK) return s;
+    dense_layer* h = new (std::nothrow) dense_layer();
+    if (!h) return PIFA_ERR_OOM;
+    h->dtype = dtype;
+    h->d_in = d_in;
+    h->d_out = d_out;
+    auto fail = [&](pifa_status st) {
+        free_dense(h);
+        return st;
+    };
+    if (hipGetDevice(&h->device) != hipSuccess) return fail(PIFA_ERR_HIP);
+    if (hipDeviceSynchronize() != hipSuccess) return fail(PIFA_ERR_HIP);
+    const bool bf = dtype == PIFA_BF16;
+    const size_t bytes = bf ? (size_t)packed_elems(d_out, d_in) * 2 : (size_t)d_out * d_in * 4;
+    if (hipMalloc(&h->W, bytes) != hipSuccess) return fail(PIFA_ERR_OOM);
+    if ((bf ? pack_lane_bf16(W, d_out, d_in, h->W, d_out, d_in)
+            : pack_rowmajor_f32(W, d_out, d_in, h->W, d_out, d_in)) != hipSuccess)
+        return fail(PIFA_ERR_HIP);
+    if (hipDeviceSynchronize() != hipSuccess) return fail(PIFA_ERR_HIP);
+    *out = h;
+    return PIFA_OK;
+}
+
+pifa_status dense_layer_forward(dense_handle h, const void* X, void* Y, int64_t M, void* stream) {
+    if (!h || M < 0) return PIFA_ERR_INVALID_ARG;
+    if (M == 0) return PIFA_OK;
+    if (!X || !Y) return PIFA_ERR_INVALID_ARG;
+    if (h->dtype == PIFA_BF16 && !aligned16(X)) return PIFA_ERR_UNSUPPORTED;
+    return dense_run<true>(h->dtype, h->W, X, Y, M, h->d_in, h->d_out, as_stream(stream));
+}
+
+pifa_status dense_layer_destroy(dense_handle h) {
+    if (!h) return PIFA_OK;
+    (void)hipDeviceSynchronize();
+    free_dense(h);
+    return PIFA_OK;
 }
 
 pifa_status lowrank_uv_forward(const void* U, const void* V, const void* X, void* Y, int64_t M,
@@ -599,12 +704,7 @@ pifa_status lowrank_uv_forward(const void* U, const void* V, const void* X, void
     std::lock_guard<std::mutex> g(ds.mu);
     s = ds.inter.ensure(lowrank_ws_bytes(dtype, M, dims.r), st);
     if (s != PIFA_OK) return s;
-    if (dtype == PIFA_BF16 && M <= kDecodeMaxM) {
-        s = ds.split.ensure(skinny_plan(dims.r, dims.d_in), st);
-        if (s == PIFA_OK) s = ds.split.ensure(skinny_plan(dims.d_out, dims.r), st);
-        if (s != PIFA_OK) return s;
-    }
-    return lowrank_run(dtype, U, V, X, Y, M, dims.d_in, dims.d_out, dims.r, ds.inter.ptr, ds.split, st);
+    return lowrank_run<false>(dtype, U, V, X, Y, M, dims.d_in, dims.d_out, dims.r, ds.inter.ptr, st);
 }
 
 pifa_status lowrank_layer_create(const void* U, const void* V, pifa_dims dims, pifa_dtype dtype,
@@ -623,19 +723,29 @@ pifa_status lowrank_layer_create(const void* U, const void* V, pifa_dims dims, p
     h->d_in = dims.d_in;
     h->d_out = dims.d_out;
     h->r = dims.r;
-    h->r_pad = dtype == PIFA_BF16 ? round_up(dims.r, kRowPad) : dims.r;
+    const bool bf = dtype == PIFA_BF16;
+    h->r_pad = bf ? round_up(dims.r, kRowPad) : dims.r;
     auto fail = [&](pifa_status st) {
         free_lowrank(h);
         return st;
     };
     if (hipGetDevice(&h->device) != hipSuccess) return fail(PIFA_ERR_HIP);
     if (hipDeviceSynchronize() != hipSuccess) return fail(PIFA_ERR_HIP);
-    const size_t es = esize(dtype);
-    if (hipMalloc(&h->U, (size_t)h->d_out * h->r_pad * es) != hipSuccess) return fail(PIFA_ERR_OOM);
-    if (hipMalloc(&h->V, (size_t)h->r_pad * h->d_in * es) != hipSuccess) return fail(PIFA_ERR_OOM);
-    if (launch_pack_bits(U, h->d_out, h->r, h->r, h->U, h->d_out, h->r_pad, es, 0) != hipSuccess ||
-        launch_pack_bits(V, h->r, h->d_in, h->d_in, h->V, h->r_pad, h->d_in, es, 0) != hipSuccess)
-        return fail(PIFA_ERR_HIP);
+    if (bf) {
+        if (hipMalloc(&h->U, (size_t)packed_elems(h->d_out, h->r_pad) * 2) != hipSuccess ||
+            hipMalloc(&h->V, (size_t)packed_elems(h->r_pad, h->d_in) * 2) != hipSuccess)
+            return fail(PIFA_ERR_OOM);
+        if (pack_lane_bf16(U, h->d_out, h->r, h->U, h->d_out, h->r_pad) != hipSuccess ||
+            pack_lane_bf16(V, h->r, h->d_in, h->V, h->r_pad, h->d_in) != hipSuccess)
+            return fail(PIFA_ERR_HIP);
+    } else {
+        if (hipMalloc(&h->U, (size_t)h->d_out * h->r * 4) != hipSuccess ||
+            hipMalloc(&h->V, (size_t)h->r * h->d_in * 4) != hipSuccess)
+            return fail(PIFA_ERR_OOM);
+        if (pack_rowmajor_f32(U, h->d_out, h->r, h->U, h->d_out, h->r) != hipSuccess ||
+            pack_rowmajor_f32(V, h->r, h->d_in, h->V, h->r, h->d_in) != hipSuccess)
+            return fail(PIFA_ERR_HIP);
+    }
     if (hipDeviceSynchronize() != hipSuccess) return fail(PIFA_ERR_HIP);
     *out = h;
     return PIFA_OK;
@@ -643,14 +753,9 @@ pifa_status lowrank_layer_create(const void* U, const void* V, pifa_dims dims, p
 
 pifa_status lowrank_layer_reserve(lowrank_handle h, int64_t max_M) {
     if (!h || max_M < 0) return PIFA_ERR_INVALID_ARG;
-    const int64_t m = std::max<int64_t>(max_M, kDecodeMaxM);
-    pifa_status s = h->ws.ensure(std::max(lowrank_ws_bytes(h->dtype, m, h->r_pad),
-                                          lowrank_ws_bytes(h->dtype, kDecodeMaxM, h->r_pad)),
-                                 0);
-    if (s == PIFA_OK && h->dtype == PIFA_BF16) {
-        s = h->split.ensure(skinny_plan(h->r_pad, h->d_in), 0);
-        if (s == PIFA_OK) s = h->split.ensure(skinny_plan(h->d_out, h->r_pad), 0);
-    }
+    const size_t need = std::max(lowrank_ws_bytes(h->dtype, max_M, h->r_pad),
+                                 lowrank_ws_bytes(h->dtype, std::min<int64_t>(max_M, kDecodeMaxM), h->r_pad));
+    pifa_status s = h->ws.ensure(need, 0);
     if (s != PIFA_OK) return s;
     return hipDeviceSynchronize() == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
 }
@@ -663,13 +768,9 @@ pifa_status lowrank_layer_forward(lowrank_handle h, const void* X, void* Y, int6
     hipStream_t st = as_stream(stream);
     pifa_status s = h->ws.ensure(lowrank_ws_bytes(h->dtype, M, h->r_pad), st);
     if (s != PIFA_OK) return s;
-    if (h->dtype == PIFA_BF16 && M <= kDecodeMaxM) {
-        s = h->split.ensure(skinny_plan(h->r_pad, h->d_in), st);
-        if (s == PIFA_OK) s = h->split.ensure(skinny_plan(h->d_out, h->r_pad), st);
-        if (s != PIFA_OK) return s;
-    }
-    return lowrank_run(h->dtype, h->U, h->V, X, Y, M, h->d_in, h->d_out, h->r_pad, h->ws.ptr, h->split,
-                       st);
+    if (h->dtype == PIFA_BF16)
+        return lowrank_run<true>(h->dtype, h->U, h->V, X, Y, M, h->d_in, h->d_out, h->r_pad, h->ws.ptr, st);
+    return lowrank_run<false>(h->dtype, h->U, h->V, X, Y, M, h->d_in, h->d_out, h->r, h->ws.ptr, st);
 }
 
 pifa_status lowrank_layer_destroy(lowrank_handle h) {
@@ -677,6 +778,58 @@ pifa_status lowrank_layer_destroy(lowrank_handle h) {
     (void)hipDeviceSynchronize();
     free_lowrank(h);
     return PIFA_OK;
+}
+
+pifa_status pifa_profile_enable(int on) {
+    Profiler& p = profiler();
+    std::lock_guard<std::mutex> g(p.mu);
+    p.on = on != 0;
+    return PIFA_OK;
+}
+
+pifa_status pifa_profile_reset(void) {
+    Profiler& p = profiler();
+    std::lock_guard<std::mutex> g(p.mu);
+    for (auto& r : p.pending) {
+        (void)hipEventSynchronize(r.stop);
+        p.pool.push_back(r.start);
+        p.pool.push_back(r.stop);
+    }
+    p.pending.clear();
+    for (int i = 0; i < kSiteCount; ++i) {
+        p.launches[i] = 0;
+        p.ms[i] = 0.0;
+    }
+    return PIFA_OK;
+}
+
+pifa_status pifa_profile_read(const char** names, int64_t* launches, double* total_ms, int max_sites,
+                              int* n_sites) {
+    if (!names || !launches || !total_ms || !n_sites || max_sites < 0) return PIFA_ERR_INVALID_ARG;
+    Profiler& p = profiler();
+    std::lock_guard<std::mutex> g(p.mu);
+    pifa_status status = PIFA_OK;
+    for (auto& r : p.pending) {
+        float ms = 0.f;
+        if (hipEventSynchronize(r.stop) != hipSuccess ||
+            hipEventElapsedTime(&ms, r.start, r.stop) != hipSuccess)
+            status = PIFA_ERR_HIP;
+        p.launches[r.site] += 1;
+        p.ms[r.site] += ms;
+        p.pool.push_back(r.start);
+        p.pool.push_back(r.stop);
+    }
+    p.pending.clear();
+    int n = 0;
+    for (int i = 0; i < kSiteCount && n < max_sites; ++i) {
+        if (p.launches[i] == 0) continue;
+        names[n] = kSiteNames[i];
+        launches[n] = p.launches[i];
+        total_ms[n] = p.ms[i];
+        ++n;
+    }
+    *n_sites = n;
+    return status;
 }
 
 }  // extern "C"

@@ -58,11 +58,18 @@ _SIGNATURES = {
     "pifa_layer_set_intermediate_scale": (_st, [_vp, ctypes.c_int]),
     "pifa_layer_overflow_count": (_st, [_vp, ctypes.POINTER(_i64)]),
     "dense_forward": (_st, [_vp, _vp, _vp, _i64, _i64, _i64, ctypes.c_int, _vp]),
+    "dense_layer_create": (_st, [_vp, _i64, _i64, ctypes.c_int, ctypes.POINTER(_vp)]),
+    "dense_layer_forward": (_st, [_vp, _vp, _vp, _i64, _vp]),
+    "dense_layer_destroy": (_st, [_vp]),
     "lowrank_uv_forward": (_st, [_vp, _vp, _vp, _vp, _i64, pifa_dims, ctypes.c_int, _vp]),
     "lowrank_layer_create": (_st, [_vp, _vp, pifa_dims, ctypes.c_int, ctypes.POINTER(_vp)]),
     "lowrank_layer_forward": (_st, [_vp, _vp, _vp, _i64, _vp]),
     "lowrank_layer_reserve": (_st, [_vp, _i64]),
     "lowrank_layer_destroy": (_st, [_vp]),
+    "pifa_profile_enable": (_st, [ctypes.c_int]),
+    "pifa_profile_reset": (_st, []),
+    "pifa_profile_read": (_st, [ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(_i64),
+                                ctypes.POINTER(ctypes.c_double), ctypes.c_int, ctypes.POINTER(ctypes.c_int)]),
 }
 
 
@@ -191,6 +198,27 @@ def dense_forward(W, X, Y, M: int | None = None, d_in: int | None = None, d_out:
                                                 M, d_in, d_out, dt, _stream(stream)))
 
 
+def dense_layer_create(W, d_in: int | None = None, d_out: int | None = None,
+                       dtype: int | None = None) -> int:
+    d_in = W.shape[1] if d_in is None else int(d_in)
+    d_out = W.shape[0] if d_out is None else int(d_out)
+    dt = _dtype_code(W) if dtype is None else int(dtype)
+    out = _vp()
+    _check("dense_layer_create", lib().dense_layer_create(_dev_ptr(W, "W"), d_in, d_out, dt,
+                                                          ctypes.byref(out)))
+    return out.value
+
+
+def dense_layer_forward(handle: int, X, Y, M: int | None = None, stream=None) -> None:
+    M = X.shape[0] if M is None else int(M)
+    _check("dense_layer_forward", lib().dense_layer_forward(handle, _dev_ptr(X, "X"), _dev_ptr(Y, "Y"), M,
+                                                            _stream(stream)))
+
+
+def dense_layer_destroy(handle: int) -> None:
+    _check("dense_layer_destroy", lib().dense_layer_destroy(handle))
+
+
 def lowrank_uv_forward(U, V, X, Y, M: int | None = None, dims=None, dtype: int | None = None,
                        stream=None) -> None:
     M = X.shape[0] if M is None else int(M)
@@ -222,6 +250,24 @@ def lowrank_layer_reserve(handle: int, max_M: int) -> None:
 
 def lowrank_layer_destroy(handle: int) -> None:
     _check("lowrank_layer_destroy", lib().lowrank_layer_destroy(handle))
+
+
+def pifa_profile_enable(on: bool) -> None:
+    _check("pifa_profile_enable", lib().pifa_profile_enable(1 if on else 0))
+
+
+def pifa_profile_reset() -> None:
+    _check("pifa_profile_reset", lib().pifa_profile_reset())
+
+
+def pifa_profile_read(max_sites: int = 32) -> dict:
+    """{site name: (launches, total milliseconds)} since the last reset."""
+    names = (ctypes.c_char_p * max_sites)()
+    launches = (_i64 * max_sites)()
+    ms = (ctypes.c_double * max_sites)()
+    n = ctypes.c_int()
+    _check("pifa_profile_read", lib().pifa_profile_read(names, launches, ms, max_sites, ctypes.byref(n)))
+    return {names[i].decode(): (int(launches[i]), float(ms[i])) for i in range(n.value)}
 
 
 # ---------------------------------------------------------------- convenience

@@ -38,7 +38,16 @@ def _run_all(d_in, d_out, r, M, dtype, seed=1):
     y = torch.full((M, d_out), float("nan"), dtype=x_dev.dtype, device="cuda:0")
     pifa.dense_forward(w_dev, x_dev, y)
     torch.cuda.synchronize()
-    errs["dense"] = rel_fro(from_dev(y)[rows], oracle.dense_forward(x64[rows], W64))
+    ref_d = oracle.dense_forward(x64[rows], W64)
+    errs["dense"] = rel_fro(from_dev(y)[rows], ref_d)
+    hd = pifa.dense_layer_create(w_dev)
+    try:
+        y.fill_(float("nan"))
+        pifa.dense_layer_forward(hd, x_dev, y)
+        torch.cuda.synchronize()
+        errs["dense_layer"] = rel_fro(from_dev(y)[rows], ref_d)
+    finally:
+        pifa.dense_layer_destroy(hd)
     ref_lr = oracle.lowrank_forward(x64[rows], U64, V64)
     if dtype == "f32" or r % 8 == 0:
         y.fill_(float("nan"))
@@ -87,6 +96,16 @@ def test_dense_integer_bitexact(M):
         x_st, x64 = inputs.round_to(X, dtype)
         x_dev = to_dev(x_st)
         y = torch.full((M, d_out), float("nan"), dtype=x_dev.dtype, device="cuda:0")
-        pifa.dense_forward(to_dev(w_st), x_dev, y)
+        w_dev = to_dev(w_st)
+        pifa.dense_forward(w_dev, x_dev, y)
         torch.cuda.synchronize()
-        assert np.array_equal(from_dev(y), oracle.dense_forward(x64, W64))
+        ref = oracle.dense_forward(x64, W64)
+        assert np.array_equal(from_dev(y), ref)
+        h = pifa.dense_layer_create(w_dev)
+        try:
+            y.fill_(float("nan"))
+            pifa.dense_layer_forward(h, x_dev, y)
+            torch.cuda.synchronize()
+            assert np.array_equal(from_dev(y), ref)
+        finally:
+            pifa.dense_layer_destroy(h)

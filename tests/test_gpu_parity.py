@@ -115,6 +115,39 @@ def test_integer_layers_bitexact(dims, dtype):
             lay.close()
 
 
+@pytest.mark.parametrize("dims", [(2048, 4096, 2048), (1536, 2752, 1536)])
+def test_integer_layers_bitexact_large_tiles(dims):
+    """M = 4096 selects the large 256 x 128 prefill tile; integer data keeps
+    every element exact, checked on sampled rows against the oracle."""
+    d_in, d_out, r = dims
+    M = 4096
+    piv, npiv = inputs.random_partition(d_out, r, seed=r + 1)
+    X, Wp, C = inputs.integer_layer(d_in, d_out, r, M, seed=7)
+    for dtype in ("bf16", "f32"):
+        lay = DeviceLayer(piv, npiv, Wp, C, dtype)
+        try:
+            st, x64 = inputs.round_to(X, dtype)
+            y = from_dev(lay.forward(to_dev(st)))
+            rows = sample_rows(M, k=64, seed=3)
+            assert np.array_equal(y[rows], lay.oracle(x64[rows]))
+        finally:
+            lay.close()
+
+
+def test_layout_probe_large_m():
+    """Probe weights at the attention shape with M = 4096 rows."""
+    name = "B_attn_4096"
+    cfg, lay_i, d_in, d_out, r, dt, Ms, kind = inputs.CONFIGS[name]
+    piv, npiv, *_ = config_layer(name)
+    Wp, C = inputs.layout_probe_layer(d_in, d_out, r)
+    lay = DeviceLayer(piv, npiv, Wp, C, dt)
+    try:
+        for M in (2048, 4096):
+            _check_layout(lay, M, seed=M)
+    finally:
+        lay.close()
+
+
 # ------------------------------------------------------------------ Gaussian configs
 def _gaussian_case(name: str, M: int):
     cfg, lay_i, d_in, d_out, r, dt, Ms, kind = inputs.CONFIGS[name]
