@@ -237,7 +237,7 @@ def cpu_baseline(d_in, d_out, r, seed, M_full, budget_s=10.0):
 def traffic_from_profiles(kernel: str):
     """HBM bytes per launch from a committed counter summary, if it matches
     the current kernel sources; else None."""
-    path = os.path.join(ROOT, "profiles", "traffic_%s.json" % kernel)
+    path = os.path.join(ROOT, "profiles", "%s_attn4096_M4096_traffic.txt" % kernel)
     if not os.path.exists(path):
         return None
     try:
@@ -259,6 +259,8 @@ def main():
     ap.add_argument("--full", action="store_true", help="also sweep every configuration")
     ap.add_argument("--out", default=os.path.join(ROOT, "gpurun_out", "bench_full.json"))
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--profile-run", action="store_true",
+                    help="only the headline steps plus one calibration copy of 512 MiB (for counter passes)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: this PIFA layer build has no multi-GPU path "
@@ -282,6 +284,18 @@ def main():
     y = torch.empty((M, d_out), dtype=torch.bfloat16, device="cuda:0")
     h = wl.pifa_h[0]
     pifa.pifa_layer_reserve(h, M)
+
+    if args.profile_run:
+        # a device-to-device copy of known size: the counters' scale factor
+        src = torch.empty(512 << 20, dtype=torch.uint8, device="cuda:0")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        for _ in range(args.steps):
+            pifa.pifa_forward(h, x, y, M, stream)
+        torch.cuda.synchronize()
+        log("profile run done")
+        return
 
     # ---- headline: K timed steps of the M = 4096 forward
     for _ in range(args.warmup):

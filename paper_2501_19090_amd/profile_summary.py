@@ -1,0 +1,98 @@
+"""Summarise rocprofv3 output for the committed profiles.
+
+    python -m paper_2501_19090_amd.profile_summary stats  <kernel_stats.csv> <out.md> <command...>
+    python -m paper_2501_19090_amd.profile_summary traffic <fetch_dir> <write_dir> <kernel-substring>
+           <launch-name> <out.txt> <command...>
+
+`stats` turns a --kernel-trace --stats CSV into a short markdown table.
+`traffic` reads two --pmc passes (FETCH_SIZE, then WRITE_SIZE; KiB per
+dispatch), takes the average for the kernel whose name contains
+<kernel-substring>, and scales it by what the same counters read for the
+calibration copy (a device-to-device copy of a known byte count, recorded by
+bench.py --profile-run); the result is written as JSON text together with
+the source digest of the kernels it was measured on.
+"""
+from __future__ import annotations
+
+import csv
+import glob
+import json
+import os
+import sys
+
+from paper_2501_19090_amd import build
+
+COPY_BYTES = 512 << 20  # bench.py --profile-run copies this many bytes once
+
+
+def _short(name: str) -> str:
+    for a, b in [("_ZN4pifa", ""), ("ENS_10ScatterEpi", "|Epi"), ("IDF16bLi", "<bf16,"), ("IDF16_Li", "<f16,")]:
+        name = name.replace(a, b)
+    return name[:110]
+
+
+def stats(csv_path: str, out_md: str, command: str) -> None:
+    rows = list(csv.DictReader(open(csv_path)))
+    lines = ["# rocprofv3 kernel statistics", "", "Command (run from the repository root on the GPU host):", "",
+             "```", command, "```", "",
+             "| kernel | calls | avg us | min us | max us | share % |", "|---|---:|---:|---:|---:|---:|"]
+    for r in rows[:16]:
+        lines.append("| `%s` | %s | %.2f | %.2f | %.2f | %.1f |" % (
+            _short(r["Name"]), r["Calls"], float(r["AverageNs"]) / 1e3, float(r["MinNs"]) / 1e3,
+            float(r["MaxNs"]) / 1e3, float(r["Percentage"])))
+    with open(out_md, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
+def _counter(dirname: str, counter: str):
+    files = glob.glob(os.path.join(dirname, "**", "*counter_collection.csv"), recursive=True)
+    out = []
+    for fn in files:
+        for r in csv.DictReader(open(fn)):
+            if r["Counter_Name"] == counter:
+                out.append((r["Kernel_Name"], float(r["Counter_Value"])))
+    return out
+
+
+def _avg(vals, pred):
+    v = [x for n, x in vals if pred(n)]
+    return (sum(v) / len(v), len(v)) if v else (None, 0)
+
+
+def traffic(fetch_dir, write_dir, kernel_sub, launch_name, out_txt, command):
+    fetch = _counter(fetch_dir, "FETCH_SIZE")
+    write = _counter(write_dir, "WRITE_SIZE")
+    k_fetch, nf = _avg(fetch, lambda n: kernel_sub in n)
+    k_write, nw = _avg(write, lambda n: kernel_sub in n)
+    is_copy = lambda n: "copyBuffer" in n or "elementwise_kernel" in n and "copy" in n
+    # the calibration copy is the largest copy dispatch in the run
+    c_fetch = max((x for n, x in fetch if is_copy(n)), default=None)
+    c_write = max((x for n, x in write if is_copy(n)), default=None)
+    rec = {
+        "kernel": launch_name, "kernel_name_match": kernel_sub,
+        "dispatches": {"fetch": nf, "write": nw},
+        "fetch_kib_raw": k_fetch, "write_kib_raw": k_write,
+        "copy_bytes": COPY_BYTES, "copy_fetch_kib_raw": c_fetch, "copy_write_kib_raw": c_write,
+        "source_digest": build.source_digest(), "command": command,
+    }
+    if None not in (k_fetch, k_write, c_fetch, c_write):
+        f_scale = COPY_BYTES / (c_fetch * 1024.0)
+        w_scale = COPY_BYTES / (c_write * 1024.0)
+        rec.update({"fetch_scale": f_scale, "write_scale": w_scale,
+                    "hbm_read_bytes_per_launch": k_fetch * 1024.0 * f_scale,
+                    "hbm_write_bytes_per_launch": k_write * 1024.0 * w_scale})
+        rec["hbm_bytes_per_launch"] = rec["hbm_read_bytes_per_launch"] + rec["hbm_write_bytes_per_launch"]
+    with open(out_txt, "w") as f:
+        json.dump(rec, f, indent=1)
+        f.write("\n")
+    print(json.dumps(rec, indent=1))
+
+
+if __name__ == "__main__":
+    mode = sys.argv[1]
+    if mode == "stats":
+        stats(sys.argv[2], sys.argv[3], " ".join(sys.argv[4:]))
+    elif mode == "traffic":
+        traffic(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5], sys.argv[6], " ".join(sys.argv[7:]))
+    else:
+        raise SystemExit(__doc__)
