@@ -146,6 +146,7 @@ pifa_status dense_forward(const void* W, const void* X, void* Y, int64_t M, int6
 pifa_status dense_layer_create(const void* W, int64_t d_in, int64_t d_out, pifa_dtype dtype,
                                dense_handle* out);
 pifa_status dense_layer_forward(dense_handle h, const void* X, void* Y, int64_t M, void* stream);
+pifa_status dense_layer_reserve(dense_handle h, int64_t max_M);
 pifa_status dense_layer_destroy(dense_handle h);
 
 /*

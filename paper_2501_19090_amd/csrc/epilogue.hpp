@@ -7,14 +7,16 @@
 //     non-pivot assignment of Algorithm "PIFA Layer" (its last two steps),
 //     fused into the producing kernel so there is no separate permutation pass;
 //   * optionally keeps a workspace copy ws[m * ldws + n] for n < n_ws, as fp16
-//     times ws_scale (the bf16 path's Y_p hand-off) or as fp32.
+//     times ws_scale (the bf16 path's Y_p hand-off), as fp32, or as an fp16
+//     pair hi = fp16(v * ws_scale), lo = fp16(v * ws_scale - hi) in two planes
+//     of M * ldws elements (the decode hand-off, about 22 significant bits).
 #pragma once
 
 #include "common.hpp"
 
 namespace pifa {
 
-enum WsKind { kWsNone = 0, kWsF16 = 1, kWsF32 = 2 };
+enum WsKind { kWsNone = 0, kWsF16 = 1, kWsF32 = 2, kWsF16Pair = 3 };
 
 template <typename TOut, int WS>
 struct ScatterEpi {
@@ -56,8 +58,25 @@ struct ScatterEpi {
                 if (!__builtin_isfinite((float)h) && __builtin_isfinite(s)) atomicAdd(overflow, 1);
                 reinterpret_cast<f16*>(ws)[m * ldws + c.n] = h;
             }
+        } else if constexpr (WS == kWsF16Pair) {
+            if (c.ws_ok) {
+                const float s = v * ws_scale;
+                const f16 hi = (f16)s;
+                const f16 lo = (f16)(s - (float)hi);
+                if (!__builtin_isfinite((float)hi) && __builtin_isfinite(s)) atomicAdd(overflow, 1);
+                f16* w = reinterpret_cast<f16*>(ws);
+                w[m * ldws + c.n] = hi;
+                w[(M + m) * ldws + c.n] = lo;
+            }
         } else if constexpr (WS == kWsF32) {
-            if (c.ws_ok) reinterpret_cast<float*>(ws)[m * ldws + c.n] = v;
+            if (c.ws_ok) {
+                reinterpret_cast<float*>(ws)[m * ldws + c.n] = v;
+                // the consumer splits v * ws_scale into fp16 hi + lo
+                if (overflow) {
+                    const float s = v * ws_scale;
+                    if (!__builtin_isfinite((float)(f16)s) && __builtin_isfinite(s)) atomicAdd(overflow, 1);
+                }
+            }
         }
     }
 };

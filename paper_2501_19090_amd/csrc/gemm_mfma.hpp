@@ -83,11 +83,14 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc31(const void* base, 
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, 0x00020000);
 }
 
+// K splitting: workgroup (tile, blockIdx.y = s) reduces K range
+// [s * k_split, min(K, (s + 1) * k_split)); k_split is a multiple of BK
+// (k_split >= K: no split).  Both operands are masked outside that range.
 template <typename T, int BM, int BN, int BK, int WM, int WN, bool BPACK, int PGR, typename Epi>
 __global__ __launch_bounds__(WM* WN* kWave) void gemm_nt_mfma(const T* __restrict__ A, int64_t lda,
                                                              int64_t M, const T* __restrict__ B,
                                                              int64_t ldb, int64_t N, int64_t K,
-                                                             Epi epi) {
+                                                             int64_t k_split, Epi epi) {
     constexpr int NT = WM * WN * kWave;
     constexpr int LDK = BK + 8;  // padded LDS row, in elements
     constexpr int CPR = BK / 8;  // 16-byte chunks per tile row
@@ -121,6 +124,8 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_nt_mfma(const T* __restric
     const int lane = tid & (kWave - 1);
     const int wave = tid / kWave;
     const int wm = wave / WN, wn = wave % WN;
+    const int64_t kbeg = (int64_t)blockIdx.y * k_split;
+    const int64_t kend = (kbeg + k_split) < K ? (kbeg + k_split) : K;
 
     struct Stage {
         u32x4 a[A_CH], b[B_CH];
@@ -132,7 +137,7 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_nt_mfma(const T* __restric
         for (int i = 0; i < A_CH; ++i) {
             const int c = tid + i * NT, row = c / CPR;
             const int64_t k = k0 + (c % CPR) * 8;
-            R.a[i] = load16(ars, k < K ? (uint32_t)((row * lda + k) * (int64_t)sizeof(T)) : kMaskedOffset);
+            R.a[i] = load16(ars, k < kend ? (uint32_t)((row * lda + k) * (int64_t)sizeof(T)) : kMaskedOffset);
         }
         if constexpr (BPACK) {
             const int64_t blk = k0 / kPackCols;
@@ -141,15 +146,17 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_nt_mfma(const T* __restric
             for (int i = 0; i < B_CH; ++i) {
                 const int cid = tid + i * NT, gl = cid / CPG, rem = cid % CPG;
                 const int c = rem / LPC, l = hsel * LPC + rem % LPC;
-                R.b[i] = load16(brs, (uint32_t)((((gl * KB + blk) * 4 + c) * 64 + l) * 16));
-                R.blds[i] = (gl * kPackRows + (l & 15)) * LDK + (4 * ((l >> 4) - hsel * (LPC / 16)) + c) * 8;
+                const int kc = 4 * ((l >> 4) - hsel * (LPC / 16)) + c;  // chunk index in the tile
+                R.b[i] = load16(brs, k0 + kc * 8 < kend ? (uint32_t)((((gl * KB + blk) * 4 + c) * 64 + l) * 16)
+                                                        : kMaskedOffset);
+                R.blds[i] = (gl * kPackRows + (l & 15)) * LDK + kc * 8;
             }
         } else {
 #pragma unroll
             for (int i = 0; i < B_CH; ++i) {
                 const int c = tid + i * NT, row = c / CPR;
                 const int64_t k = k0 + (c % CPR) * 8;
-                R.b[i] = load16(brs, k < K ? (uint32_t)((row * ldb + k) * (int64_t)sizeof(T)) : kMaskedOffset);
+                R.b[i] = load16(brs, k < kend ? (uint32_t)((row * ldb + k) * (int64_t)sizeof(T)) : kMaskedOffset);
                 R.blds[i] = row * LDK + (c % CPR) * 8;
             }
         }
@@ -182,13 +189,13 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_nt_mfma(const T* __restric
         for (int j = 0; j < TN; ++j) fb[slot][j] = *reinterpret_cast<const u32x4*>(bs + j * 32 * LDK);
     };
 
-    const int64_t nk = ceil_div(K, BK);
+    const int64_t nk = ceil_div(kend - kbeg, BK);
     // Tile t is staged in S[t % PGR].  Before iteration kt the LDS buffer
     // (kt & 1) holds tile kt and tiles kt+1 .. kt+PGR are in flight.
-    gload(0, S[0]);
-    if (PGR == 2 && nk > 1) gload(BK, S[PGR - 1]);
+    gload(kbeg, S[0]);
+    if (PGR == 2 && nk > 1) gload(kbeg + BK, S[PGR - 1]);
     sstore(0, S[0]);
-    if (nk > PGR) gload((int64_t)PGR * BK, S[0]);
+    if (nk > PGR) gload(kbeg + (int64_t)PGR * BK, S[0]);
     __syncthreads();
     lds_frag(0, 0, 0);
     auto body = [&](int64_t kt, Stage& nxt) {  // nxt = S[(kt + 1) % PGR]
@@ -203,7 +210,7 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_nt_mfma(const T* __restric
                 for (int j = 0; j < TN; ++j) acc[i][j] = Mfma<T>::mma32(fa[slot][i], fb[slot][j], acc[i][j]);
             // the other LDS buffer was last read before the previous barrier
             if (kk == 0 && kt + 1 < nk) sstore(cur ^ 1, nxt);
-            if (kk == 1 && kt + 1 + PGR < nk) gload((kt + 1 + PGR) * BK, nxt);
+            if (kk == 1 && kt + 1 + PGR < nk) gload(kbeg + (kt + 1 + PGR) * BK, nxt);
         }
         __syncthreads();
         if (kt + 1 < nk) lds_frag(cur ^ 1, 0, 0);
@@ -228,6 +235,43 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_nt_mfma(const T* __restric
 #pragma unroll
             for (int v = 0; v < 16; ++v) epi.store(mb + 8 * (v >> 2) + (v & 3), c, acc[i][j][v]);
         }
+    }
+}
+
+// Epilogue of a K-split launch: the fp32 partial tile of split s goes to
+// P[s][m][n] (row-major M x N per split).
+struct SplitEpi {
+    float* P;
+    int64_t M, N;
+    struct Col {
+        int64_t n;
+        bool ok;
+    };
+    __device__ __forceinline__ Col col(int64_t n) const { return Col{n, n < N}; }
+    __device__ __forceinline__ void store(int64_t m, const Col& c, float v) const {
+        if (m < M && c.ok) P[((int64_t)blockIdx.y * M + m) * N + c.n] = v;
+    }
+};
+
+// Sum the S partial products in split order (deterministic) and apply the
+// real epilogue; one thread per 4 consecutive columns of a row.
+template <typename Epi>
+__global__ __launch_bounds__(256) void split_reduce(const float* __restrict__ P, int S, int64_t M,
+                                                    int64_t N, Epi epi) {
+    const int64_t nq = ceil_div(N, 4);
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < M * nq;
+         q += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t m = q / nq, n0 = (q % nq) * 4;
+        float v[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int s = 0; s < S; ++s) {
+            const float* p = P + ((int64_t)s * M + m) * N + n0;
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (n0 + e < N) v[e] += p[e];
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            if (n0 + e < N) epi.store(m, epi.col(n0 + e), v[e]);
     }
 }
 

@@ -1,11 +1,12 @@
-// Decode-sized products (M <= 16 activation rows), bound by the weight stream.
+// Decode-sized products (M <= 16 * MT activation rows, MT <= 8), bound by the
+// weight stream.
 //
-// acc(m, n) = sum_k A[m, k] * B[n, k] for m < M <= 16, B = weight rows.
-// One workgroup owns 16 output columns (one MFMA 16x16x32 output tile) and
-// the whole K range, so no workgroup waits on another: its waves take
-// interleaved 128-wide K slices, stream the 16 weight rows of each slice,
-// keep the activation rows in the MFMA A operand (rows >= M are zero), and
-// are summed in LDS at the end.
+// acc(m, n) = sum_k A[m, k] * B[n, k] for m < M, B = weight rows.
+// One workgroup owns 16 output columns (one MFMA 16x16x32 output tile per
+// 16 activation rows) and the whole K range, so no workgroup waits on
+// another: its waves take interleaved 128-wide K slices, stream the 16 weight
+// rows of each slice once, feed every weight chunk to MT MFMAs (one per
+// 16-row activation tile; rows >= M are zero), and are summed in LDS.
 //
 // The K order inside an MFMA is free as long as A and B use the same one, so
 // a lane covers 32 consecutive K values of its row per slice and feeds them
@@ -34,6 +35,24 @@ struct ALoad16 {
     __device__ __forceinline__ void load(int m, int64_t k, int64_t K, u32x4 (&out)[1]) const {
         out[0] = (m < M && k < K) ? *reinterpret_cast<const u32x4*>(a + (int64_t)m * lda + k)
                                   : zero16();
+    }
+};
+
+// A operand from an fp16 pair hand-off (epilogue kWsF16Pair): hi plane at
+// a, lo plane at a + M * lda; two MFMAs against the same weights.
+struct ALoadPair16 {
+    const f16* a;
+    int64_t lda;
+    int64_t M;
+    static constexpr int kOps = 2;
+    __device__ __forceinline__ void load(int m, int64_t k, int64_t K, u32x4 (&out)[2]) const {
+        if (!(m < M && k < K)) {
+            out[0] = zero16();
+            out[1] = zero16();
+            return;
+        }
+        out[0] = *reinterpret_cast<const u32x4*>(a + (int64_t)m * lda + k);
+        out[1] = *reinterpret_cast<const u32x4*>(a + (M + (int64_t)m) * lda + k);
     }
 };
 
@@ -67,26 +86,29 @@ struct ASplit32 {
     }
 };
 
-// Sum the per-wave 16x16 tiles in LDS and hand the result to the epilogue.
-template <int WAVES, typename Epi>
-__device__ __forceinline__ void skinny_finish(f32x4 acc, int64_t n0, const Epi& epi) {
-    __shared__ f32x4 red[WAVES][kWave];
+// Sum the per-wave 16x16 tiles in LDS and hand the result to the epilogue;
+// wave t finishes activation tile t (t < MT).
+template <int WAVES, int MT, typename Epi>
+__device__ __forceinline__ void skinny_finish(const f32x4 (&acc)[MT], int64_t n0, const Epi& epi) {
+    static_assert(MT <= WAVES, "one finishing wave per tile");
+    __shared__ f32x4 red[WAVES][MT][kWave];
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
-    red[wave][lane] = acc;
-    __syncthreads();
-    if (wave != 0) return;
-    f32x4 tot = red[0][lane];
 #pragma unroll
-    for (int w = 1; w < WAVES; ++w) tot += red[w][lane];
+    for (int t = 0; t < MT; ++t) red[wave][t][lane] = acc[t];
+    __syncthreads();
+    if (wave >= MT) return;
+    f32x4 tot = red[0][wave][lane];
+#pragma unroll
+    for (int w = 1; w < WAVES; ++w) tot += red[w][wave][lane];
     // 16x16 accumulator layout: lane holds column (lane % 16), rows 4*(lane/16) + v
     const auto c = epi.col(n0 + (lane & 15));
 #pragma unroll
-    for (int v = 0; v < 4; ++v) epi.store(4 * (lane >> 4) + v, c, tot[v]);
+    for (int v = 0; v < 4; ++v) epi.store(16 * wave + 4 * (lane >> 4) + v, c, tot[v]);
 }
 
 // Weights in lane order (layout.hpp): B holds packed_elems(N, K) elements.
-template <typename TB, int WAVES, int UNROLL, typename AL, typename Epi>
+template <typename TB, int WAVES, int UNROLL, int MT, typename AL, typename Epi>
 __global__ __launch_bounds__(WAVES* kWave) void skinny_packed(AL al, const TB* __restrict__ B,
                                                              int64_t N, int64_t K, Epi epi) {
     constexpr int OPS = AL::kOps;
@@ -98,10 +120,11 @@ __global__ __launch_bounds__(WAVES* kWave) void skinny_packed(AL al, const TB* _
     const int row = lane & 15;
     const int kq = (lane >> 4) * 32;
 
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    f32x4 acc[MT];
+#pragma unroll
+    for (int t = 0; t < MT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int64_t kb = wave; kb < KB; kb += (int64_t)WAVES * UNROLL) {
         u32x4 bw[UNROLL][4];
-        u32x4 aw[UNROLL][4][OPS];
 #pragma unroll
         for (int u = 0; u < UNROLL; ++u) {
             const int64_t b = kb + (int64_t)u * WAVES;
@@ -112,19 +135,19 @@ __global__ __launch_bounds__(WAVES* kWave) void skinny_packed(AL al, const TB* _
         for (int u = 0; u < UNROLL; ++u)
 #pragma unroll
             for (int c = 0; c < 4; ++c)
-                al.load(row, (kb + (int64_t)u * WAVES) * kSkinnyStepK + kq + c * 8, K, aw[u][c]);
 #pragma unroll
-        for (int u = 0; u < UNROLL; ++u)
+                for (int t = 0; t < MT; ++t) {
+                    u32x4 aw[OPS];
+                    al.load(row + 16 * t, (kb + (int64_t)u * WAVES) * kSkinnyStepK + kq + c * 8, K, aw);
 #pragma unroll
-            for (int c = 0; c < 4; ++c)
-#pragma unroll
-                for (int o = 0; o < OPS; ++o) acc = Mfma<TB>::mma16(aw[u][c][o], bw[u][c], acc);
+                    for (int o = 0; o < OPS; ++o) acc[t] = Mfma<TB>::mma16(aw[o], bw[u][c], acc[t]);
+                }
     }
-    skinny_finish<WAVES>(acc, g * kSkinnyRows, epi);
+    skinny_finish<WAVES, MT>(acc, g * kSkinnyRows, epi);
 }
 
 // Row-major weights (row stride ldb), for caller-owned matrices.
-template <typename TB, int WAVES, int UNROLL, typename AL, typename Epi>
+template <typename TB, int WAVES, int UNROLL, int MT, typename AL, typename Epi>
 __global__ __launch_bounds__(WAVES* kWave) void skinny_rowmajor(AL al, const TB* __restrict__ B,
                                                                int64_t ldb, int64_t N, int64_t K,
                                                                Epi epi) {
@@ -136,10 +159,11 @@ __global__ __launch_bounds__(WAVES* kWave) void skinny_rowmajor(AL al, const TB*
     const int row = lane & 15;
     const int kq = (lane >> 4) * 32;
 
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    f32x4 acc[MT];
+#pragma unroll
+    for (int t = 0; t < MT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int64_t kb = (int64_t)wave * kSkinnyStepK; kb < K; kb += (int64_t)WAVES * kSkinnyStepK * UNROLL) {
         u32x4 bw[UNROLL][4];
-        u32x4 aw[UNROLL][4][OPS];
 #pragma unroll
         for (int u = 0; u < UNROLL; ++u)
 #pragma unroll
@@ -151,15 +175,15 @@ __global__ __launch_bounds__(WAVES* kWave) void skinny_rowmajor(AL al, const TB*
         for (int u = 0; u < UNROLL; ++u)
 #pragma unroll
             for (int c = 0; c < 4; ++c)
-                al.load(row, kb + (int64_t)u * WAVES * kSkinnyStepK + kq + c * 8, K, aw[u][c]);
 #pragma unroll
-        for (int u = 0; u < UNROLL; ++u)
+                for (int t = 0; t < MT; ++t) {
+                    u32x4 aw[OPS];
+                    al.load(row + 16 * t, kb + (int64_t)u * WAVES * kSkinnyStepK + kq + c * 8, K, aw);
 #pragma unroll
-            for (int c = 0; c < 4; ++c)
-#pragma unroll
-                for (int o = 0; o < OPS; ++o) acc = Mfma<TB>::mma16(aw[u][c][o], bw[u][c], acc);
+                    for (int o = 0; o < OPS; ++o) acc[t] = Mfma<TB>::mma16(aw[o], bw[u][c], acc[t]);
+                }
     }
-    skinny_finish<WAVES>(acc, n0, epi);
+    skinny_finish<WAVES, MT>(acc, n0, epi);
 }
 
 }  // namespace pifa

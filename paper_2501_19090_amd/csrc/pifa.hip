@@ -31,11 +31,9 @@ using namespace pifa;
 namespace {
 
 // ------------------------------------------------------------------ config
-constexpr int64_t kDecodeMaxM = 16;  // M at or below this takes the skinny path
+constexpr int64_t kDecodeMaxM = 16;  // M at or below this takes the weight-streaming path
 constexpr int64_t kRowPad = 64;      // W_p rows / C columns padded to this multiple
 
-// Prefill tiles: 256 x 128 (8 waves of 64 x 64, two tiles of global
-// prefetch); 128 x 128 when the large tile would leave CUs without work.
 constexpr int kGemmBK = 64;
 constexpr int64_t kCus = 256;
 constexpr int kSkinnyWaves = 8, kSkinnyUnroll = 2;
@@ -149,19 +147,89 @@ struct TimedLaunch {
 };
 
 // ------------------------------------------------------------------ launchers
+enum TileCfg : int { kTile256x256 = 0, kTile256x128 = 1, kTile128x128 = 2 };
+
+// K splitting for launches that would leave CUs idle: at most kMaxSplit
+// splits of at least two K tiles each, partials capped at kMaxPartialBytes.
+constexpr int64_t kMaxSplit = 16;
+constexpr int64_t kMaxPartialBytes = 256ll << 20;
+
+struct SplitPlan {
+    int64_t splits, k_split;
+};
+
+SplitPlan split_plan(int64_t tiles, int64_t M, int64_t N, int64_t K) {
+    SplitPlan p{1, K};
+    if (tiles >= kCus) return p;
+    int64_t s = std::min<int64_t>({ceil_div(kCus, tiles), K / (2 * kGemmBK), kMaxSplit,
+                                   kMaxPartialBytes / std::max<int64_t>(1, M * N * 4)});
+    if (s <= 1) return p;
+    p.k_split = round_up(ceil_div(K, s), kGemmBK);
+    p.splits = ceil_div(K, p.k_split);
+    return p;
+}
+
+// Partial-product bytes a launch of this shape needs (0 if it does not split).
+TileCfg pick_tile(int64_t M, int64_t N);
+
+size_t split_bytes(int64_t M, int64_t N, int64_t K) {
+    if (M == 0 || N == 0 || pick_tile(M, N) != kTile128x128) return 0;
+    const SplitPlan p = split_plan(ceil_div(M, 128) * ceil_div(N, 128), M, N, K);
+    return p.splits > 1 ? (size_t)(p.splits * M * N) * 4 : 0;
+}
+
+// Prefill tile configurations and a cost model to pick one: time ~ rounds
+// of concurrently resident tiles x tile area x tiles sharing a CU / relative
+// efficiency (measured: 256x256 tiles reach ~1.15x and 128x128 ~0.9x the
+// per-FLOP rate of 256x128).  128x128 fits two workgroups per CU.
+TileCfg pick_tile(int64_t M, int64_t N) {
+    struct C { int64_t bm, bn, per_cu; double eff; };
+    const C cfg[3] = {{256, 256, 1, 1.15}, {256, 128, 1, 1.0}, {128, 128, 2, 0.9}};
+    int best = 2;
+    double best_t = 1e300;
+    for (int i = 0; i < 3; ++i) {
+        const int64_t tiles = ceil_div(M, cfg[i].bm) * ceil_div(N, cfg[i].bn);
+        const int64_t rounds = ceil_div(tiles, kCus * cfg[i].per_cu);
+        const int64_t sharing = std::min(cfg[i].per_cu, ceil_div(tiles, kCus));
+        const double t = (double)rounds * cfg[i].bm * cfg[i].bn * sharing / cfg[i].eff;
+        if (t < best_t * 0.999) {
+            best_t = t;
+            best = i;
+        }
+    }
+    return (TileCfg)best;
+}
+
 template <typename T, bool BPACK, typename Epi>
 hipError_t launch_gemm(int site, const T* A, int64_t lda, int64_t M, const T* B, int64_t ldb,
-                       int64_t N, int64_t K, Epi epi, hipStream_t st) {
+                       int64_t N, int64_t K, Epi epi, float* partials, hipStream_t st) {
     if (M == 0 || N == 0) return hipSuccess;
     TimedLaunch timed(site, st);
-    const int64_t big = ceil_div(M, 256) * ceil_div(N, 128);
-    if (big >= kCus) {
-        hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 128, kGemmBK, 4, 2, BPACK, 2, Epi>), dim3((unsigned)big),
-                           dim3(8 * kWave), 0, st, A, lda, M, B, ldb, N, K, epi);
+    const TileCfg cfg = pick_tile(M, N);
+    if (cfg == kTile256x256) {
+        hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 256, kGemmBK, 2, 4, BPACK, 1, Epi>),
+                           dim3((unsigned)(ceil_div(M, 256) * ceil_div(N, 256))), dim3(8 * kWave), 0, st, A, lda,
+                           M, B, ldb, N, K, K, epi);
+    } else if (cfg == kTile256x128) {
+        hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 128, kGemmBK, 4, 2, BPACK, 2, Epi>),
+                           dim3((unsigned)(ceil_div(M, 256) * ceil_div(N, 128))), dim3(8 * kWave), 0, st, A, lda,
+                           M, B, ldb, N, K, K, epi);
     } else {
-        const int64_t small = ceil_div(M, 128) * ceil_div(N, 128);
-        hipLaunchKernelGGL((gemm_nt_mfma<T, 128, 128, kGemmBK, 4, 2, BPACK, 2, Epi>), dim3((unsigned)small),
-                           dim3(8 * kWave), 0, st, A, lda, M, B, ldb, N, K, epi);
+        // too few tiles for the chip even at 128 x 128: split K
+        const int64_t t128x128 = ceil_div(M, 128) * ceil_div(N, 128);
+        const SplitPlan p = partials ? split_plan(t128x128, M, N, K) : SplitPlan{1, K};
+        if (p.splits == 1) {
+            hipLaunchKernelGGL((gemm_nt_mfma<T, 128, 128, kGemmBK, 4, 2, BPACK, 2, Epi>), dim3((unsigned)t128x128),
+                               dim3(8 * kWave), 0, st, A, lda, M, B, ldb, N, K, K, epi);
+        } else {
+            SplitEpi se{partials, M, N};
+            hipLaunchKernelGGL((gemm_nt_mfma<T, 128, 128, kGemmBK, 4, 2, BPACK, 2, SplitEpi>),
+                               dim3((unsigned)t128x128, (unsigned)p.splits), dim3(8 * kWave), 0, st, A, lda, M,
+                               B, ldb, N, K, p.k_split, se);
+            const int64_t work = M * ceil_div(N, 4);
+            hipLaunchKernelGGL((split_reduce<Epi>), dim3((unsigned)std::min<int64_t>(ceil_div(work, 256), 65536)),
+                               dim3(256), 0, st, (const float*)partials, (int)p.splits, M, N, epi);
+        }
     }
     return hipGetLastError();
 }
@@ -176,27 +244,45 @@ hipError_t launch_gemm_f32(int site, const float* A, int64_t lda, int64_t M, con
     return hipGetLastError();
 }
 
+// Weight-streaming launches: MT 16-row activation tiles cover M = al.M.
 // B in lane order (layout.hpp), logical N x K.
+template <typename TB, int MT, typename AL, typename Epi>
+void skinny_packed_mt(const AL& al, const TB* B, int64_t N, int64_t K, const Epi& epi, hipStream_t st) {
+    constexpr int U = MT == 1 ? kSkinnyUnroll : 1;
+    hipLaunchKernelGGL((skinny_packed<TB, kSkinnyWaves, U, MT, AL, Epi>), dim3((unsigned)packed_groups(N)),
+                       dim3(kSkinnyWaves * kWave), 0, st, al, B, N, K, epi);
+}
+
 template <typename TB, typename AL, typename Epi>
 hipError_t launch_skinny_packed(int site, AL al, const TB* B, int64_t N, int64_t K, Epi epi,
                                 hipStream_t st) {
-    const int64_t groups = packed_groups(N);
-    if (groups == 0) return hipSuccess;
+    if (packed_groups(N) == 0) return hipSuccess;
     TimedLaunch timed(site, st);
-    hipLaunchKernelGGL((skinny_packed<TB, kSkinnyWaves, kSkinnyUnroll, AL, Epi>), dim3((unsigned)groups),
-                       dim3(kSkinnyWaves * kWave), 0, st, al, B, N, K, epi);
+    if (al.M <= 16) skinny_packed_mt<TB, 1>(al, B, N, K, epi, st);
+    else if (al.M <= 32) skinny_packed_mt<TB, 2>(al, B, N, K, epi, st);
+    else if (al.M <= 64) skinny_packed_mt<TB, 4>(al, B, N, K, epi, st);
+    else skinny_packed_mt<TB, 8>(al, B, N, K, epi, st);
     return hipGetLastError();
 }
 
 // B row-major with row stride ldb.
+template <typename TB, int MT, typename AL, typename Epi>
+void skinny_rowmajor_mt(const AL& al, const TB* B, int64_t ldb, int64_t N, int64_t K, const Epi& epi,
+                        hipStream_t st) {
+    constexpr int U = MT == 1 ? kSkinnyUnroll : 1;
+    hipLaunchKernelGGL((skinny_rowmajor<TB, kSkinnyWaves, U, MT, AL, Epi>), dim3((unsigned)ceil_div(N, kSkinnyRows)),
+                       dim3(kSkinnyWaves * kWave), 0, st, al, B, ldb, N, K, epi);
+}
+
 template <typename TB, typename AL, typename Epi>
 hipError_t launch_skinny_rowmajor(int site, AL al, const TB* B, int64_t ldb, int64_t N, int64_t K,
                                   Epi epi, hipStream_t st) {
-    const int64_t groups = ceil_div(N, kSkinnyRows);
-    if (groups == 0) return hipSuccess;
+    if (N == 0) return hipSuccess;
     TimedLaunch timed(site, st);
-    hipLaunchKernelGGL((skinny_rowmajor<TB, kSkinnyWaves, kSkinnyUnroll, AL, Epi>), dim3((unsigned)groups),
-                       dim3(kSkinnyWaves * kWave), 0, st, al, B, ldb, N, K, epi);
+    if (al.M <= 16) skinny_rowmajor_mt<TB, 1>(al, B, ldb, N, K, epi, st);
+    else if (al.M <= 32) skinny_rowmajor_mt<TB, 2>(al, B, ldb, N, K, epi, st);
+    else if (al.M <= 64) skinny_rowmajor_mt<TB, 4>(al, B, ldb, N, K, epi, st);
+    else skinny_rowmajor_mt<TB, 8>(al, B, ldb, N, K, epi, st);
     return hipGetLastError();
 }
 
@@ -243,6 +329,7 @@ pifa_status absmax_bf16_host(const void* src, int64_t n, float* out) {
 struct DeviceScratch {
     std::mutex mu;
     GrowBuf inter;  // intermediate X V^T of the stateless low-rank baseline
+    GrowBuf part;   // K-split partial products of stateless calls
 };
 
 DeviceScratch& device_scratch(int dev) {
@@ -281,6 +368,7 @@ struct pifa_layer {
     int* overflow = nullptr;
     int c_log2 = 0, y_log2 = 0;
     GrowBuf ws;                // Y_p hand-off
+    GrowBuf part;              // K-split partial products
 };
 
 struct lowrank_layer {
@@ -290,6 +378,7 @@ struct lowrank_layer {
     void* U = nullptr;  // bf16: lane order of d_out x r_pad; f32: d_out x r
     void* V = nullptr;  // bf16: lane order of r_pad x d_in; f32: r x d_in
     GrowBuf ws;
+    GrowBuf part;
 };
 
 struct dense_layer {
@@ -297,6 +386,7 @@ struct dense_layer {
     pifa_dtype dtype = PIFA_BF16;
     int64_t d_in = 0, d_out = 0;
     void* W = nullptr;  // bf16: lane order of d_out x d_in; f32: d_out x d_in
+    GrowBuf part;
 };
 
 namespace {
@@ -309,6 +399,7 @@ void free_layer(pifa_layer* h) {
     if (h->npiv) (void)hipFree(h->npiv);
     if (h->overflow) (void)hipFree(h->overflow);
     h->ws.release();
+    h->part.release();
     delete h;
 }
 
@@ -317,12 +408,14 @@ void free_lowrank(lowrank_layer* h) {
     if (h->U) (void)hipFree(h->U);
     if (h->V) (void)hipFree(h->V);
     h->ws.release();
+    h->part.release();
     delete h;
 }
 
 void free_dense(dense_layer* h) {
     if (!h) return;
     if (h->W) (void)hipFree(h->W);
+    h->part.release();
     delete h;
 }
 
@@ -330,6 +423,21 @@ size_t pifa_ws_bytes(const pifa_layer* h, int64_t M) {
     if (h->dtype == PIFA_F32) return (size_t)M * (size_t)h->r * 4;
     if (M <= kDecodeMaxM) return (size_t)M * (size_t)h->r_pad * 4;
     return (size_t)M * (size_t)h->r_pad * 2;
+}
+
+size_t pifa_part_bytes(const pifa_layer* h, int64_t M) {
+    if (h->dtype == PIFA_F32 || M <= kDecodeMaxM) return 0;
+    return std::max(split_bytes(M, h->r_pad, h->d_in), split_bytes(M, h->n_np, h->r_pad));
+}
+
+size_t lowrank_part_bytes(pifa_dtype dt, int64_t M, int64_t d_in, int64_t d_out, int64_t r_cols) {
+    if (dt == PIFA_F32 || M <= kDecodeMaxM) return 0;
+    return std::max(split_bytes(M, r_cols, d_in), split_bytes(M, d_out, r_cols));
+}
+
+size_t dense_part_bytes(pifa_dtype dt, int64_t M, int64_t d_in, int64_t d_out) {
+    if (dt == PIFA_F32 || M <= kDecodeMaxM) return 0;
+    return split_bytes(M, d_out, d_in);
 }
 
 size_t lowrank_ws_bytes(pifa_dtype dt, int64_t M, int64_t r_cols) {
@@ -342,7 +450,7 @@ size_t lowrank_ws_bytes(pifa_dtype dt, int64_t M, int64_t r_cols) {
 template <bool PACKED>
 pifa_status lowrank_run(pifa_dtype dt, const void* U, const void* V, const void* X, void* Y,
                         int64_t M, int64_t d_in, int64_t d_out, int64_t r_cols, void* T,
-                        hipStream_t st) {
+                        float* partials, hipStream_t st) {
     hipError_t e;
     if (dt == PIFA_F32) {
         float* t = (float*)T;
@@ -382,19 +490,19 @@ pifa_status lowrank_run(pifa_dtype dt, const void* U, const void* V, const void*
                                   r_cols, d_in,
                                   make_epi<bf16, kWsNone>(t, r_cols, nullptr, r_cols, 1.f, nullptr, 0,
                                                           0, 1.f, nullptr, M),
-                                  st);
+                                  partials, st);
     if (e != hipSuccess) return PIFA_ERR_HIP;
     e = launch_gemm<bf16, PACKED>(kSiteLowrankGemm2, t, r_cols, M, (const bf16*)U, r_cols, d_out, r_cols,
                                   make_epi<bf16, kWsNone>((bf16*)Y, d_out, nullptr, d_out, 1.f, nullptr,
                                                           0, 0, 1.f, nullptr, M),
-                                  st);
+                                  partials, st);
     return e == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
 }
 
 // Y = X W^T; W lane order (PACKED) or row-major.
 template <bool PACKED>
 pifa_status dense_run(pifa_dtype dt, const void* W, const void* X, void* Y, int64_t M, int64_t d_in,
-                      int64_t d_out, hipStream_t st) {
+                      int64_t d_out, float* partials, hipStream_t st) {
     hipError_t e;
     if (dt == PIFA_F32) {
         e = launch_gemm_f32(kSiteDenseF32, (const float*)X, d_in, M, (const float*)W, d_in, d_out, d_in,
@@ -414,7 +522,7 @@ pifa_status dense_run(pifa_dtype dt, const void* W, const void* X, void* Y, int6
         return e == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
     }
     e = launch_gemm<bf16, PACKED>(kSiteDenseGemm, (const bf16*)X, d_in, M, (const bf16*)W, d_in, d_out,
-                                  d_in, epi, st);
+                                  d_in, epi, partials, st);
     return e == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
 }
 
@@ -540,6 +648,12 @@ pifa_status pifa_layer_reserve(pifa_handle h, int64_t max_M) {
     const size_t need = std::max(pifa_ws_bytes(h, max_M), pifa_ws_bytes(h, std::min<int64_t>(max_M, kDecodeMaxM)));
     pifa_status s = h->ws.ensure(need, 0);
     if (s != PIFA_OK) return s;
+    // the split partials of every M up to max_M (they are not monotone in M)
+    size_t part = 0;
+    for (int64_t m = kDecodeMaxM + 1; m <= max_M; m = m < 4096 ? m + 1 : m * 2)
+        part = std::max(part, pifa_part_bytes(h, std::min(m, max_M)));
+    s = h->part.ensure(part, 0);
+    if (s != PIFA_OK) return s;
     return hipDeviceSynchronize() == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
 }
 
@@ -595,16 +709,16 @@ pifa_status pifa_forward(pifa_handle h, const void* X, void* Y, int64_t M, void*
     const float y_scale = std::ldexp(1.0f, h->y_log2);
     const float out_scale = std::ldexp(1.0f, -(h->y_log2 + h->c_log2));
     if (M <= kDecodeMaxM) {
-        float* yp = (float*)h->ws.ptr;
+        f16* yp = (f16*)h->ws.ptr;  // hi plane, then lo plane, M x r_pad each
         e = launch_skinny_packed<bf16>(kSitePifaGemv1, ALoad16<bf16>{(const bf16*)X, h->d_in, M},
                                        (const bf16*)h->Wp, h->r_pad, h->d_in,
-                                       make_epi<bf16, kWsF32>((bf16*)Y, h->d_out, h->piv, h->r, 1.f, yp,
-                                                              h->r_pad, h->r_pad, y_scale, h->overflow, M),
+                                       make_epi<bf16, kWsF16Pair>((bf16*)Y, h->d_out, h->piv, h->r, 1.f, yp,
+                                                                  h->r_pad, h->r_pad, y_scale, h->overflow, M),
                                        st);
         if (e != hipSuccess) return PIFA_ERR_HIP;
         if (h->n_np > 0) {
-            e = launch_skinny_packed<f16>(kSitePifaGemv2, ASplit32<f16>{yp, h->r_pad, M, y_scale},
-                                          (const f16*)h->C, h->n_np, h->r_pad,
+            e = launch_skinny_packed<f16>(kSitePifaGemv2, ALoadPair16{yp, h->r_pad, M}, (const f16*)h->C, h->n_np,
+                                          h->r_pad,
                                           make_epi<bf16, kWsNone>((bf16*)Y, h->d_out, h->npiv, h->n_np,
                                                                   out_scale, nullptr, 0, 0, 1.f, nullptr, M),
                                           st);
@@ -613,18 +727,21 @@ pifa_status pifa_forward(pifa_handle h, const void* X, void* Y, int64_t M, void*
         return PIFA_OK;
     }
 
+    s = h->part.ensure(pifa_part_bytes(h, M), st);
+    if (s != PIFA_OK) return s;
+    float* part = (float*)h->part.ptr;
     f16* yp = (f16*)h->ws.ptr;
     e = launch_gemm<bf16, true>(kSitePifaGemm1, (const bf16*)X, h->d_in, M, (const bf16*)h->Wp, 0, h->r_pad,
                                 h->d_in,
                                 make_epi<bf16, kWsF16>((bf16*)Y, h->d_out, h->piv, h->r, 1.f, yp, h->r_pad,
                                                        h->r_pad, y_scale, h->overflow, M),
-                                st);
+                                part, st);
     if (e != hipSuccess) return PIFA_ERR_HIP;
     if (h->n_np > 0) {
         e = launch_gemm<f16, true>(kSitePifaGemm2, yp, h->r_pad, M, (const f16*)h->C, 0, h->n_np, h->r_pad,
                                    make_epi<bf16, kWsNone>((bf16*)Y, h->d_out, h->npiv, h->n_np, out_scale,
                                                            nullptr, 0, 0, 1.f, nullptr, M),
-                                   st);
+                                   part, st);
         if (e != hipSuccess) return PIFA_ERR_HIP;
     }
     return PIFA_OK;
@@ -638,7 +755,14 @@ pifa_status dense_forward(const void* W, const void* X, void* Y, int64_t M, int6
     pifa_status s = check_rows_aligned(dtype, d_in);
     if (s != PIFA_OK) return s;
     if (dtype == PIFA_BF16 && (!aligned16(X) || !aligned16(W))) return PIFA_ERR_UNSUPPORTED;
-    return dense_run<false>(dtype, W, X, Y, M, d_in, d_out, as_stream(stream));
+    hipStream_t st = as_stream(stream);
+    int dev = 0;
+    PIFA_HIP(hipGetDevice(&dev));
+    DeviceScratch& ds = device_scratch(dev);
+    std::lock_guard<std::mutex> g(ds.mu);
+    s = ds.part.ensure(dense_part_bytes(dtype, M, d_in, d_out), st);
+    if (s != PIFA_OK) return s;
+    return dense_run<false>(dtype, W, X, Y, M, d_in, d_out, (float*)ds.part.ptr, st);
 }
 
 pifa_status dense_layer_create(const void* W, int64_t d_in, int64_t d_out, pifa_dtype dtype,
@@ -676,7 +800,22 @@ pifa_status dense_layer_forward(dense_handle h, const void* X, void* Y, int64_t 
     if (M == 0) return PIFA_OK;
     if (!X || !Y) return PIFA_ERR_INVALID_ARG;
     if (h->dtype == PIFA_BF16 && !aligned16(X)) return PIFA_ERR_UNSUPPORTED;
-    return dense_run<true>(h->dtype, h->W, X, Y, M, h->d_in, h->d_out, as_stream(stream));
+    hipStream_t st = as_stream(stream);
+    pifa_status s = h->part.ensure(dense_part_bytes(h->dtype, M, h->d_in, h->d_out), st);
+    if (s != PIFA_OK) return s;
+    if (h->dtype == PIFA_BF16)
+        return dense_run<true>(h->dtype, h->W, X, Y, M, h->d_in, h->d_out, (float*)h->part.ptr, st);
+    return dense_run<false>(h->dtype, h->W, X, Y, M, h->d_in, h->d_out, nullptr, st);
+}
+
+pifa_status dense_layer_reserve(dense_handle h, int64_t max_M) {
+    if (!h || max_M < 0) return PIFA_ERR_INVALID_ARG;
+    size_t part = 0;
+    for (int64_t m = kDecodeMaxM + 1; m <= max_M; m = m < 4096 ? m + 1 : m * 2)
+        part = std::max(part, dense_part_bytes(h->dtype, std::min(m, max_M), h->d_in, h->d_out));
+    pifa_status s = h->part.ensure(part, 0);
+    if (s != PIFA_OK) return s;
+    return hipDeviceSynchronize() == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
 }
 
 pifa_status dense_layer_destroy(dense_handle h) {
@@ -703,8 +842,10 @@ pifa_status lowrank_uv_forward(const void* U, const void* V, const void* X, void
     DeviceScratch& ds = device_scratch(dev);
     std::lock_guard<std::mutex> g(ds.mu);
     s = ds.inter.ensure(lowrank_ws_bytes(dtype, M, dims.r), st);
+    if (s == PIFA_OK) s = ds.part.ensure(lowrank_part_bytes(dtype, M, dims.d_in, dims.d_out, dims.r), st);
     if (s != PIFA_OK) return s;
-    return lowrank_run<false>(dtype, U, V, X, Y, M, dims.d_in, dims.d_out, dims.r, ds.inter.ptr, st);
+    return lowrank_run<false>(dtype, U, V, X, Y, M, dims.d_in, dims.d_out, dims.r, ds.inter.ptr,
+                              (float*)ds.part.ptr, st);
 }
 
 pifa_status lowrank_layer_create(const void* U, const void* V, pifa_dims dims, pifa_dtype dtype,
@@ -757,6 +898,11 @@ pifa_status lowrank_layer_reserve(lowrank_handle h, int64_t max_M) {
                                  lowrank_ws_bytes(h->dtype, std::min<int64_t>(max_M, kDecodeMaxM), h->r_pad));
     pifa_status s = h->ws.ensure(need, 0);
     if (s != PIFA_OK) return s;
+    size_t part = 0;
+    for (int64_t m = kDecodeMaxM + 1; m <= max_M; m = m < 4096 ? m + 1 : m * 2)
+        part = std::max(part, lowrank_part_bytes(h->dtype, std::min(m, max_M), h->d_in, h->d_out, h->r_pad));
+    s = h->part.ensure(part, 0);
+    if (s != PIFA_OK) return s;
     return hipDeviceSynchronize() == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
 }
 
@@ -767,10 +913,12 @@ pifa_status lowrank_layer_forward(lowrank_handle h, const void* X, void* Y, int6
     if (h->dtype == PIFA_BF16 && !aligned16(X)) return PIFA_ERR_UNSUPPORTED;
     hipStream_t st = as_stream(stream);
     pifa_status s = h->ws.ensure(lowrank_ws_bytes(h->dtype, M, h->r_pad), st);
+    if (s == PIFA_OK) s = h->part.ensure(lowrank_part_bytes(h->dtype, M, h->d_in, h->d_out, h->r_pad), st);
     if (s != PIFA_OK) return s;
     if (h->dtype == PIFA_BF16)
-        return lowrank_run<true>(h->dtype, h->U, h->V, X, Y, M, h->d_in, h->d_out, h->r_pad, h->ws.ptr, st);
-    return lowrank_run<false>(h->dtype, h->U, h->V, X, Y, M, h->d_in, h->d_out, h->r, h->ws.ptr, st);
+        return lowrank_run<true>(h->dtype, h->U, h->V, X, Y, M, h->d_in, h->d_out, h->r_pad, h->ws.ptr,
+                                 (float*)h->part.ptr, st);
+    return lowrank_run<false>(h->dtype, h->U, h->V, X, Y, M, h->d_in, h->d_out, h->r, h->ws.ptr, nullptr, st);
 }
 
 pifa_status lowrank_layer_destroy(lowrank_handle h) {

@@ -61,6 +61,7 @@ _SIGNATURES = {
     "dense_layer_create": (_st, [_vp, _i64, _i64, ctypes.c_int, ctypes.POINTER(_vp)]),
     "dense_layer_forward": (_st, [_vp, _vp, _vp, _i64, _vp]),
     "dense_layer_destroy": (_st, [_vp]),
+    "dense_layer_reserve": (_st, [_vp, _i64]),
     "lowrank_uv_forward": (_st, [_vp, _vp, _vp, _vp, _i64, pifa_dims, ctypes.c_int, _vp]),
     "lowrank_layer_create": (_st, [_vp, _vp, pifa_dims, ctypes.c_int, ctypes.POINTER(_vp)]),
     "lowrank_layer_forward": (_st, [_vp, _vp, _vp, _i64, _vp]),
@@ -213,6 +214,10 @@ def dense_layer_forward(handle: int, X, Y, M: int | None = None, stream=None) ->
     M = X.shape[0] if M is None else int(M)
     _check("dense_layer_forward", lib().dense_layer_forward(handle, _dev_ptr(X, "X"), _dev_ptr(Y, "Y"), M,
                                                             _stream(stream)))
+
+
+def dense_layer_reserve(handle: int, max_M: int) -> None:
+    _check("dense_layer_reserve", lib().dense_layer_reserve(handle, int(max_M)))
 
 
 def dense_layer_destroy(handle: int) -> None:

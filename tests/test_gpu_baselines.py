@@ -74,7 +74,7 @@ def test_baselines_config_b_shape(M):
 
 @pytest.mark.parametrize("dims", [(256, 256, 128), (136, 200, 33), (512, 1000, 410)])
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
-@pytest.mark.parametrize("M", [1, 16, 100])
+@pytest.mark.parametrize("M", [1, 16, 40, 100, 128])
 def test_baselines_ragged(dims, dtype, M):
     d_in, d_out, r = dims
     errs = _run_all(d_in, d_out, r, M, dtype, seed=d_out)

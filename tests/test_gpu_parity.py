@@ -18,7 +18,7 @@ from gpu_util import (DeviceLayer, activations, config_layer, from_dev, gaussian
 pytestmark = pytest.mark.gpu
 
 TOL = {"bf16": 5e-3, "f32": 1e-5}
-DECODE_AND_PREFILL_M = (1, 2, 7, 16, 17, 64, 129, 300)
+DECODE_AND_PREFILL_M = (1, 2, 7, 16, 17, 33, 64, 100, 128, 129, 300)
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -290,18 +290,23 @@ def test_pivot_set_invariance():
 
 
 def test_intermediate_overflow_is_counted():
-    """|Y_p * 2^s| beyond fp16's range is reported, not silently wrong."""
+    """|Y_p * 2^s| beyond fp16's range is reported, not silently wrong, on the
+    weight-streaming path (M <= 128) and on the GEMM path alike."""
     from paper_2501_19090_amd import pifa
     piv, npiv, Wp, C, _, _ = gaussian_layer(512, 768, 256, 4)
     lay = DeviceLayer(piv, npiv, Wp, C, "bf16")
     try:
         assert pifa.pifa_layer_overflow_count(lay.handle) == 0
         pifa.pifa_layer_set_intermediate_scale(lay.handle, 20)
-        for M in (4, 100):
+        seen = 0
+        for M in (4, 100, 300):
             x_dev, _ = activations(M, 512, 2, "bf16")
             y = from_dev(lay.forward(x_dev))
             assert not np.isfinite(y[:, lay.npiv]).all()
-        assert pifa.pifa_layer_overflow_count(lay.handle) > 0
+            assert np.isfinite(y[:, lay.piv]).all()
+            count = pifa.pifa_layer_overflow_count(lay.handle)
+            assert count > seen, M
+            seen = count
     finally:
         lay.close()
 
