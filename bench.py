@@ -14,9 +14,10 @@ weights rotated through more than the 256 MB Infinity Cache), the same-engine
 low-rank U V and dense baselines, the dominant kernel's roofline (timed live
 with HIP events on its launch stream) and the fp64 oracle timed on the host.
 
-The layer values are synthetic (timing does not depend on them): a seeded
-random pivot set with Gaussian W_p and C of the right shapes; the parity
-tests check the same kernels against layers built by the oracle.
+The layers are synthetic: Gaussian low-rank W' = U V (seeded), turned into
+PIFA form on the GPU by pifa_build_f64 (QR with column pivoting, timed and
+reported as build_ms), rounded to bf16; the dense and low-rank baselines use
+the same W' and U, V.
 """
 from __future__ import annotations
 
@@ -56,21 +57,30 @@ def dense_flops(M, d_in, d_out):
 
 
 class Workload:
-    """Device-resident synthetic PIFA, low-rank and dense layers of one shape."""
+    """Device-resident PIFA, low-rank and dense layers of one synthetic W' = U V."""
 
-    def __init__(self, d_in, d_out, r, seed, copies_for_decode=True):
+    def __init__(self, d_in, d_out, r, seed):
         import torch
         from paper_2501_19090_amd import inputs, pifa
         self.torch, self.pifa = torch, pifa
         self.d_in, self.d_out, self.r = d_in, d_out, r
         dev = torch.device("cuda:0")
-        piv, npiv, Wp, C = inputs.direct_layer(d_in, d_out, r, seed)
         U, V = inputs.lowrank_factors(d_out, d_in, r, seed)
-        bf = lambda a: torch.from_numpy(inputs.round_bf16(a)[0].view(np.int16)).to(dev).view(torch.bfloat16)
-        self.wp, self.c = bf(Wp), bf(C) if C.size else None
-        self.u, self.v = bf(U), bf(V)
-        del Wp, C
-        self.w = (self.u.float() @ self.v.float()).to(torch.bfloat16)  # dense baseline weight
+        U64 = torch.from_numpy(U).to(dev)
+        V64 = torch.from_numpy(V).to(dev)
+        del U, V
+        W64 = U64 @ V64
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        piv, npiv, Wp, C, report = pifa.pifa_build_f64(W64, r)
+        torch.cuda.synchronize()
+        self.build_ms = 1e3 * (time.perf_counter() - t0)
+        self.build_report = report.tolist()
+        self.wp, self.c = Wp.to(torch.bfloat16), (C.to(torch.bfloat16) if C.numel() else None)
+        self.u, self.v = U64.to(torch.bfloat16), V64.to(torch.bfloat16)
+        self.w = W64.to(torch.bfloat16)  # dense baseline weight
+        del W64, Wp, C, U64, V64
+        torch.cuda.empty_cache()
         self.piv, self.npiv = piv, npiv
         self.pifa_bytes = 2 * (r * d_in + (d_out - r) * r) + 4 * d_out
         self.uv_bytes = 2 * r * (d_in + d_out)
@@ -103,6 +113,8 @@ class Workload:
             self.pifa.pifa_layer_reserve(h, M)
         for h in self.uv_h:
             self.pifa.lowrank_layer_reserve(h, M)
+        for h in self.dense_h:
+            self.pifa.dense_layer_reserve(h, M)
 
     def close(self):
         for h in self.pifa_h:
@@ -210,13 +222,15 @@ def measure(wl: Workload, M: int, iters: int, warmup: int, rotate: bool):
     return res
 
 
-def cpu_baseline(d_in, d_out, r, seed, M_full, budget_s=10.0):
-    """The fp64 oracle's PIFA forward on a bounded row sample of the workload."""
+def cpu_baseline(wl, M_full, budget_s=10.0):
+    """The fp64 oracle's PIFA forward on a bounded row sample of the workload
+    (the same bf16 layer the GPU runs)."""
     import oracle
     from paper_2501_19090_amd import inputs
-    piv, npiv, Wp, C = inputs.direct_layer(d_in, d_out, r, seed)
-    Wp = inputs.round_bf16(Wp)[1]
-    C = inputs.round_bf16(C)[1]
+    d_in, d_out, r = wl.d_in, wl.d_out, wl.r
+    piv, npiv = wl.piv, wl.npiv
+    Wp = wl.wp.float().cpu().numpy().astype(np.float64)
+    C = wl.c.float().cpu().numpy().astype(np.float64)
     X = inputs.round_bf16(inputs.activations(M_full, d_in, 99))[1]
     threads = oracle.default_threads()
     rows = 16
@@ -338,12 +352,14 @@ def main():
               "uv_us": dec["uv_us"], "dense_us": dec["dense_us"],
               "speedup_vs_uv": dec["speedup_vs_uv"], "speedup_vs_dense": dec["speedup_vs_dense"],
               "weights_rotated": dec["weights_rotated"], "kernels": dec["kernels"]}
-    wl.close()
-
     cpu = None
     if not args.no_cpu:
-        cpu = cpu_baseline(d_in, d_out, r, seed, M)
+        cpu = cpu_baseline(wl, M)
         log("cpu baseline:", json.dumps(cpu))
+    build = {"ms": wl.build_ms, "report": wl.build_report,
+             "what": "pifa_build_f64 of the 4096x4096 rank-2048 W' on the GPU (fp64 QR with column pivoting "
+                     "+ coefficient solve)"}
+    wl.close()
 
     out = {
         "metric": METRIC, "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
@@ -360,6 +376,7 @@ def main():
         "prefill": {k: pre[k] for k in ("pifa_us", "uv_us", "dense_us", "pifa_tflops", "uv_tflops",
                                         "dense_tflops")},
         "decode": decode,
+        "build": build,
         "kernels": kernels,
         "paper_context": "arXiv 2501.19090 reports, on an NVIDIA RTX A6000 (d=8192, 65,536 rows), "
                          "24.2% memory saving and 24.6% lower time than the low-rank layer at r=d/2",
@@ -385,7 +402,7 @@ def run_full(args):
         for M in Ms:
             rotate = M <= 128
             res = measure(wl, M, 100 if rotate else 20, 10 if rotate else 3, rotate)
-            res.update({"config": name, "d_in": d_in, "d_out": d_out, "r": r,
+            res.update({"config": name, "d_in": d_in, "d_out": d_out, "r": r, "build_ms": wl.build_ms,
                         "pifa_weight_bytes": wl.pifa_bytes, "uv_weight_bytes": wl.uv_bytes,
                         "dense_weight_bytes": wl.dense_bytes,
                         "pifa_frac_mfma": res["pifa_tflops"] / PEAK_BF16_TFLOPS,

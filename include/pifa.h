@@ -46,7 +46,9 @@ typedef enum {
                                /* two sets do not partition [0, d_out)   */
     PIFA_ERR_UNSUPPORTED = -3, /* a shape or alignment this build lacks  */
     PIFA_ERR_HIP = -4,         /* a HIP runtime call or launch failed    */
-    PIFA_ERR_OOM = -5          /* device memory allocation failed        */
+    PIFA_ERR_OOM = -5,         /* device memory allocation failed        */
+    PIFA_ERR_NOT_RANK_R = -6   /* pifa_build_f64: W' is not numerically  */
+                               /* of rank r                              */
 } pifa_status;
 
 /* Layer shape: W is d_out x d_in with rank r, 1 <= r <= min(d_in, d_out)
@@ -171,6 +173,29 @@ pifa_status lowrank_layer_forward(lowrank_handle h, const void* X, void* Y, int6
                                   void* stream);
 pifa_status lowrank_layer_reserve(lowrank_handle h, int64_t max_M);
 pifa_status lowrank_layer_destroy(lowrank_handle h);
+
+/*
+ * Algorithm "Pivoting Factorization" (Sec. 3.2) on the GPU, in fp64: QR with
+ * column pivoting (Businger-Golub) on W'^T picks r pivot rows (largest
+ * residual norm first, ties to the lowest row index, residual norms
+ * recomputed exactly after every step), then C solves W_np = C W_p by least
+ * squares through the pivoted QR factors (C R11^T = R12^T).
+ *   W            device, d_out x d_in fp64, the rank-r matrix W' (read only)
+ *   W_p          device, r x d_in fp64 output: W'[pivot_idx, :]
+ *   C            device, (d_out - r) x r fp64 output (may be NULL if r = d_out);
+ *                columns follow pivot_idx
+ *   pivot_idx    host, r int32 output, sorted ascending
+ *   nonpivot_idx host, d_out - r int32 output, sorted ascending
+ *   report       host, 4 doubles or NULL: |R_00|, |R_{r-1,r-1}|, largest
+ *                residual column norm after r steps, 1.0 if certified
+ * W' must have numerical rank exactly r: |R_{r-1,r-1}| >= 1e-8 |R_00| and
+ * every residual norm <= 1e-10 |R_00|, else PIFA_ERR_NOT_RANK_R (outputs
+ * other than report are then unspecified).  Synchronous on `stream`;
+ * allocates and frees its own workspace (about (d_out + r) x max(d_in, r)
+ * doubles).
+ */
+pifa_status pifa_build_f64(const double* W, pifa_dims dims, double* W_p, double* C, int32_t* pivot_idx,
+                           int32_t* nonpivot_idx, double* report, void* stream);
 
 /*
  * Per-kernel timing.  While enabled, every kernel the library launches for a

@@ -1,0 +1,311 @@
+// PIFA build on the GPU (Algorithm "Pivoting Factorization", Sec. 3.2), fp64.
+//
+// QR with column pivoting (Businger & Golub) on A = W'^T: column j of A is
+// row j of W', so A is held as d_out contiguous columns of length d_in -- the
+// bytes of W' in row-major order.  Step k:
+//   qr_pivot_reflect (one workgroup): pick the column of largest residual
+//     norm (ties to the lowest original row index), swap it into position k,
+//     and turn A[k:, k] into a Householder reflector H = I - tau v v^T
+//     (v[0] = 1 implicit, v[1:] stored below the diagonal, R[k][k] on it);
+//   qr_apply (one wave per trailing column): a_j -= tau (v^T a_j) v and the
+//     residual norm ||a_j[k+1:]||^2 recomputed exactly in the same pass.
+// After r steps R11 (r x r, upper triangular) and R12 (r x (d_out - r)) sit in
+// the first r entries of the columns.  The coefficient matrix solves
+// W_p^T C^T = W_np^T in the least-squares sense through those factors:
+// C R11^T = R12^T (row by row a back substitution), done by
+// coeff_solve in blocks of 64 unknowns, each workgroup owning 64 rows of C.
+#pragma once
+
+#include "common.hpp"
+
+namespace pifa {
+
+constexpr int kBuildThreads = 1024;
+
+__device__ __forceinline__ double wave_sum(double v) {
+    for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    return v;
+}
+
+// A (d_out columns of length d_in) = W' rows; norm2[j] = ||A_j||^2; perm[j] = j.
+__global__ __launch_bounds__(256) void qr_init(const double* __restrict__ W, double* __restrict__ A,
+                                               double* __restrict__ norm2, int32_t* __restrict__ perm,
+                                               int64_t d_out, int64_t d_in) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t j = (int64_t)blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+    if (j >= d_out) return;
+    const double* w = W + j * d_in;
+    double* a = A + j * d_in;
+    double s = 0.0;
+    for (int64_t i = lane; i < d_in; i += kWave) {
+        const double x = w[i];
+        a[i] = x;
+        s += x * x;
+    }
+    s = wave_sum(s);
+    if (lane == 0) {
+        norm2[j] = s;
+        perm[j] = (int32_t)j;
+    }
+}
+
+// Step k, part 1 (a single workgroup of kBuildThreads threads).
+// scal[0] = tau_k; status[0] is set to 1 if the pivot column is zero.
+__global__ __launch_bounds__(kBuildThreads) void qr_pivot_reflect(double* __restrict__ A,
+                                                                  double* __restrict__ norm2,
+                                                                  int32_t* __restrict__ perm,
+                                                                  double* __restrict__ tau,
+                                                                  int* __restrict__ status, int64_t k,
+                                                                  int64_t d_out, int64_t d_in) {
+    __shared__ double s_val[kBuildThreads / kWave];
+    __shared__ int64_t s_idx[kBuildThreads / kWave];
+    __shared__ int32_t s_key[kBuildThreads / kWave];
+    __shared__ int64_t s_p;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+
+    // argmax of norm2[k..d_out), ties to the lowest original index perm[]
+    double bv = -1.0;
+    int64_t bi = -1;
+    int32_t bk = INT32_MAX;
+    for (int64_t j = k + tid; j < d_out; j += kBuildThreads) {
+        const double v = norm2[j];
+        const int32_t key = perm[j];
+        if (v > bv || (v == bv && key < bk)) {
+            bv = v;
+            bi = j;
+            bk = key;
+        }
+    }
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+        const double ov = __shfl_xor(bv, off);
+        const int64_t oi = __shfl_xor(bi, off);
+        const int32_t ok = __shfl_xor(bk, off);
+        if (ov > bv || (ov == bv && ok < bk)) {
+            bv = ov;
+            bi = oi;
+            bk = ok;
+        }
+    }
+    if (lane == 0) {
+        s_val[wave] = bv;
+        s_idx[wave] = bi;
+        s_key[wave] = bk;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        for (int w = 1; w < kBuildThreads / kWave; ++w)
+            if (s_val[w] > bv || (s_val[w] == bv && s_key[w] < bk)) {
+                bv = s_val[w];
+                bi = s_idx[w];
+                bk = s_key[w];
+            }
+        s_val[0] = bv;
+        s_idx[0] = bi;
+        s_key[0] = bk;
+    }
+    __syncthreads();
+    const int64_t p = s_idx[0];
+
+    // swap columns k and p
+    if (p != k) {
+        double* ak = A + k * d_in;
+        double* ap = A + p * d_in;
+        for (int64_t i = tid; i < d_in; i += kBuildThreads) {
+            const double t = ak[i];
+            ak[i] = ap[i];
+            ap[i] = t;
+        }
+        if (tid == 0) {
+            const int32_t tp = perm[k];
+            perm[k] = perm[p];
+            perm[p] = tp;
+            const double tn = norm2[k];
+            norm2[k] = norm2[p];
+            norm2[p] = tn;
+        }
+    }
+    __syncthreads();
+
+    // Householder reflector for x = A[k:, k]
+    double* x = A + k * d_in;
+    double s = 0.0;
+    for (int64_t i = k + tid; i < d_in; i += kBuildThreads) s += x[i] * x[i];
+    s = wave_sum(s);
+    __syncthreads();
+    if (lane == 0) s_val[wave] = s;
+    __syncthreads();
+    if (tid == 0) {
+        double t = 0.0;
+        for (int w = 0; w < kBuildThreads / kWave; ++w) t += s_val[w];
+        s_val[0] = t;
+    }
+    __syncthreads();
+    const double xnorm = sqrt(s_val[0]);
+    const double alpha = x[k];
+    if (xnorm == 0.0) {
+        if (tid == 0) {
+            status[0] = 1;
+            tau[k] = 0.0;
+        }
+        return;
+    }
+    const double beta = -copysign(xnorm, alpha);
+    const double inv = 1.0 / (alpha - beta);
+    __syncthreads();
+    for (int64_t i = k + 1 + tid; i < d_in; i += kBuildThreads) x[i] *= inv;
+    if (tid == 0) {
+        x[k] = beta;
+        tau[k] = (beta - alpha) / beta;
+    }
+}
+
+// Step k, part 2: one wave per trailing column j > k.
+__global__ __launch_bounds__(256) void qr_apply(double* __restrict__ A, double* __restrict__ norm2,
+                                                const double* __restrict__ tau, int64_t k, int64_t d_out,
+                                                int64_t d_in) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t j = k + 1 + (int64_t)blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+    if (j >= d_out) return;
+    const double* v = A + k * d_in;  // v[k] = 1 (implicit), v[k+1:] stored
+    double* a = A + j * d_in;
+    double w = 0.0;
+    for (int64_t i = k + 1 + lane; i < d_in; i += kWave) w += v[i] * a[i];
+    w = wave_sum(w) + a[k];
+    w *= tau[k];
+    if (lane == 0) a[k] -= w;
+    double s = 0.0;
+    for (int64_t i = k + 1 + lane; i < d_in; i += kWave) {
+        const double t = a[i] - w * v[i];
+        a[i] = t;
+        s += t * t;
+    }
+    s = wave_sum(s);
+    if (lane == 0) norm2[j] = s;
+}
+
+// R11 in row-major form: RT[s][t] = A_t[s] for s <= t < r, 0 below.
+__global__ void extract_r11(const double* __restrict__ A, double* __restrict__ RT, int64_t r, int64_t d_in) {
+    const int64_t total = r * r;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t s = e / r, t = e % r;
+        RT[e] = t >= s ? A[t * d_in + s] : 0.0;
+    }
+}
+
+// C (n_np x r) with C R11^T = R12^T, i.e. for each row q of C:
+//   sum_{t >= s} R11[s][t] c[t] = b[s],  b[s] = A_{r+q}[s]   (s < r),
+// solved from the last unknown up in blocks of 64.  Workgroup = 64 rows of
+// C, 256 threads; for each block: b' = b - C[:, after] R11[block, after]^T
+// (4 x 4 outputs per thread through LDS), then a 64 x 64 triangular solve.
+constexpr int kSolveRows = 64;
+constexpr int kSolveBlock = 64;
+constexpr int kSolveK = 16;
+
+__global__ __launch_bounds__(256) void coeff_solve(const double* __restrict__ A,
+                                                   const double* __restrict__ RT,
+                                                   double* __restrict__ C, int64_t r, int64_t n_np,
+                                                   int64_t d_in) {
+    __shared__ double sC[kSolveK][kSolveRows + 1];
+    __shared__ double sR[kSolveK][kSolveBlock + 1];
+    __shared__ double sB[kSolveRows][kSolveBlock + 1];
+    __shared__ double sD[kSolveBlock][kSolveBlock + 1];
+    const int tid = threadIdx.x;
+    const int tx = tid % 16, ty = tid / 16;  // 4 x 4 outputs: rows ty*4.., cols tx*4..
+    const int64_t q0 = (int64_t)blockIdx.x * kSolveRows;
+
+    const int64_t nblk = ceil_div(r, kSolveBlock);
+    for (int64_t blk = nblk - 1; blk >= 0; --blk) {
+        const int64_t s0 = blk * kSolveBlock;
+        const int64_t s1 = (s0 + kSolveBlock) < r ? (s0 + kSolveBlock) : r;
+        const int nb = (int)(s1 - s0);
+        // right-hand sides b[q][s] = A_{r+q}[s]
+        double acc[4][4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) acc[i][jj] = 0.0;
+        // acc[q][s] = sum_{t >= s1} C[q][t] * R11[s][t]
+        for (int64_t t0 = s1; t0 < r; t0 += kSolveK) {
+            for (int e = tid; e < kSolveK * kSolveRows; e += 256) {
+                const int kk = e % kSolveK, row = e / kSolveK;
+                const int64_t q = q0 + row, t = t0 + kk;
+                sC[kk][row] = (q < n_np && t < r) ? C[q * r + t] : 0.0;
+            }
+            for (int e = tid; e < kSolveK * kSolveBlock; e += 256) {
+                const int kk = e % kSolveK, col = e / kSolveK;
+                const int64_t s = s0 + col, t = t0 + kk;
+                sR[kk][col] = (s < s1 && t < r) ? RT[s * r + t] : 0.0;
+            }
+            __syncthreads();
+#pragma unroll
+            for (int kk = 0; kk < kSolveK; ++kk) {
+                double a[4], b[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) a[i] = sC[kk][ty * 4 + i];
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) b[jj] = sR[kk][tx * 4 + jj];
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int jj = 0; jj < 4; ++jj) acc[i][jj] = fma(a[i], b[jj], acc[i][jj]);
+            }
+            __syncthreads();
+        }
+        // b' = b - acc into LDS, plus the diagonal block of R11
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+                const int row = ty * 4 + i, col = tx * 4 + jj;
+                const int64_t q = q0 + row, s = s0 + col;
+                sB[row][col] = (q < n_np && s < s1) ? A[(r + q) * d_in + s] - acc[i][jj] : 0.0;
+            }
+        for (int e = tid; e < kSolveBlock * kSolveBlock; e += 256) {
+            const int a = e / kSolveBlock, b = e % kSolveBlock;
+            sD[a][b] = (a < nb && b < nb) ? RT[(s0 + a) * r + s0 + b] : 0.0;
+        }
+        __syncthreads();
+        // back substitution inside the block: thread `row` owns one row of C
+        if (tid < kSolveRows) {
+            const int row = tid;
+            for (int a = nb - 1; a >= 0; --a) {
+                double v = sB[row][a];
+                for (int b = a + 1; b < nb; ++b) v -= sD[a][b] * sB[row][b];
+                sB[row][a] = v / sD[a][a];
+            }
+        }
+        __syncthreads();
+        for (int e = tid; e < kSolveRows * kSolveBlock; e += 256) {
+            const int row = e / kSolveBlock, col = e % kSolveBlock;
+            const int64_t q = q0 + row, s = s0 + col;
+            if (q < n_np && s < s1) C[q * r + s] = sB[row][col];
+        }
+        __syncthreads();
+    }
+}
+
+// Outputs in sorted order: W_p[i] = W'[pivot_idx[i]], and
+// C_out[q][i] = C_sel[row_src[q]][col_src[i]].
+__global__ void gather_rows(const double* __restrict__ W, const int32_t* __restrict__ rows, double* __restrict__ out,
+                            int64_t n_rows, int64_t n_cols) {
+    const int64_t total = n_rows * n_cols;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t i = e / n_cols, c = e % n_cols;
+        out[e] = W[(int64_t)rows[i] * n_cols + c];
+    }
+}
+
+__global__ void gather_coeffs(const double* __restrict__ Csel, const int32_t* __restrict__ row_src,
+                              const int32_t* __restrict__ col_src, double* __restrict__ out, int64_t n_np,
+                              int64_t r) {
+    const int64_t total = n_np * r;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t q = e / r, i = e % r;
+        out[e] = Csel[(int64_t)row_src[q] * r + col_src[i]];
+    }
+}
+
+}  // namespace pifa

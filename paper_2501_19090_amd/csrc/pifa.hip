@@ -22,6 +22,7 @@
 #include "epilogue.hpp"
 #include "gemm_f32.hpp"
 #include "gemm_mfma.hpp"
+#include "build.hpp"
 #include "gemv_skinny.hpp"
 #include "layout.hpp"
 #include "prepack.hpp"
@@ -539,6 +540,7 @@ const char* pifa_status_string(pifa_status s) {
         case PIFA_ERR_UNSUPPORTED: return "PIFA_ERR_UNSUPPORTED";
         case PIFA_ERR_HIP: return "PIFA_ERR_HIP";
         case PIFA_ERR_OOM: return "PIFA_ERR_OOM";
+        case PIFA_ERR_NOT_RANK_R: return "PIFA_ERR_NOT_RANK_R";
     }
     return "PIFA_ERR_UNKNOWN";
 }
@@ -925,6 +927,101 @@ pifa_status lowrank_layer_destroy(lowrank_handle h) {
     if (!h) return PIFA_OK;
     (void)hipDeviceSynchronize();
     free_lowrank(h);
+    return PIFA_OK;
+}
+
+pifa_status pifa_build_f64(const double* W, pifa_dims dims, double* W_p, double* C, int32_t* pivot_idx,
+                           int32_t* nonpivot_idx, double* report, void* stream) {
+    pifa_status s = check_dims(dims);
+    if (s != PIFA_OK) return s;
+    const int64_t d_in = dims.d_in, d_out = dims.d_out, r = dims.r, n_np = d_out - r;
+    if (!W || !W_p || !pivot_idx || (n_np > 0 && (!C || !nonpivot_idx))) return PIFA_ERR_INVALID_ARG;
+    hipStream_t st = as_stream(stream);
+
+    struct Buf {
+        void* p = nullptr;
+        ~Buf() {
+            if (p) (void)hipFree(p);
+        }
+    } A, norm2, perm, tau, status, RT, Csel, diag, idx;
+    auto alloc = [](Buf& b, size_t bytes) { return hipMalloc(&b.p, bytes < 16 ? 16 : bytes) == hipSuccess; };
+    if (!alloc(A, (size_t)d_out * d_in * 8) || !alloc(norm2, (size_t)d_out * 8) ||
+        !alloc(perm, (size_t)d_out * 4) || !alloc(tau, (size_t)r * 8) || !alloc(status, 4) ||
+        !alloc(diag, (size_t)r * 8) || !alloc(idx, (size_t)(r + 2 * n_np + r) * 4))
+        return PIFA_ERR_OOM;
+    double* dA = (double*)A.p;
+    double* dn = (double*)norm2.p;
+    int32_t* dperm = (int32_t*)perm.p;
+    PIFA_HIP(hipMemsetAsync(status.p, 0, 4, st));
+
+    hipLaunchKernelGGL(qr_init, dim3((unsigned)ceil_div(d_out, 4)), dim3(256), 0, st, W, dA, dn, dperm, d_out, d_in);
+    for (int64_t k = 0; k < r; ++k) {
+        hipLaunchKernelGGL(qr_pivot_reflect, dim3(1), dim3(kBuildThreads), 0, st, dA, dn, dperm, (double*)tau.p,
+                           (int*)status.p, k, d_out, d_in);
+        if (k + 1 < d_out)
+            hipLaunchKernelGGL(qr_apply, dim3((unsigned)ceil_div(d_out - k - 1, 4)), dim3(256), 0, st, dA, dn,
+                               (const double*)tau.p, k, d_out, d_in);
+    }
+    PIFA_HIP(hipGetLastError());
+
+    // rank certification on the host: diagonal of R, residual norms
+    std::vector<int32_t> hperm((size_t)d_out);
+    std::vector<double> hdiag((size_t)r), hnorm((size_t)d_out);
+    int hstatus = 0;
+    for (int64_t k = 0; k < r; ++k)
+        PIFA_HIP(hipMemcpyAsync(&hdiag[(size_t)k], dA + k * d_in + k, 8, hipMemcpyDeviceToHost, st));
+    PIFA_HIP(hipMemcpyAsync(hperm.data(), dperm, (size_t)d_out * 4, hipMemcpyDeviceToHost, st));
+    PIFA_HIP(hipMemcpyAsync(hnorm.data(), dn, (size_t)d_out * 8, hipMemcpyDeviceToHost, st));
+    PIFA_HIP(hipMemcpyAsync(&hstatus, status.p, 4, hipMemcpyDeviceToHost, st));
+    PIFA_HIP(hipStreamSynchronize(st));
+    const double r00 = std::fabs(hdiag[0]), rlast = std::fabs(hdiag[(size_t)r - 1]);
+    double resid = 0.0;
+    for (int64_t j = r; j < d_out; ++j) resid = std::max(resid, std::sqrt(std::max(hnorm[(size_t)j], 0.0)));
+    const bool certified = hstatus == 0 && rlast >= 1e-8 * r00 && resid <= 1e-10 * r00;
+    if (report) {
+        report[0] = r00;
+        report[1] = rlast;
+        report[2] = resid;
+        report[3] = certified ? 1.0 : 0.0;
+    }
+    if (!certified) return PIFA_ERR_NOT_RANK_R;
+
+    // sorted index sets and the selection slot each came from
+    std::vector<std::pair<int32_t, int32_t>> piv((size_t)r), npv((size_t)n_np);
+    for (int64_t s2 = 0; s2 < r; ++s2) piv[(size_t)s2] = {hperm[(size_t)s2], (int32_t)s2};
+    for (int64_t t = 0; t < n_np; ++t) npv[(size_t)t] = {hperm[(size_t)(r + t)], (int32_t)t};
+    std::sort(piv.begin(), piv.end());
+    std::sort(npv.begin(), npv.end());
+    std::vector<int32_t> hidx((size_t)(r + 2 * n_np + r));
+    int32_t* rows_p = hidx.data();            // r: sorted pivot rows
+    int32_t* rows_np = rows_p + r;            // n_np: sorted non-pivot rows
+    int32_t* row_src = rows_np + n_np;        // n_np: selection slot of each sorted non-pivot
+    int32_t* col_src = row_src + n_np;        // r: selection slot of each sorted pivot
+    for (int64_t i = 0; i < r; ++i) {
+        rows_p[i] = piv[(size_t)i].first;
+        col_src[i] = piv[(size_t)i].second;
+        pivot_idx[i] = rows_p[i];
+    }
+    for (int64_t q = 0; q < n_np; ++q) {
+        rows_np[q] = npv[(size_t)q].first;
+        row_src[q] = npv[(size_t)q].second;
+        nonpivot_idx[q] = rows_np[q];
+    }
+    int32_t* didx = (int32_t*)idx.p;
+    PIFA_HIP(hipMemcpyAsync(didx, hidx.data(), hidx.size() * 4, hipMemcpyHostToDevice, st));
+
+    hipLaunchKernelGGL(gather_rows, dim3(grid_for(r * d_in)), dim3(256), 0, st, W, didx, W_p, r, d_in);
+    if (n_np > 0) {
+        if (!alloc(RT, (size_t)r * r * 8) || !alloc(Csel, (size_t)n_np * r * 8)) return PIFA_ERR_OOM;
+        hipLaunchKernelGGL(extract_r11, dim3(grid_for(r * r)), dim3(256), 0, st, (const double*)dA, (double*)RT.p, r,
+                           d_in);
+        hipLaunchKernelGGL(coeff_solve, dim3((unsigned)ceil_div(n_np, kSolveRows)), dim3(256), 0, st,
+                           (const double*)dA, (const double*)RT.p, (double*)Csel.p, r, n_np, d_in);
+        hipLaunchKernelGGL(gather_coeffs, dim3(grid_for(n_np * r)), dim3(256), 0, st, (const double*)Csel.p,
+                           didx + r + n_np, didx + r + 2 * n_np, C, n_np, r);
+    }
+    PIFA_HIP(hipGetLastError());
+    PIFA_HIP(hipStreamSynchronize(st));
     return PIFA_OK;
 }
 

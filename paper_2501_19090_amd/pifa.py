@@ -27,6 +27,7 @@ PIFA_ERR_BAD_INDEX = -2
 PIFA_ERR_UNSUPPORTED = -3
 PIFA_ERR_HIP = -4
 PIFA_ERR_OOM = -5
+PIFA_ERR_NOT_RANK_R = -6
 
 
 class pifa_dims(ctypes.Structure):
@@ -67,6 +68,7 @@ _SIGNATURES = {
     "lowrank_layer_forward": (_st, [_vp, _vp, _vp, _i64, _vp]),
     "lowrank_layer_reserve": (_st, [_vp, _i64]),
     "lowrank_layer_destroy": (_st, [_vp]),
+    "pifa_build_f64": (_st, [_vp, pifa_dims, _vp, _vp, _i32p, _i32p, ctypes.POINTER(ctypes.c_double), _vp]),
     "pifa_profile_enable": (_st, [ctypes.c_int]),
     "pifa_profile_reset": (_st, []),
     "pifa_profile_read": (_st, [ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(_i64),
@@ -255,6 +257,27 @@ def lowrank_layer_reserve(handle: int, max_M: int) -> None:
 
 def lowrank_layer_destroy(handle: int) -> None:
     _check("lowrank_layer_destroy", lib().lowrank_layer_destroy(handle))
+
+
+def pifa_build_f64(W, r: int, stream=None):
+    """Algorithm "Pivoting Factorization" on the GPU for a device fp64 W'
+    (d_out x d_in).  Returns (pivot_idx, nonpivot_idx, W_p, C, report) with
+    sorted numpy index arrays, device fp64 W_p / C, and the 4-entry report."""
+    import torch
+    if W.dtype != torch.float64:
+        raise TypeError("W must be float64")
+    d_out, d_in = W.shape
+    r = int(r)
+    Wp = torch.empty((r, d_in), dtype=torch.float64, device=W.device)
+    C = torch.empty((d_out - r, r), dtype=torch.float64, device=W.device)
+    piv = np.zeros(r, np.int32)
+    npiv = np.zeros(max(d_out - r, 0), np.int32)
+    report = (ctypes.c_double * 4)()
+    npp = npiv.ctypes.data_as(_i32p) if npiv.size else None
+    _check("pifa_build_f64", lib().pifa_build_f64(
+        _dev_ptr(W, "W"), pifa_dims(d_in, d_out, r), _dev_ptr(Wp, "W_p"), C.data_ptr() if C.numel() else None,
+        piv.ctypes.data_as(_i32p), npp, report, _stream(stream)))
+    return piv, npiv, Wp, C, np.array(list(report))
 
 
 def pifa_profile_enable(on: bool) -> None:
