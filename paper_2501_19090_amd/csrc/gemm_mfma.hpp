@@ -192,36 +192,54 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_nt_mfma(const T* __restric
     const int64_t nk = ceil_div(kend - kbeg, BK);
     // Tile t is staged in S[t % PGR].  Before iteration kt the LDS buffer
     // (kt & 1) holds tile kt and tiles kt+1 .. kt+PGR are in flight.
+    // The steady state has no data-dependent branches: loads past kend are
+    // masked (they return zeros), and the LDS store and fragment reads of
+    // the last iterations touch a buffer nobody reads again.  A branch here
+    // would make the compiler wait for every outstanding load at the join,
+    // which serialises the prefetch.
     gload(kbeg, S[0]);
-    if (PGR == 2 && nk > 1) gload(kbeg + BK, S[PGR - 1]);
+    if (PGR == 2) gload(kbeg + BK, S[PGR - 1]);
     sstore(0, S[0]);
-    if (nk > PGR) gload(kbeg + (int64_t)PGR * BK, S[0]);
+    gload(kbeg + (int64_t)PGR * BK, S[0]);
     __syncthreads();
     lds_frag(0, 0, 0);
+    // With EARLY, the one barrier per tile sits before the last MFMA step
+    // (after every wave has read its last fragments of this tile and written
+    // the next one), so the next tile's first fragments are read while the
+    // last MFMA step runs instead of after the barrier.
+    constexpr bool EARLY = PGR == 2;
     auto body = [&](int64_t kt, Stage& nxt) {  // nxt = S[(kt + 1) % PGR]
         const int cur = (int)(kt & 1);
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk) {
             const int slot = kk & 1;
             if (kk + 1 < KK) lds_frag(cur, kk + 1, slot ^ 1);
+            else if (EARLY) lds_frag(cur ^ 1, 0, slot ^ 1);
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
                 for (int j = 0; j < TN; ++j) acc[i][j] = Mfma<T>::mma32(fa[slot][i], fb[slot][j], acc[i][j]);
             // the other LDS buffer was last read before the previous barrier
-            if (kk == 0 && kt + 1 < nk) sstore(cur ^ 1, nxt);
-            if (kk == 1 && kt + 1 + PGR < nk) gload(kbeg + (kt + 1 + PGR) * BK, nxt);
+            if (kk == 0) sstore(cur ^ 1, nxt);
+            if (kk == 1) gload(kbeg + (kt + 1 + PGR) * BK, nxt);
+            if (EARLY && kk == KK - 2) __syncthreads();
         }
-        __syncthreads();
-        if (kt + 1 < nk) lds_frag(cur ^ 1, 0, 0);
+        if constexpr (EARLY) {
+            __builtin_amdgcn_iglp_opt(0);
+        } else {
+            __syncthreads();
+            lds_frag(cur ^ 1, 0, 0);
+        }
     };
     if constexpr (PGR == 1) {
         for (int64_t kt = 0; kt < nk; ++kt) body(kt, S[0]);
     } else {
-        for (int64_t kt = 0; kt < nk; kt += 2) {
+        int64_t kt = 0;
+        for (; kt + 1 < nk; kt += 2) {
             body(kt, S[PGR - 1]);
-            if (kt + 1 < nk) body(kt + 1, S[0]);
+            body(kt + 1, S[0]);
         }
+        if (kt < nk) body(kt, S[PGR - 1]);
     }
 
     // 32x32 accumulator layout: lane holds column (lane % 32) and rows
