@@ -63,6 +63,7 @@ typedef struct {
 typedef struct pifa_layer* pifa_handle;
 typedef struct lowrank_layer* lowrank_handle;
 typedef struct dense_layer* dense_handle;
+typedef struct pifa_group* pifa_group_handle;
 
 /* Human-readable name of a status code (static storage, never NULL). */
 const char* pifa_status_string(pifa_status s);
@@ -132,6 +133,55 @@ pifa_status pifa_layer_set_intermediate_scale(pifa_handle h, int log2_scale);
 /* Number of Y_p elements that overflowed fp16 since creation (synchronises
  * the device).  Always 0 for f32 layers. */
 pifa_status pifa_layer_overflow_count(pifa_handle h, int64_t* count);
+
+/*
+ * Grouped PIFA layers that read the same activations X (for example a
+ * transformer MLP's gate and up projections, or attention's q, k and v), with
+ * a rank of their own each (MPIFA_NS sets a density per module: appendix
+ * "Experiment Details", MPIFA_NS).  Evaluated together: one product X [W_p,1; W_p,2; ...]^T reads
+ * X once for every layer's pivot outputs, and one launch computes every
+ * layer's Y_np,i = Y_p,i C_i^T.
+ *   n             number of layers, 1 <= n <= 8.
+ *   W_p[i], C[i]  device pointers as for pifa_layer_create (C[i] may be NULL
+ *                 when r_i = d_out,i).
+ *   pivot_idx[i], nonpivot_idx[i]  host arrays as for pifa_layer_create,
+ *                 relative to layer i's own outputs [0, d_out,i).
+ *   dims[i]       all with the same d_in.
+ *   dtype         PIFA_BF16 only (PIFA_F32 returns PIFA_ERR_UNSUPPORTED).
+ * Everything is copied into memory the group owns (one concatenated W_p; no
+ * copy is kept twice).  Synchronises the device.
+ */
+pifa_status pifa_group_create(int n, const void* const* W_p, const void* const* C,
+                              const int32_t* const* pivot_idx, const int32_t* const* nonpivot_idx,
+                              const pifa_dims* dims, pifa_dtype dtype, pifa_group_handle* out);
+
+/* Release a group (synchronises the device).  NULL is OK. */
+pifa_status pifa_group_destroy(pifa_group_handle g);
+
+/* Pre-size the group's workspace for forwards of up to max_M rows. */
+pifa_status pifa_group_reserve(pifa_group_handle g, int64_t max_M);
+
+/*
+ * Y = [Y_1 | Y_2 | ... | Y_n]: layer i's Algorithm "PIFA Layer" output goes
+ * to columns [o_i, o_i + d_out,i) of Y, o_i = d_out,1 + ... + d_out,i-1.
+ *   X  device, M x d_in, bf16 (16-byte aligned), borrowed.
+ *   Y  device, M x (sum of d_out,i), bf16; every element is written.
+ * Each layer's result equals its own pifa_forward with the same intermediate
+ * scale: bit for bit for M <= 16, and up to the fp32 summation order of
+ * K-split products otherwise (the two calls may split K differently).  Same
+ * stream, workspace and overflow rules as pifa_forward; M = 0 returns
+ * PIFA_OK without launching.
+ */
+pifa_status pifa_group_forward(pifa_group_handle g, const void* X, void* Y, int64_t M, void* stream);
+
+/* Sum of pifa_layer_weight_bytes over the group's layers. */
+size_t pifa_group_weight_bytes(pifa_group_handle g);
+
+/* Intermediate scale exponent s for every layer of the group (-30..30). */
+pifa_status pifa_group_set_intermediate_scale(pifa_group_handle g, int log2_scale);
+
+/* fp16 hand-off overflows of the group since creation (synchronises). */
+pifa_status pifa_group_overflow_count(pifa_group_handle g, int64_t* count);
 
 /*
  * Dense baseline (Sec. 3.3, 2 m n b FLOPs): Y = X W^T.

@@ -148,6 +148,14 @@ def pifa_forward(X, pivot_idx, nonpivot_idx, Wp, C, d_out: int | None = None,
     return Y
 
 
+def group_forward(X, layers, threads: int | None = None) -> np.ndarray:
+    """Layers that read the same X, their outputs side by side: the block
+    [Y_1 | Y_2 | ...] with Y_i = Algorithm "PIFA Layer" of layer i.
+    layers: sequence of (pivot_idx, nonpivot_idx, Wp, C)."""
+    outs = [pifa_forward(X, piv, npiv, Wp, C, threads=threads) for piv, npiv, Wp, C in layers]
+    return np.concatenate(outs, axis=1) if outs else np.zeros((np.shape(X)[0], 0))
+
+
 def dense_forward(X, W, threads: int | None = None) -> np.ndarray:
     """Dense layer Y = X W^T in fp64."""
     lib = _load()

@@ -3,7 +3,8 @@
 // A kernel produces fp32 values acc(m, n) of a product with N columns and
 // hands each one to the epilogue, which
 //   * writes round(acc * out_scale) to out[m * ldo + idx[n]] for n < n_out
-//     (idx == nullptr means the identity map) -- this is the pivot /
+//     (idx == nullptr means the identity map; idx[n] < 0 means no output for
+//     column n, used for the padding rows of grouped layers) -- this is the pivot /
 //     non-pivot assignment of Algorithm "PIFA Layer" (its last two steps),
 //     fused into the producing kernel so there is no separate permutation pass;
 //   * optionally keeps a workspace copy ws[m * ldws + n] for n < n_ws, as fp16
@@ -44,6 +45,10 @@ struct ScatterEpi {
         c.n = n;
         c.out_ok = n < n_out;
         c.dst = c.out_ok ? (idx ? (int64_t)idx[n] : n) : 0;
+        if (c.dst < 0) {  // a padding column of a grouped layer: no output
+            c.out_ok = false;
+            c.dst = 0;
+        }
         c.ws_ok = (WS != kWsNone) && n < n_ws;
         return c;
     }

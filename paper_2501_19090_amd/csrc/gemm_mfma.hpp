@@ -61,17 +61,25 @@ struct Mfma<f16> {
 constexpr int kXcds = 8;
 constexpr int kGroupM = 8;
 
-__device__ __forceinline__ void tile_coords(int64_t bid, int64_t tiles_m, int64_t tiles_n,
-                                            int64_t& tm, int64_t& tn) {
-    const int64_t ntiles = tiles_m * tiles_n;
-    int64_t t = bid;
-    if (ntiles % kXcds == 0) t = (bid % kXcds) * (ntiles / kXcds) + bid / kXcds;
+// Step 1 on its own: consecutive ids of one XCD become a contiguous range.
+__device__ __forceinline__ int64_t xcd_remap(int64_t bid, int64_t ntiles) {
+    return ntiles % kXcds == 0 ? (bid % kXcds) * (ntiles / kXcds) + bid / kXcds : bid;
+}
+
+// Step 2 on its own: tile t of a tiles_m x tiles_n grid, in bands of kGroupM tile rows.
+__device__ __forceinline__ void band_coords(int64_t t, int64_t tiles_m, int64_t tiles_n, int64_t& tm,
+                                            int64_t& tn) {
     const int64_t band = (int64_t)kGroupM * tiles_n;
     const int64_t first_m = (t / band) * kGroupM;
     const int64_t rows = (tiles_m - first_m) < kGroupM ? (tiles_m - first_m) : kGroupM;
     const int64_t in_band = t % band;
     tm = first_m + in_band % rows;
     tn = in_band / rows;
+}
+
+__device__ __forceinline__ void tile_coords(int64_t bid, int64_t tiles_m, int64_t tiles_n,
+                                            int64_t& tm, int64_t& tn) {
+    band_coords(xcd_remap(bid, tiles_m * tiles_n), tiles_m, tiles_n, tm, tn);
 }
 
 // Offset past every buffer range: the load returns 0 without a branch.
@@ -83,14 +91,13 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc31(const void* base, 
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, 0x00020000);
 }
 
-// K splitting: workgroup (tile, blockIdx.y = s) reduces K range
-// [s * k_split, min(K, (s + 1) * k_split)); k_split is a multiple of BK
-// (k_split >= K: no split).  Both operands are masked outside that range.
+// One output tile (tm, tn) over the K range [kbeg, kend); both operands are
+// masked outside that range.
 template <typename T, int BM, int BN, int BK, int WM, int WN, bool BPACK, int PGR, typename Epi>
-__global__ __launch_bounds__(WM* WN* kWave) void gemm_nt_mfma(const T* __restrict__ A, int64_t lda,
-                                                             int64_t M, const T* __restrict__ B,
-                                                             int64_t ldb, int64_t N, int64_t K,
-                                                             int64_t k_split, Epi epi) {
+__device__ __forceinline__ void gemm_nt_tile(const T* __restrict__ A, int64_t lda, int64_t M,
+                                             const T* __restrict__ B, int64_t ldb, int64_t N, int64_t K,
+                                             int64_t kbeg, int64_t kend, int64_t tm, int64_t tn,
+                                             const Epi& epi) {
     constexpr int NT = WM * WN * kWave;
     constexpr int LDK = BK + 8;  // padded LDS row, in elements
     constexpr int CPR = BK / 8;  // 16-byte chunks per tile row
@@ -109,9 +116,6 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_nt_mfma(const T* __restric
     __shared__ __attribute__((aligned(16))) T As[2][BM * LDK];
     __shared__ __attribute__((aligned(16))) T Bs[2][BN * LDK];
 
-    const int64_t tiles_m = ceil_div(M, BM), tiles_n = ceil_div(N, BN);
-    int64_t tm, tn;
-    tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn);
     const int64_t m0 = tm * BM, n0 = tn * BN;
 
     const auto ars = make_rsrc31(A + m0 * lda, ((M - m0 - 1) * lda + K) * (int64_t)sizeof(T));
@@ -124,8 +128,6 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_nt_mfma(const T* __restric
     const int lane = tid & (kWave - 1);
     const int wave = tid / kWave;
     const int wm = wave / WN, wn = wave % WN;
-    const int64_t kbeg = (int64_t)blockIdx.y * k_split;
-    const int64_t kend = (kbeg + k_split) < K ? (kbeg + k_split) : K;
 
     struct Stage {
         u32x4 a[A_CH], b[B_CH];
@@ -254,6 +256,55 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_nt_mfma(const T* __restric
             for (int v = 0; v < 16; ++v) epi.store(mb + 8 * (v >> 2) + (v & 3), c, acc[i][j][v]);
         }
     }
+}
+
+// K splitting: workgroup (tile, blockIdx.y = s) reduces K range
+// [s * k_split, min(K, (s + 1) * k_split)); k_split is a multiple of BK
+// (k_split >= K: no split).
+template <typename T, int BM, int BN, int BK, int WM, int WN, bool BPACK, int PGR, typename Epi>
+__global__ __launch_bounds__(WM* WN* kWave) void gemm_nt_mfma(const T* __restrict__ A, int64_t lda,
+                                                             int64_t M, const T* __restrict__ B,
+                                                             int64_t ldb, int64_t N, int64_t K,
+                                                             int64_t k_split, Epi epi) {
+    int64_t tm, tn;
+    tile_coords(blockIdx.x, ceil_div(M, BM), ceil_div(N, BN), tm, tn);
+    const int64_t kbeg = (int64_t)blockIdx.y * k_split;
+    const int64_t kend = (kbeg + k_split) < K ? (kbeg + k_split) : K;
+    gemm_nt_tile<T, BM, BN, BK, WM, WN, BPACK, PGR, Epi>(A, lda, M, B, ldb, N, K, kbeg, kend, tm, tn, epi);
+}
+
+// Several products with the same M in one launch (grouped layers): problem
+// g owns workgroups [tile_start[g], tile_start[g + 1]) of the XCD-remapped
+// id space; B is in lane order.
+constexpr int kMaxGroup = 8;
+
+template <typename T, typename Epi>
+struct GemmProblem {
+    const T* A;
+    int64_t lda;
+    const T* B;
+    int64_t N, K;
+    Epi epi;
+};
+
+template <typename T, typename Epi>
+struct GemmGroup {
+    GemmProblem<T, Epi> p[kMaxGroup];
+    int64_t tile_start[kMaxGroup + 1];
+    int64_t M;
+    int n;
+};
+
+template <typename T, int BM, int BN, int BK, int WM, int WN, int PGR, typename Epi>
+__global__ __launch_bounds__(WM* WN* kWave) void gemm_nt_grouped(GemmGroup<T, Epi> grp) {
+    const int64_t t = xcd_remap(blockIdx.x, grp.tile_start[grp.n]);
+    int g = 0;
+    while (g + 1 < grp.n && t >= grp.tile_start[g + 1]) ++g;
+    const GemmProblem<T, Epi>& p = grp.p[g];
+    int64_t tm, tn;
+    band_coords(t - grp.tile_start[g], ceil_div(grp.M, BM), ceil_div(p.N, BN), tm, tn);
+    gemm_nt_tile<T, BM, BN, BK, WM, WN, true, PGR, Epi>(p.A, p.lda, grp.M, p.B, 0, p.N, p.K, 0, p.K, tm, tn,
+                                                       p.epi);
 }
 
 // Epilogue of a K-split launch: the fp32 partial tile of split s goes to

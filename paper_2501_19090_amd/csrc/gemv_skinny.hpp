@@ -107,14 +107,14 @@ __device__ __forceinline__ void skinny_finish(const f32x4 (&acc)[MT], int64_t n0
     for (int v = 0; v < 4; ++v) epi.store(16 * wave + 4 * (lane >> 4) + v, c, tot[v]);
 }
 
-// Weights in lane order (layout.hpp): B holds packed_elems(N, K) elements.
+// Weights in lane order (layout.hpp): B holds packed_elems(N, K) elements;
+// this workgroup owns 16-row group g of B.
 template <typename TB, int WAVES, int UNROLL, int MT, typename AL, typename Epi>
-__global__ __launch_bounds__(WAVES* kWave) void skinny_packed(AL al, const TB* __restrict__ B,
-                                                             int64_t N, int64_t K, Epi epi) {
+__device__ __forceinline__ void skinny_packed_group(const AL& al, const TB* __restrict__ B, int64_t K,
+                                                    const Epi& epi, int64_t g) {
     constexpr int OPS = AL::kOps;
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
-    const int64_t g = blockIdx.x;
     const int64_t KB = packed_kblocks(K);
     const u32x4* blk = reinterpret_cast<const u32x4*>(B) + g * KB * kPackChunks;
     const int row = lane & 15;
@@ -144,6 +144,41 @@ __global__ __launch_bounds__(WAVES* kWave) void skinny_packed(AL al, const TB* _
                 }
     }
     skinny_finish<WAVES, MT>(acc, g * kSkinnyRows, epi);
+}
+
+template <typename TB, int WAVES, int UNROLL, int MT, typename AL, typename Epi>
+__global__ __launch_bounds__(WAVES* kWave) void skinny_packed(AL al, const TB* __restrict__ B,
+                                                             int64_t N, int64_t K, Epi epi) {
+    (void)N;
+    skinny_packed_group<TB, WAVES, UNROLL, MT, AL, Epi>(al, B, K, epi, blockIdx.x);
+}
+
+// Several weight streams with the same activation rows in one launch
+// (grouped layers): problem p owns workgroups [start[p], start[p + 1]).
+constexpr int kMaxSkinnyGroup = 8;
+
+template <typename TB, typename AL, typename Epi>
+struct SkinnyProblem {
+    AL al;
+    const TB* B;
+    int64_t K;
+    Epi epi;
+};
+
+template <typename TB, typename AL, typename Epi>
+struct SkinnyGroup {
+    SkinnyProblem<TB, AL, Epi> p[kMaxSkinnyGroup];
+    int64_t start[kMaxSkinnyGroup + 1];
+    int n;
+};
+
+template <typename TB, int WAVES, int UNROLL, int MT, typename AL, typename Epi>
+__global__ __launch_bounds__(WAVES* kWave) void skinny_packed_grouped(SkinnyGroup<TB, AL, Epi> grp) {
+    const int64_t b = blockIdx.x;
+    int q = 0;
+    while (q + 1 < grp.n && b >= grp.start[q + 1]) ++q;
+    const SkinnyProblem<TB, AL, Epi>& p = grp.p[q];
+    skinny_packed_group<TB, WAVES, UNROLL, MT, AL, Epi>(p.al, p.B, p.K, p.epi, b - grp.start[q]);
 }
 
 // Row-major weights (row stride ldb), for caller-owned matrices.

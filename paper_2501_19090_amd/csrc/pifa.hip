@@ -87,6 +87,10 @@ enum Site {
     kSiteLowrankGemv1,
     kSiteLowrankGemv2,
     kSiteLowrankF32,
+    kSiteGroupGemm1,
+    kSiteGroupGemm2,
+    kSiteGroupGemv1,
+    kSiteGroupGemv2,
     kSiteCount
 };
 
@@ -94,7 +98,8 @@ const char* const kSiteNames[kSiteCount] = {
     "pifa_gemm1_xwp",      "pifa_gemm2_ypc",      "pifa_gemv1_xwp",      "pifa_gemv2_ypc",
     "pifa_f32_gemm1",      "pifa_f32_gemm2",      "dense_gemm",          "dense_gemv",
     "dense_f32",           "lowrank_gemm1_xv",    "lowrank_gemm2_tu",    "lowrank_gemv1_xv",
-    "lowrank_gemv2_tu",    "lowrank_f32"};
+    "lowrank_gemv2_tu",    "lowrank_f32",         "pifa_group_gemm1",    "pifa_group_gemm2",
+    "pifa_group_gemv1",    "pifa_group_gemv2"};
 
 struct Profiler {
     std::mutex mu;
@@ -266,6 +271,45 @@ hipError_t launch_skinny_packed(int site, AL al, const TB* B, int64_t N, int64_t
     return hipGetLastError();
 }
 
+// Grouped prefill products (same M, B in lane order): one launch, the tile
+// shape picked for the group's total width.
+template <int BM, int BN, int WM, int WN, int PGR, typename T, typename Epi>
+hipError_t launch_grouped_cfg(GemmGroup<T, Epi> grp, hipStream_t st) {
+    grp.tile_start[0] = 0;
+    for (int g = 0; g < grp.n; ++g)
+        grp.tile_start[g + 1] = grp.tile_start[g] + ceil_div(grp.M, BM) * ceil_div(grp.p[g].N, BN);
+    if (grp.tile_start[grp.n] == 0) return hipSuccess;
+    hipLaunchKernelGGL((gemm_nt_grouped<T, BM, BN, kGemmBK, WM, WN, PGR, Epi>),
+                       dim3((unsigned)grp.tile_start[grp.n]), dim3(WM * WN * kWave), 0, st, grp);
+    return hipGetLastError();
+}
+
+template <typename T, typename Epi>
+hipError_t launch_gemm_grouped(int site, const GemmGroup<T, Epi>& grp, hipStream_t st) {
+    int64_t n_total = 0;
+    for (int g = 0; g < grp.n; ++g) n_total += grp.p[g].N;
+    if (grp.M == 0 || n_total == 0) return hipSuccess;
+    TimedLaunch timed(site, st);
+    switch (pick_tile(grp.M, n_total)) {
+        case kTile256x256: return launch_grouped_cfg<256, 256, 2, 4, 1>(grp, st);
+        case kTile256x128: return launch_grouped_cfg<256, 128, 4, 2, 2>(grp, st);
+        default: return launch_grouped_cfg<128, 128, 4, 2, 2>(grp, st);
+    }
+}
+
+// Grouped weight streams for decode-sized M (at most 16 rows).
+template <typename TB, typename AL, typename Epi>
+hipError_t launch_skinny_grouped(int site, SkinnyGroup<TB, AL, Epi> grp, const int64_t* n_rows,
+                                 hipStream_t st) {
+    grp.start[0] = 0;
+    for (int q = 0; q < grp.n; ++q) grp.start[q + 1] = grp.start[q] + packed_groups(n_rows[q]);
+    if (grp.start[grp.n] == 0) return hipSuccess;
+    TimedLaunch timed(site, st);
+    hipLaunchKernelGGL((skinny_packed_grouped<TB, kSkinnyWaves, kSkinnyUnroll, 1, AL, Epi>),
+                       dim3((unsigned)grp.start[grp.n]), dim3(kSkinnyWaves * kWave), 0, st, grp);
+    return hipGetLastError();
+}
+
 // B row-major with row stride ldb.
 template <typename TB, int MT, typename AL, typename Epi>
 void skinny_rowmajor_mt(const AL& al, const TB* B, int64_t ldb, int64_t N, int64_t K, const Epi& epi,
@@ -390,6 +434,23 @@ struct dense_layer {
     GrowBuf part;
 };
 
+// Layers that share X.  The members keep their C, non-pivot indices (already
+// offset into the group's output) and C scale; their W_p blocks are moved
+// into one concatenated lane-order W_p, so nothing is stored twice.
+struct pifa_group {
+    int device = 0;
+    int n = 0;
+    int64_t d_in = 0, d_out = 0, r_pad = 0;  // d_out, r_pad: sums over the members
+    std::vector<pifa_layer*> layers;
+    std::vector<int64_t> r_off;  // first W_p row (and Y_p column) of each member
+    void* Wp = nullptr;          // lane order of r_pad x d_in
+    int32_t* piv = nullptr;      // r_pad: output column of each W_p row, -1 on padding rows
+    int* overflow = nullptr;
+    int y_log2 = 0;
+    GrowBuf ws;
+    GrowBuf part;
+};
+
 namespace {
 
 void free_layer(pifa_layer* h) {
@@ -411,6 +472,25 @@ void free_lowrank(lowrank_layer* h) {
     h->ws.release();
     h->part.release();
     delete h;
+}
+
+void free_group(pifa_group* g) {
+    if (!g) return;
+    for (pifa_layer* h : g->layers) free_layer(h);
+    if (g->Wp) (void)hipFree(g->Wp);
+    if (g->piv) (void)hipFree(g->piv);
+    if (g->overflow) (void)hipFree(g->overflow);
+    g->ws.release();
+    g->part.release();
+    delete g;
+}
+
+size_t group_ws_bytes(const pifa_group* g, int64_t M) {
+    return (size_t)M * (size_t)g->r_pad * (M <= kDecodeMaxM ? 4 : 2);
+}
+
+size_t group_part_bytes(const pifa_group* g, int64_t M) {
+    return M <= kDecodeMaxM ? 0 : split_bytes(M, g->r_pad, g->d_in);
 }
 
 void free_dense(dense_layer* h) {
@@ -565,9 +645,24 @@ pifa_status pifa_validate_partition(const int32_t* pivot_idx, const int32_t* non
     return PIFA_OK;  // d_out distinct in-range values: an exact partition
 }
 
-pifa_status pifa_layer_create(const void* W_p, const void* C, const int32_t* pivot_idx,
-                              const int32_t* nonpivot_idx, pifa_dims dims, pifa_dtype dtype,
-                              pifa_handle* out) {
+}  // extern "C"
+
+namespace {
+
+// Copy n host indices to a new device array, adding `offset` to each.
+pifa_status upload_indices(const int32_t* src, int64_t n, int64_t offset, int32_t** dst) {
+    std::vector<int32_t> tmp((size_t)n);
+    for (int64_t i = 0; i < n; ++i) tmp[(size_t)i] = (int32_t)(src[i] + offset);
+    if (hipMalloc(dst, (size_t)n * sizeof(int32_t)) != hipSuccess) return PIFA_ERR_OOM;
+    PIFA_HIP(hipMemcpy(*dst, tmp.data(), (size_t)n * sizeof(int32_t), hipMemcpyHostToDevice));
+    return PIFA_OK;
+}
+
+// pifa_layer_create with every output index shifted by out_offset (the
+// layer's column offset inside a group's output; 0 for a plain layer).
+pifa_status create_layer(const void* W_p, const void* C, const int32_t* pivot_idx,
+                         const int32_t* nonpivot_idx, pifa_dims dims, pifa_dtype dtype, int64_t out_offset,
+                         pifa_layer** out) {
     if (!out) return PIFA_ERR_INVALID_ARG;
     *out = nullptr;
     if (!valid_dtype(dtype)) return PIFA_ERR_INVALID_ARG;
@@ -603,17 +698,14 @@ pifa_status pifa_layer_create(const void* W_p, const void* C, const int32_t* piv
             : pack_rowmajor_f32(W_p, h->r, h->d_in, h->Wp, h->r, h->d_in)) != hipSuccess)
         return fail(PIFA_ERR_HIP);
 
-    if (hipMalloc(&h->piv, (size_t)h->r * sizeof(int32_t)) != hipSuccess) return fail(PIFA_ERR_OOM);
-    if (hipMemcpy(h->piv, pivot_idx, (size_t)h->r * sizeof(int32_t), hipMemcpyHostToDevice) != hipSuccess)
-        return fail(PIFA_ERR_HIP);
+    s = upload_indices(pivot_idx, h->r, out_offset, &h->piv);
+    if (s != PIFA_OK) return fail(s);
     if (hipMalloc(&h->overflow, sizeof(int)) != hipSuccess) return fail(PIFA_ERR_OOM);
     if (hipMemset(h->overflow, 0, sizeof(int)) != hipSuccess) return fail(PIFA_ERR_HIP);
 
     if (n_np > 0) {
-        if (hipMalloc(&h->npiv, (size_t)n_np * sizeof(int32_t)) != hipSuccess) return fail(PIFA_ERR_OOM);
-        if (hipMemcpy(h->npiv, nonpivot_idx, (size_t)n_np * sizeof(int32_t), hipMemcpyHostToDevice) !=
-            hipSuccess)
-            return fail(PIFA_ERR_HIP);
+        s = upload_indices(nonpivot_idx, n_np, out_offset, &h->npiv);
+        if (s != PIFA_OK) return fail(s);
         if (!bf) {
             if (hipMalloc(&h->C, (size_t)n_np * h->r * 4) != hipSuccess) return fail(PIFA_ERR_OOM);
             if (pack_rowmajor_f32(C, n_np, h->r, h->C, n_np, h->r) != hipSuccess) return fail(PIFA_ERR_HIP);
@@ -636,6 +728,16 @@ pifa_status pifa_layer_create(const void* W_p, const void* C, const int32_t* piv
     if (hipDeviceSynchronize() != hipSuccess) return fail(PIFA_ERR_HIP);
     *out = h;
     return PIFA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+pifa_status pifa_layer_create(const void* W_p, const void* C, const int32_t* pivot_idx,
+                              const int32_t* nonpivot_idx, pifa_dims dims, pifa_dtype dtype,
+                              pifa_handle* out) {
+    return create_layer(W_p, C, pivot_idx, nonpivot_idx, dims, dtype, 0, out);
 }
 
 pifa_status pifa_layer_destroy(pifa_handle h) {
@@ -928,6 +1030,167 @@ pifa_status lowrank_layer_destroy(lowrank_handle h) {
     (void)hipDeviceSynchronize();
     free_lowrank(h);
     return PIFA_OK;
+}
+
+pifa_status pifa_group_create(int n, const void* const* W_p, const void* const* C,
+                              const int32_t* const* pivot_idx, const int32_t* const* nonpivot_idx,
+                              const pifa_dims* dims, pifa_dtype dtype, pifa_group_handle* out) {
+    if (!out) return PIFA_ERR_INVALID_ARG;
+    *out = nullptr;
+    if (n < 1 || n > kMaxGroup || !W_p || !pivot_idx || !dims || !valid_dtype(dtype)) return PIFA_ERR_INVALID_ARG;
+    if (dtype != PIFA_BF16) return PIFA_ERR_UNSUPPORTED;
+    for (int i = 0; i < n; ++i) {
+        pifa_status s = check_dims(dims[i]);
+        if (s != PIFA_OK) return s;
+        if (dims[i].d_in != dims[0].d_in) return PIFA_ERR_INVALID_ARG;
+        const int64_t n_np = dims[i].d_out - dims[i].r;
+        if (!W_p[i] || (n_np > 0 && (!C || !C[i] || !nonpivot_idx || !nonpivot_idx[i])))
+            return PIFA_ERR_INVALID_ARG;
+        s = pifa_validate_partition(pivot_idx[i], n_np > 0 ? nonpivot_idx[i] : nullptr, dims[i]);
+        if (s != PIFA_OK) return s;
+    }
+    pifa_group* g = new (std::nothrow) pifa_group();
+    if (!g) return PIFA_ERR_OOM;
+    auto fail = [&](pifa_status st) {
+        free_group(g);
+        return st;
+    };
+    if (hipGetDevice(&g->device) != hipSuccess) return fail(PIFA_ERR_HIP);
+    g->n = n;
+    g->d_in = dims[0].d_in;
+    std::vector<int32_t> piv_host;
+    for (int i = 0; i < n; ++i) {
+        pifa_layer* h = nullptr;
+        pifa_status s = create_layer(W_p[i], C ? C[i] : nullptr, pivot_idx[i],
+                                     nonpivot_idx ? nonpivot_idx[i] : nullptr, dims[i], dtype, g->d_out, &h);
+        if (s != PIFA_OK) return fail(s);
+        g->layers.push_back(h);
+        g->r_off.push_back(g->r_pad);
+        for (int64_t j = 0; j < h->r_pad; ++j)
+            piv_host.push_back(j < h->r ? (int32_t)(g->d_out + pivot_idx[i][j]) : -1);
+        g->d_out += h->d_out;
+        g->r_pad += h->r_pad;
+    }
+    if (g->d_out > INT32_MAX) return fail(PIFA_ERR_UNSUPPORTED);
+    // concatenate the members' lane-order W_p blocks (16-row groups follow one another)
+    const size_t wp_bytes = (size_t)packed_elems(g->r_pad, g->d_in) * 2;
+    if (hipMalloc(&g->Wp, wp_bytes) != hipSuccess) return fail(PIFA_ERR_OOM);
+    size_t off = 0;
+    for (pifa_layer* h : g->layers) {
+        const size_t b = (size_t)packed_elems(h->r_pad, h->d_in) * 2;
+        if (hipMemcpy((char*)g->Wp + off, h->Wp, b, hipMemcpyDeviceToDevice) != hipSuccess)
+            return fail(PIFA_ERR_HIP);
+        off += b;
+        (void)hipFree(h->Wp);
+        h->Wp = nullptr;
+    }
+    if (hipMalloc(&g->piv, piv_host.size() * sizeof(int32_t)) != hipSuccess) return fail(PIFA_ERR_OOM);
+    if (hipMemcpy(g->piv, piv_host.data(), piv_host.size() * sizeof(int32_t), hipMemcpyHostToDevice) != hipSuccess)
+        return fail(PIFA_ERR_HIP);
+    if (hipMalloc(&g->overflow, sizeof(int)) != hipSuccess) return fail(PIFA_ERR_OOM);
+    if (hipMemset(g->overflow, 0, sizeof(int)) != hipSuccess) return fail(PIFA_ERR_HIP);
+    if (hipDeviceSynchronize() != hipSuccess) return fail(PIFA_ERR_HIP);
+    *out = g;
+    return PIFA_OK;
+}
+
+pifa_status pifa_group_destroy(pifa_group_handle g) {
+    if (!g) return PIFA_OK;
+    (void)hipDeviceSynchronize();
+    free_group(g);
+    return PIFA_OK;
+}
+
+pifa_status pifa_group_reserve(pifa_group_handle g, int64_t max_M) {
+    if (!g || max_M < 0) return PIFA_ERR_INVALID_ARG;
+    pifa_status s = g->ws.ensure(std::max(group_ws_bytes(g, max_M),
+                                          group_ws_bytes(g, std::min<int64_t>(max_M, kDecodeMaxM))), 0);
+    if (s != PIFA_OK) return s;
+    size_t part = 0;
+    for (int64_t m = kDecodeMaxM + 1; m <= max_M; m = m < 4096 ? m + 1 : m * 2)
+        part = std::max(part, group_part_bytes(g, std::min(m, max_M)));
+    s = g->part.ensure(part, 0);
+    if (s != PIFA_OK) return s;
+    return hipDeviceSynchronize() == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
+}
+
+size_t pifa_group_weight_bytes(pifa_group_handle g) {
+    if (!g) return 0;
+    size_t b = 0;
+    for (pifa_layer* h : g->layers) b += pifa_layer_weight_bytes(h);
+    return b;
+}
+
+pifa_status pifa_group_set_intermediate_scale(pifa_group_handle g, int log2_scale) {
+    if (!g || log2_scale < -30 || log2_scale > 30) return PIFA_ERR_INVALID_ARG;
+    g->y_log2 = log2_scale;
+    return PIFA_OK;
+}
+
+pifa_status pifa_group_overflow_count(pifa_group_handle g, int64_t* count) {
+    if (!g || !count) return PIFA_ERR_INVALID_ARG;
+    int v = 0;
+    PIFA_HIP(hipDeviceSynchronize());
+    PIFA_HIP(hipMemcpy(&v, g->overflow, sizeof(int), hipMemcpyDeviceToHost));
+    *count = v;
+    return PIFA_OK;
+}
+
+pifa_status pifa_group_forward(pifa_group_handle g, const void* X, void* Y, int64_t M, void* stream) {
+    if (!g || M < 0) return PIFA_ERR_INVALID_ARG;
+    if (M == 0) return PIFA_OK;
+    if (!X || !Y) return PIFA_ERR_INVALID_ARG;
+    if (!aligned16(X)) return PIFA_ERR_UNSUPPORTED;
+    hipStream_t st = as_stream(stream);
+    pifa_status s = g->ws.ensure(group_ws_bytes(g, M), st);
+    if (s != PIFA_OK) return s;
+    const float y_scale = std::ldexp(1.0f, g->y_log2);
+    bf16* y = (bf16*)Y;
+    f16* yp = (f16*)g->ws.ptr;
+    using EpiNP = ScatterEpi<bf16, kWsNone>;
+    hipError_t e;
+    if (M <= kDecodeMaxM) {
+        // pivot outputs of every member from one weight stream; Y_p as fp16 hi + lo planes
+        e = launch_skinny_packed<bf16>(kSiteGroupGemv1, ALoad16<bf16>{(const bf16*)X, g->d_in, M},
+                                       (const bf16*)g->Wp, g->r_pad, g->d_in,
+                                       make_epi<bf16, kWsF16Pair>(y, g->d_out, g->piv, g->r_pad, 1.f, yp, g->r_pad,
+                                                                  g->r_pad, y_scale, g->overflow, M),
+                                       st);
+        if (e != hipSuccess) return PIFA_ERR_HIP;
+        SkinnyGroup<f16, ALoadPair16, EpiNP> grp{};
+        int64_t rows[kMaxSkinnyGroup] = {};
+        for (int i = 0; i < g->n; ++i) {
+            const pifa_layer* h = g->layers[(size_t)i];
+            const float out_scale = std::ldexp(1.0f, -(g->y_log2 + h->c_log2));
+            grp.p[grp.n] = {ALoadPair16{yp + g->r_off[(size_t)i], g->r_pad, M}, (const f16*)h->C, h->r_pad,
+                            make_epi<bf16, kWsNone>(y, g->d_out, h->npiv, h->n_np, out_scale, nullptr, 0, 0, 1.f,
+                                                    nullptr, M)};
+            rows[grp.n++] = h->n_np;
+        }
+        e = launch_skinny_grouped(kSiteGroupGemv2, grp, rows, st);
+        return e == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
+    }
+    s = g->part.ensure(group_part_bytes(g, M), st);
+    if (s != PIFA_OK) return s;
+    e = launch_gemm<bf16, true>(kSiteGroupGemm1, (const bf16*)X, g->d_in, M, (const bf16*)g->Wp, 0, g->r_pad,
+                                g->d_in,
+                                make_epi<bf16, kWsF16>(y, g->d_out, g->piv, g->r_pad, 1.f, yp, g->r_pad, g->r_pad,
+                                                       y_scale, g->overflow, M),
+                                (float*)g->part.ptr, st);
+    if (e != hipSuccess) return PIFA_ERR_HIP;
+    GemmGroup<f16, EpiNP> grp{};
+    grp.M = M;
+    for (int i = 0; i < g->n; ++i) {
+        const pifa_layer* h = g->layers[(size_t)i];
+        if (h->n_np == 0) continue;
+        const float out_scale = std::ldexp(1.0f, -(g->y_log2 + h->c_log2));
+        grp.p[grp.n++] = {yp + g->r_off[(size_t)i], g->r_pad, (const f16*)h->C, h->n_np, h->r_pad,
+                          make_epi<bf16, kWsNone>(y, g->d_out, h->npiv, h->n_np, out_scale, nullptr, 0, 0, 1.f,
+                                                  nullptr, M)};
+    }
+    if (grp.n == 0) return PIFA_OK;
+    e = launch_gemm_grouped(kSiteGroupGemm2, grp, st);
+    return e == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
 }
 
 pifa_status pifa_build_f64(const double* W, pifa_dims dims, double* W_p, double* C, int32_t* pivot_idx,

@@ -68,6 +68,15 @@ _SIGNATURES = {
     "lowrank_layer_forward": (_st, [_vp, _vp, _vp, _i64, _vp]),
     "lowrank_layer_reserve": (_st, [_vp, _i64]),
     "lowrank_layer_destroy": (_st, [_vp]),
+    "pifa_group_create": (_st, [ctypes.c_int, ctypes.POINTER(_vp), ctypes.POINTER(_vp), ctypes.POINTER(_i32p),
+                                ctypes.POINTER(_i32p), ctypes.POINTER(pifa_dims), ctypes.c_int,
+                                ctypes.POINTER(_vp)]),
+    "pifa_group_destroy": (_st, [_vp]),
+    "pifa_group_reserve": (_st, [_vp, _i64]),
+    "pifa_group_forward": (_st, [_vp, _vp, _vp, _i64, _vp]),
+    "pifa_group_weight_bytes": (ctypes.c_size_t, [_vp]),
+    "pifa_group_set_intermediate_scale": (_st, [_vp, ctypes.c_int]),
+    "pifa_group_overflow_count": (_st, [_vp, ctypes.POINTER(_i64)]),
     "pifa_build_f64": (_st, [_vp, pifa_dims, _vp, _vp, _i32p, _i32p, ctypes.POINTER(ctypes.c_double), _vp]),
     "pifa_profile_enable": (_st, [ctypes.c_int]),
     "pifa_profile_reset": (_st, []),
@@ -257,6 +266,60 @@ def lowrank_layer_reserve(handle: int, max_M: int) -> None:
 
 def lowrank_layer_destroy(handle: int) -> None:
     _check("lowrank_layer_destroy", lib().lowrank_layer_destroy(handle))
+
+
+def pifa_group_create(layers, dtype: int | None = None) -> int:
+    """layers: sequence of (W_p, C, pivot_idx, nonpivot_idx, (d_in, d_out, r)) with one d_in;
+    returns an opaque group handle."""
+    n = len(layers)
+    wp = (_vp * max(n, 1))()
+    cc = (_vp * max(n, 1))()
+    pp = (_i32p * max(n, 1))()
+    npp = (_i32p * max(n, 1))()
+    dims = (pifa_dims * max(n, 1))()
+    keep = []
+    for i, (W_p, C, piv, npiv, d) in enumerate(layers):
+        wp[i] = _dev_ptr(W_p, "W_p")
+        cc[i] = _dev_ptr(C, "C")
+        a, ap = _host_i32(piv)
+        b, bp = _host_i32(npiv)
+        keep += [a, b]
+        pp[i] = ap
+        npp[i] = bp
+        dims[i] = pifa_dims(*d)
+    dt = (_dtype_code(layers[0][0]) if n else PIFA_BF16) if dtype is None else int(dtype)
+    out = _vp()
+    _check("pifa_group_create", lib().pifa_group_create(n, wp, cc, pp, npp, dims, dt, ctypes.byref(out)))
+    return out.value
+
+
+def pifa_group_destroy(handle: int) -> None:
+    _check("pifa_group_destroy", lib().pifa_group_destroy(handle))
+
+
+def pifa_group_reserve(handle: int, max_M: int) -> None:
+    _check("pifa_group_reserve", lib().pifa_group_reserve(handle, int(max_M)))
+
+
+def pifa_group_forward(handle: int, X, Y, M: int | None = None, stream=None) -> None:
+    M = X.shape[0] if M is None else int(M)
+    _check("pifa_group_forward", lib().pifa_group_forward(handle, _dev_ptr(X, "X"), _dev_ptr(Y, "Y"), M,
+                                                          _stream(stream)))
+
+
+def pifa_group_weight_bytes(handle: int) -> int:
+    return int(lib().pifa_group_weight_bytes(handle))
+
+
+def pifa_group_set_intermediate_scale(handle: int, log2_scale: int) -> None:
+    _check("pifa_group_set_intermediate_scale",
+           lib().pifa_group_set_intermediate_scale(handle, int(log2_scale)))
+
+
+def pifa_group_overflow_count(handle: int) -> int:
+    out = _i64()
+    _check("pifa_group_overflow_count", lib().pifa_group_overflow_count(handle, ctypes.byref(out)))
+    return int(out.value)
 
 
 def pifa_build_f64(W, r: int, stream=None):

@@ -1,0 +1,193 @@
+"""Grouped PIFA layers sharing one X (pifa_group_*), through the C ABI.
+
+A group writes [Y_1 | Y_2 | ...]; each block must equal the member's own
+pifa_forward (bit for bit on the decode path; up to the fp32 order of K-split
+partial sums in prefill), the pivot / non-pivot layout must be exact (probe
+weights), and
+Gaussian layers must meet the bf16 bar against the oracle's grouped forward.
+Members have different ranks, including ranks that are not a multiple of 64
+(padding rows inside the concatenated W_p).
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2501_19090_amd import inputs
+
+from gpu_util import (DeviceLayer, activations, config_layer, from_dev, gaussian_layer, rel_fro, sample_rows,
+                      to_dev, torch_mod)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _cuda():
+    if not torch_mod().cuda.is_available():
+        pytest.skip("no GPU")
+
+
+class DeviceGroup:
+    def __init__(self, members):
+        from paper_2501_19090_amd import pifa
+        self.members = members
+        self.d_out = sum(m.d_out for m in members)
+        self.offsets = np.cumsum([0] + [m.d_out for m in members])
+        self.handle = pifa.pifa_group_create(
+            [(m.wp_dev, m.c_dev, m.piv, m.npiv, (m.d_in, m.d_out, m.r)) for m in members])
+
+    def forward(self, x_dev, M=None):
+        from paper_2501_19090_amd import pifa
+        torch = torch_mod()
+        M = x_dev.shape[0] if M is None else M
+        y = torch.full((max(M, 1), self.d_out), float("nan"), dtype=x_dev.dtype, device=x_dev.device)
+        pifa.pifa_group_forward(self.handle, x_dev, y, M)
+        torch.cuda.synchronize()
+        return y
+
+    def oracle(self, x64):
+        return oracle.group_forward(x64, [(m.piv, m.npiv, m.Wp, m.C) for m in self.members])
+
+    def close(self):
+        from paper_2501_19090_amd import pifa
+        if self.handle:
+            pifa.pifa_group_destroy(self.handle)
+            self.handle = 0
+        for m in self.members:
+            m.close()
+
+
+def _gauss_members(specs, d_in):
+    out = []
+    for d_out, r, seed in specs:
+        piv, npiv, Wp, C, *_ = gaussian_layer(d_in, d_out, r, seed)
+        out.append(DeviceLayer(piv, npiv, Wp, C, "bf16"))
+    return out
+
+
+MS = (1, 5, 16, 17, 64, 300, 1000)
+
+
+def test_group_equals_member_forwards_bitexact():
+    d_in = 1024
+    grp = DeviceGroup(_gauss_members([(2752, 512, 11), (2752, 512, 12), (700, 300, 13), (96, 96, 14)], d_in))
+    try:
+        for M in MS:
+            x_dev, _ = activations(M, d_in, 100 + M, "bf16")
+            y = grp.forward(x_dev).cpu()
+            for i, m in enumerate(grp.members):
+                ref = m.forward(x_dev).cpu()
+                blk = y[:, grp.offsets[i]:grp.offsets[i + 1]]
+                if M <= 16:
+                    assert torch_mod().equal(blk.view(torch_mod().int16), ref.view(torch_mod().int16)), (M, i)
+                else:
+                    b, r = blk.float().numpy().astype(np.float64), ref.float().numpy().astype(np.float64)
+                    assert rel_fro(b, r) <= 1e-3, (M, i)
+    finally:
+        grp.close()
+
+
+def test_group_layout_probe_bitexact():
+    """Probe weights at the LLaMA MLP gate/up shape (4096 -> 11008, r = 2048,
+    the oracle's I and a random partition) plus a small member of rank 100."""
+    d_in = 4096
+    piv_c, npiv_c, *_ = config_layer("C_mlp_up_4096x11008")
+    parts = [(piv_c, npiv_c, 11008, 2048)]
+    p2, n2 = inputs.random_partition(11008, 2048, 77)
+    parts.append((p2, n2, 11008, 2048))
+    p3, n3 = inputs.random_partition(1000, 100, 78)
+    parts.append((p3, n3, 1000, 100))
+    members = []
+    for piv, npiv, d_out, r in parts:
+        Wp, C = inputs.layout_probe_layer(d_in, d_out, r)
+        members.append(DeviceLayer(piv, npiv, Wp, C, "bf16"))
+    grp = DeviceGroup(members)
+    try:
+        for M in (1, 16, 17, 300):
+            st, x64 = inputs.round_to(inputs.layout_probe_activations(M, d_in, M), "bf16")
+            y = from_dev(grp.forward(to_dev(st)))
+            for i, m in enumerate(members):
+                blk = y[:, grp.offsets[i]:grp.offsets[i + 1]]
+                k = np.arange(m.d_out - m.r)
+                assert np.array_equal(blk[:, m.piv], x64[:, : m.r])
+                assert np.array_equal(blk[:, m.npiv], x64[:, (7 * k + 3) % m.r])
+            rows = sample_rows(M)
+            assert np.array_equal(y[rows], grp.oracle(x64[rows]))
+    finally:
+        grp.close()
+
+
+def test_group_parity_vs_oracle_mlp_shape():
+    """Gate/up-shaped members (4096 -> 11008, r = 2048) and a rank-410 member,
+    at decode and prefill sizes, against the oracle's grouped forward."""
+    d_in = 4096
+    piv, npiv, Wp, C, *_ = config_layer("C_mlp_up_4096x11008")
+    m1 = DeviceLayer(piv, npiv, Wp, C, "bf16")
+    piv2, npiv2, Wp2, C2, *_ = config_layer("E_sweep_r10")
+    m2 = DeviceLayer(piv2, npiv2, Wp2, C2, "bf16")
+    grp = DeviceGroup([m1, m2])
+    try:
+        for M in (1, 16, 4096):
+            x_dev, x64 = activations(M, d_in, 7 + M, "bf16")
+            y = from_dev(grp.forward(x_dev))
+            rows = sample_rows(M)
+            err = rel_fro(y[rows], grp.oracle(x64[rows]))
+            assert err <= 5e-3, (M, err)
+    finally:
+        grp.close()
+
+
+def test_group_overflow_counted_and_scale_applies():
+    from paper_2501_19090_amd import pifa
+    d_in = 256
+    grp = DeviceGroup(_gauss_members([(320, 96, 21), (200, 64, 22)], d_in))
+    try:
+        x_dev, x64 = activations(40, d_in, 3, "bf16")
+        ref = grp.oracle(x64)
+        pifa.pifa_group_set_intermediate_scale(grp.handle, -4)
+        assert rel_fro(from_dev(grp.forward(x_dev)), ref) <= 5e-3
+        assert pifa.pifa_group_overflow_count(grp.handle) == 0
+        pifa.pifa_group_set_intermediate_scale(grp.handle, 30)
+        for M in (3, 40):  # decode and prefill paths
+            before = pifa.pifa_group_overflow_count(grp.handle)
+            grp.forward(x_dev[:M].contiguous())
+            assert pifa.pifa_group_overflow_count(grp.handle) > before, M
+    finally:
+        grp.close()
+
+
+def test_group_weight_bytes_and_empty_batch():
+    from paper_2501_19090_amd import pifa
+    d_in = 128
+    members = _gauss_members([(160, 64, 31), (96, 96, 32)], d_in)
+    grp = DeviceGroup(members)
+    try:
+        assert pifa.pifa_group_weight_bytes(grp.handle) == sum(
+            pifa.pifa_layer_weight_bytes(m.handle) for m in members)
+        x_dev, _ = activations(4, d_in, 1, "bf16")
+        pifa.pifa_group_forward(grp.handle, x_dev, x_dev, 0)  # M = 0: no launch, no write
+        pifa.pifa_group_reserve(grp.handle, 5000)
+        y = grp.forward(x_dev)
+        assert torch_mod().isfinite(y.float()).all()
+    finally:
+        grp.close()
+
+
+def test_group_rejects_bad_arguments():
+    from paper_2501_19090_amd import pifa
+    torch = torch_mod()
+    wp = torch.zeros((64, 128), dtype=torch.bfloat16, device="cuda:0")
+    c = torch.zeros((32, 64), dtype=torch.bfloat16, device="cuda:0")
+    piv, npiv = np.arange(64), np.arange(64, 96)
+    good = (wp, c, piv, npiv, (128, 96, 64))
+    with pytest.raises(pifa.PifaError) as e:
+        pifa.pifa_group_create([good, (wp, c, piv, npiv, (64, 96, 64))])  # different d_in
+    assert e.value.status == pifa.PIFA_ERR_INVALID_ARG
+    with pytest.raises(pifa.PifaError) as e:
+        pifa.pifa_group_create([good] * 9)
+    assert e.value.status == pifa.PIFA_ERR_INVALID_ARG
+    with pytest.raises(pifa.PifaError) as e:
+        pifa.pifa_group_create([(wp, c, piv, np.arange(63, 95), (128, 96, 64))])
+    assert e.value.status == pifa.PIFA_ERR_BAD_INDEX
+    with pytest.raises(pifa.PifaError) as e:
+        pifa.pifa_group_create([good], dtype=pifa.PIFA_F32)
+    assert e.value.status == pifa.PIFA_ERR_UNSUPPORTED

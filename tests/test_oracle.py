@@ -249,6 +249,23 @@ def test_config_a_matches_dense():
     assert _rel(Y, oracle.lowrank_forward(X, U, V)) <= 1e-12
 
 
+def test_group_forward_is_stacked_dense_product():
+    """Grouped layers on one X: the block [Y_1 | Y_2 | Y_3] equals a triple-loop
+    X [W_1; W_2; W_3]^T of the stacked weights, with a different rank each."""
+    d_in = 9
+    shapes = [(7, 3), (5, 5), (11, 2)]
+    Ws, layers = [], []
+    for i, (d_out, r) in enumerate(shapes):
+        U, V, W = _layer(d_out, d_in, r, seed=40 + i)
+        b = oracle.build_pifa(W, r)
+        Ws.append(W)
+        layers.append((b["pivot_idx"], b["nonpivot_idx"], b["Wp"], b["C"]))
+    X = inputs.activations(4, d_in, seed=3)
+    Y = oracle.group_forward(X, layers)
+    assert Y.shape == (4, 23)
+    assert _rel(Y, _triple_loop_dense(X, np.vstack(Ws))) <= 1e-12
+
+
 def test_forward_is_pivot_set_invariant():
     """Two different valid pivot sets of the same W' give the same Y."""
     U, V, W = _layer(120, 90, 40, 4)
