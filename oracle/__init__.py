@@ -62,6 +62,9 @@ def _load():
         lib.oracle_lowrank_forward.restype = None
         lib.oracle_lowrank_forward.argtypes = [f64p, f64p, f64p, i64, i64, i64, i64, f64p,
                                                ctypes.c_int]
+        lib.oracle_pifa_backward.restype = None
+        lib.oracle_pifa_backward.argtypes = [f64p, f64p, i64, i64, i64, i64, i32p, i32p, f64p, f64p, f64p,
+                                             f64p, f64p, ctypes.c_int]
         lib.oracle_reconstruction_error.restype = ctypes.c_double
         lib.oracle_reconstruction_error.argtypes = [f64p, i64, i64, i64, i32p, i32p, f64p, f64p,
                                                     ctypes.c_int]
@@ -154,6 +157,29 @@ def group_forward(X, layers, threads: int | None = None) -> np.ndarray:
     layers: sequence of (pivot_idx, nonpivot_idx, Wp, C)."""
     outs = [pifa_forward(X, piv, npiv, Wp, C, threads=threads) for piv, npiv, Wp, C in layers]
     return np.concatenate(outs, axis=1) if outs else np.zeros((np.shape(X)[0], 0))
+
+
+def pifa_backward(X, G, pivot_idx, nonpivot_idx, Wp, C, threads: int | None = None):
+    """Gradients of Algorithm "PIFA Layer" for G = dL/dY: returns (dX, dWp, dC)."""
+    lib = _load()
+    X, G, Wp = _f64(X), _f64(G), _f64(Wp)
+    piv, npiv = _i32(pivot_idx), _i32(nonpivot_idx)
+    M, d_in = X.shape
+    r = Wp.shape[0]
+    d_out = G.shape[1]
+    C = _f64(C).reshape(d_out - r, r)
+    dX = np.zeros((M, d_in), np.float64)
+    dWp = np.zeros((r, d_in), np.float64)
+    dC = np.zeros((d_out - r, r), np.float64)
+    nt = threads if threads is not None else default_threads()
+    Cbuf = C if C.size else np.zeros(1, np.float64)
+    dCbuf = dC if dC.size else np.zeros(1, np.float64)
+    npbuf = npiv if npiv.size else np.zeros(1, np.int32)
+    lib.oracle_pifa_backward(_p(X, ctypes.c_double), _p(G, ctypes.c_double), M, d_in, d_out, r,
+                             _p(piv, ctypes.c_int32), _p(npbuf, ctypes.c_int32), _p(Wp, ctypes.c_double),
+                             _p(Cbuf, ctypes.c_double), _p(dX, ctypes.c_double), _p(dWp, ctypes.c_double),
+                             _p(dCbuf, ctypes.c_double), int(nt))
+    return dX, dWp, dC
 
 
 def dense_forward(X, W, threads: int | None = None) -> np.ndarray:

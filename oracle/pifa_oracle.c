@@ -23,6 +23,10 @@
  *                             paper's U (V^T X) in row-major form (Sec. 3.3).
  *   oracle_reconstruction_error -- the losslessness check
  *                             || P[W_p; C W_p] - W ||_F / ||W||_F.
+ *   oracle_pifa_backward   -- gradients of Algorithm "PIFA Layer" (the layer
+ *                             is differentiable end to end, Sec. 5 and 6):
+ *                             the chain rule through its two products and
+ *                             two column assignments.
  *
  * Readings of points the paper leaves open (each is listed in the design
  * notes of the repository):
@@ -383,4 +387,78 @@ int oracle_max_threads(void) {
 #else
     return 1;
 #endif
+}
+
+/*
+ * Gradients of Algorithm "PIFA Layer" for G = dL/dY (M x d_out).  Forward:
+ * Y_p = X W_p^T, Y_np = Y_p C^T, Y[:, I] = Y_p, Y[:, I^c] = Y_np.  Backward,
+ * step by step:
+ *   G_p   = G[:, I] + G[:, I^c] C        (Y_p feeds both assignments)
+ *   dC    = G[:, I^c]^T Y_p              (n_np x r)
+ *   dX    = G_p W_p                      (M x d_in)
+ *   dW_p  = G_p^T X                      (r x d_in)
+ * Y_p is recomputed from X and W_p.  dX, dWp, dC are overwritten; dC may be
+ * NULL when r = d_out.
+ */
+void oracle_pifa_backward(const double* X, const double* G, int64_t M, int64_t d_in,
+                          int64_t d_out, int64_t r, const int32_t* pivot_idx,
+                          const int32_t* nonpivot_idx, const double* Wp, const double* C,
+                          double* dX, double* dWp, double* dC, int nthreads) {
+    const int nt = clamp_threads(nthreads);
+    const int64_t n_np = d_out - r;
+    const size_t mr = (size_t)(M > 0 ? M : 1) * (size_t)r;
+    double* Yp = (double*)malloc(mr * sizeof(double));
+    double* Gp = (double*)malloc(mr * sizeof(double));
+    if (!Yp || !Gp) {
+        free(Yp);
+        free(Gp);
+        return;
+    }
+
+#pragma omp parallel for collapse(2) schedule(static) num_threads(nt)
+    for (int64_t m = 0; m < M; ++m)
+        for (int64_t j = 0; j < r; ++j) {
+            double s = 0.0;
+            for (int64_t k = 0; k < d_in; ++k) s += X[m * d_in + k] * Wp[j * d_in + k];
+            Yp[m * r + j] = s;
+        }
+
+    /* G_p = G[:, I] + G[:, I^c] C */
+#pragma omp parallel for collapse(2) schedule(static) num_threads(nt)
+    for (int64_t m = 0; m < M; ++m)
+        for (int64_t j = 0; j < r; ++j) {
+            double s = G[m * d_out + pivot_idx[j]];
+            for (int64_t k = 0; k < n_np; ++k) s += G[m * d_out + nonpivot_idx[k]] * C[k * r + j];
+            Gp[m * r + j] = s;
+        }
+
+    /* dC = G[:, I^c]^T Y_p */
+#pragma omp parallel for collapse(2) schedule(static) num_threads(nt)
+    for (int64_t k = 0; k < n_np; ++k)
+        for (int64_t j = 0; j < r; ++j) {
+            double s = 0.0;
+            for (int64_t m = 0; m < M; ++m) s += G[m * d_out + nonpivot_idx[k]] * Yp[m * r + j];
+            dC[k * r + j] = s;
+        }
+
+    /* dX = G_p W_p */
+#pragma omp parallel for collapse(2) schedule(static) num_threads(nt)
+    for (int64_t m = 0; m < M; ++m)
+        for (int64_t i = 0; i < d_in; ++i) {
+            double s = 0.0;
+            for (int64_t j = 0; j < r; ++j) s += Gp[m * r + j] * Wp[j * d_in + i];
+            dX[m * d_in + i] = s;
+        }
+
+    /* dW_p = G_p^T X */
+#pragma omp parallel for collapse(2) schedule(static) num_threads(nt)
+    for (int64_t j = 0; j < r; ++j)
+        for (int64_t i = 0; i < d_in; ++i) {
+            double s = 0.0;
+            for (int64_t m = 0; m < M; ++m) s += Gp[m * r + j] * X[m * d_in + i];
+            dWp[j * d_in + i] = s;
+        }
+
+    free(Yp);
+    free(Gp);
 }

@@ -339,3 +339,88 @@ def test_bf16_rounding_matches_torch():
     ours = inputs.f32_bits_to_bf16_bits(x)
     ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
     assert np.array_equal(ours, ref)
+
+
+# ---------------------------------------------------------------- backward
+def _backward_case(d_out=14, d_in=11, r=5, M=6, seed=3):
+    U, V, W = _layer(d_out, d_in, r, seed)
+    b = oracle.build_pifa(W, r)
+    X = inputs.activations(M, d_in, seed + 1)
+    G = np.random.default_rng(seed + 2).standard_normal((M, d_out))
+    return W, b, X, G
+
+
+def _loss(X, G, b, Wp=None, C=None):
+    """<G, Y> with Y the oracle forward (linear in each of X, W_p, C)."""
+    Y = oracle.pifa_forward(X, b["pivot_idx"], b["nonpivot_idx"], b["Wp"] if Wp is None else Wp,
+                            b["C"] if C is None else C)
+    return float(np.sum(G * Y))
+
+
+def test_backward_dx_is_dense_gradient():
+    """PIFA reproduces Y = X W^T exactly, so dL/dX = G W (the dense gradient)."""
+    for shape in [(14, 11, 5), (9, 16, 9), (30, 20, 7)]:
+        W, b, X, G = _backward_case(*shape)
+        dX, dWp, dC = oracle.pifa_backward(X, G, b["pivot_idx"], b["nonpivot_idx"], b["Wp"], b["C"])
+        assert _rel(dX, G @ W) <= 1e-12, shape
+
+
+def test_backward_weight_grads_match_finite_differences():
+    """L = <G, Y> is linear in W_p and in C, so L(W_p + E) - L(W_p) = <dW_p, E>
+    holds exactly up to rounding for any direction E (same for C)."""
+    rng = np.random.default_rng(9)
+    for shape in [(14, 11, 5), (9, 16, 9), (30, 20, 7)]:
+        W, b, X, G = _backward_case(*shape)
+        dX, dWp, dC = oracle.pifa_backward(X, G, b["pivot_idx"], b["nonpivot_idx"], b["Wp"], b["C"])
+        L0 = _loss(X, G, b)
+        for _ in range(3):
+            E = rng.standard_normal(b["Wp"].shape)
+            fd = _loss(X, G, b, Wp=b["Wp"] + E) - L0
+            assert abs(fd - np.sum(dWp * E)) <= 1e-10 * (1 + abs(fd)), shape
+            if b["C"].size:
+                F = rng.standard_normal(b["C"].shape)
+                fd = _loss(X, G, b, C=b["C"] + F) - L0
+                assert abs(fd - np.sum(dC * F)) <= 1e-10 * (1 + abs(fd)), shape
+            D = rng.standard_normal(X.shape)
+            fd = _loss(X + D, G, b) - L0
+            assert abs(fd - np.sum(dX * D)) <= 1e-10 * (1 + abs(fd)), shape
+
+
+def test_backward_full_rank_has_no_c():
+    W, b, X, G = _backward_case(6, 9, 6)
+    dX, dWp, dC = oracle.pifa_backward(X, G, b["pivot_idx"], b["nonpivot_idx"], b["Wp"], b["C"])
+    assert dC.shape == (0, 6)
+    assert _rel(dX, G @ W) <= 1e-12
+    # with r = d_out, W_p is W with its rows permuted, and dW_p = G[:, I]^T X
+    assert _rel(dWp, G[:, b["pivot_idx"]].T @ X) <= 1e-12
+
+
+def test_backward_pins_catch_planted_mistakes():
+    """Plausible slips in the gradient formulas fail the finite-difference pins."""
+    W, b, X, G = _backward_case(14, 11, 5)
+    piv, npiv, Wp, C = b["pivot_idx"], b["nonpivot_idx"], b["Wp"], b["C"]
+    rng = np.random.default_rng(4)
+    E, F = rng.standard_normal(Wp.shape), rng.standard_normal(C.shape)
+    L0 = _loss(X, G, b)
+    fd_w = _loss(X, G, b, Wp=Wp + E) - L0
+    fd_c = _loss(X, G, b, C=C + F) - L0
+    Yp = X @ Wp.T
+    good_gp = G[:, piv] + G[:, npiv] @ C
+    wrong_dwp = {
+        "dropped pivot term": (G[:, npiv] @ C).T @ X,
+        "C not applied": G[:, piv].T @ X,
+        "sign flip": (G[:, piv] - G[:, npiv] @ C).T @ X,
+    }
+    for name, dwp in wrong_dwp.items():
+        assert abs(fd_w - np.sum(dwp * E)) > 1e-6 * (1 + abs(fd_w)), name
+    n_np = len(npiv)
+    wrong_dc = {
+        "index map dropped": G[:, :n_np].T @ Yp,
+        "non-pivot order reversed": G[:, npiv[::-1]].T @ Yp,
+    }
+    for name, dc in wrong_dc.items():
+        assert abs(fd_c - np.sum(dc * F)) > 1e-6 * (1 + abs(fd_c)), name
+    # and the oracle's own output passes
+    dX, dWp, dC = oracle.pifa_backward(X, G, piv, npiv, Wp, C)
+    assert abs(fd_w - np.sum(dWp * E)) <= 1e-10 * (1 + abs(fd_w))
+    assert np.allclose(dWp, good_gp.T @ X, rtol=0, atol=1e-12)
