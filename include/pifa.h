@@ -135,6 +135,32 @@ pifa_status pifa_layer_set_intermediate_scale(pifa_handle h, int log2_scale);
 pifa_status pifa_layer_overflow_count(pifa_handle h, int64_t* count);
 
 /*
+ * Gradients of Algorithm "PIFA Layer" (the layer is differentiable end to
+ * end, Sec. 5 and 6; the chain rule through its two products and two column
+ * assignments).  With G = dL/dY:
+ *   G_p  = G[:, I] + G[:, I^c] C,   dX = G_p W_p,
+ *   dW_p = G_p^T X,                 dC = G[:, I^c]^T Y_p.
+ *   X   device, M x d_in, bf16: the forward's input.
+ *   Y   device, M x d_out, bf16: the forward's output for X; its pivot
+ *       columns Y[:, I] supply Y_p for dC.
+ *   dY  device, M x d_out, bf16: G.
+ *   dX  device, M x d_in, bf16 (overwritten), or NULL to skip.
+ *   dW_p device, r x d_in, fp32 (overwritten), rows in the layer's W_p order,
+ *       or NULL to skip.
+ *   dC  device, (d_out - r) x r, fp32 (overwritten), rows in the layer's C
+ *       order, or NULL to skip (ignored when r = d_out).
+ * No alignment is required of X, Y, dY.  M = 0 zeroes dW_p and dC.  bf16
+ * layers only (PIFA_F32 returns PIFA_ERR_UNSUPPORTED).  The first call builds
+ * transposed copies of W_p and C in the layer (synchronous); the handle's
+ * backward workspace grows on demand (synchronising `stream`).  Calls on one
+ * handle must not overlap.  G_p reaches dX as a bf16 pair (about 16
+ * significant bits), since C makes that product cancel; the other products
+ * take bf16 operands; all accumulate in fp32.
+ */
+pifa_status pifa_layer_backward(pifa_handle h, const void* X, const void* Y, const void* dY, int64_t M,
+                                void* dX, float* dW_p, float* dC, void* stream);
+
+/*
  * Grouped PIFA layers that read the same activations X (for example a
  * transformer MLP's gate and up projections, or attention's q, k and v), with
  * a rank of their own each (MPIFA_NS sets a density per module: appendix

@@ -22,6 +22,7 @@
 #include "epilogue.hpp"
 #include "gemm_f32.hpp"
 #include "gemm_mfma.hpp"
+#include "backward.hpp"
 #include "build.hpp"
 #include "gemv_skinny.hpp"
 #include "layout.hpp"
@@ -91,6 +92,11 @@ enum Site {
     kSiteGroupGemm2,
     kSiteGroupGemv1,
     kSiteGroupGemv2,
+    kSiteBwdData,
+    kSiteBwdGp,
+    kSiteBwdDx,
+    kSiteBwdDwp,
+    kSiteBwdDc,
     kSiteCount
 };
 
@@ -99,7 +105,8 @@ const char* const kSiteNames[kSiteCount] = {
     "pifa_f32_gemm1",      "pifa_f32_gemm2",      "dense_gemm",          "dense_gemv",
     "dense_f32",           "lowrank_gemm1_xv",    "lowrank_gemm2_tu",    "lowrank_gemv1_xv",
     "lowrank_gemv2_tu",    "lowrank_f32",         "pifa_group_gemm1",    "pifa_group_gemm2",
-    "pifa_group_gemv1",    "pifa_group_gemv2"};
+    "pifa_group_gemv1",    "pifa_group_gemv2",    "pifa_bwd_gather",     "pifa_bwd_gp",
+    "pifa_bwd_dx",         "pifa_bwd_dwp",        "pifa_bwd_dc"};
 
 struct Profiler {
     std::mutex mu;
@@ -414,6 +421,10 @@ struct pifa_layer {
     int c_log2 = 0, y_log2 = 0;
     GrowBuf ws;                // Y_p hand-off
     GrowBuf part;              // K-split partial products
+    // backward, built on first use from the packed forward weights
+    void* bwd_wpt = nullptr;   // lane order of d_in x 2 r_pad: [W_p^T | W_p^T]
+    void* bwd_ct = nullptr;    // lane order of r_pad x ldc: C^T in bf16 (ldc = n_np rounded up to 8)
+    GrowBuf bws;               // backward operands and partial products
 };
 
 struct lowrank_layer {
@@ -460,8 +471,11 @@ void free_layer(pifa_layer* h) {
     if (h->piv) (void)hipFree(h->piv);
     if (h->npiv) (void)hipFree(h->npiv);
     if (h->overflow) (void)hipFree(h->overflow);
+    if (h->bwd_wpt) (void)hipFree(h->bwd_wpt);
+    if (h->bwd_ct) (void)hipFree(h->bwd_ct);
     h->ws.release();
     h->part.release();
+    h->bws.release();
     delete h;
 }
 
@@ -1031,6 +1045,145 @@ pifa_status lowrank_layer_destroy(lowrank_handle h) {
     free_lowrank(h);
     return PIFA_OK;
 }
+
+}  // extern "C"
+
+// ===================================================================== backward
+namespace {
+
+inline int64_t align_elems(int64_t n) { return round_up(n, (int64_t)128); }  // 256-byte regions
+
+// Transposed weight copies for the backward products (once per layer).
+pifa_status prepare_backward(pifa_layer* h) {
+    if (h->bwd_wpt) return PIFA_OK;
+    const int64_t ldc = round_up(h->n_np, (int64_t)8);
+    void* wpt = nullptr;
+    void* ct = nullptr;
+    if (hipMalloc(&wpt, (size_t)packed_elems(h->d_in, 2 * h->r_pad) * 2) != hipSuccess) return PIFA_ERR_OOM;
+    if (h->n_np > 0 && hipMalloc(&ct, (size_t)packed_elems(h->r_pad, ldc) * 2) != hipSuccess) {
+        (void)hipFree(wpt);
+        return PIFA_ERR_OOM;
+    }
+    const int64_t c1 = packed_groups(h->d_in) * packed_kblocks(2 * h->r_pad) * kPackChunks;
+    hipLaunchKernelGGL((pack_transposed<bf16>), dim3(grid_for(c1)), dim3(256), 0, 0, (const bf16*)h->Wp,
+                       packed_kblocks(h->d_in), h->r, h->d_in, h->r_pad, 1.f, (bf16*)wpt, h->d_in, 2 * h->r_pad);
+    bool ok = hipGetLastError() == hipSuccess;
+    if (ok && ct) {
+        const int64_t c2 = packed_groups(h->r_pad) * packed_kblocks(ldc) * kPackChunks;
+        hipLaunchKernelGGL((pack_transposed<f16>), dim3(grid_for(c2)), dim3(256), 0, 0, (const f16*)h->C,
+                           packed_kblocks(h->r_pad), h->n_np, h->r, ldc, std::ldexp(1.0f, -h->c_log2), (bf16*)ct,
+                           h->r_pad, ldc);
+        ok = hipGetLastError() == hipSuccess;
+    }
+    ok = ok && hipDeviceSynchronize() == hipSuccess;
+    if (!ok) {
+        (void)hipFree(wpt);
+        if (ct) (void)hipFree(ct);
+        return PIFA_ERR_HIP;
+    }
+    h->bwd_wpt = wpt;
+    h->bwd_ct = ct;
+    return PIFA_OK;
+}
+
+hipError_t launch_gather_transpose(const bf16* in, int64_t ld_in, int64_t M, const int32_t* idx, int64_t ncols,
+                                   bf16* out, int64_t ld_out, hipStream_t st) {
+    if (ncols == 0 || ld_out == 0) return hipSuccess;
+    hipLaunchKernelGGL(gather_transpose, dim3((unsigned)ceil_div(ld_out, kTrTile), (unsigned)ceil_div(ncols, kTrTile)),
+                       dim3(256), 0, st, in, ld_in, M, idx, ncols, out, ld_out);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+extern "C" {
+
+pifa_status pifa_layer_backward(pifa_handle h, const void* X, const void* Y, const void* dY, int64_t M,
+                                void* dX, float* dW_p, float* dC, void* stream) {
+    if (!h || M < 0) return PIFA_ERR_INVALID_ARG;
+    if (h->dtype != PIFA_BF16) return PIFA_ERR_UNSUPPORTED;
+    hipStream_t st = as_stream(stream);
+    const int64_t r = h->r, n_np = h->n_np, d_in = h->d_in, d_out = h->d_out, r_pad = h->r_pad;
+    if (M == 0) {  // the gradient of an empty batch
+        if (dW_p) PIFA_HIP(hipMemsetAsync(dW_p, 0, (size_t)r * d_in * 4, st));
+        if (dC && n_np > 0) PIFA_HIP(hipMemsetAsync(dC, 0, (size_t)n_np * r * 4, st));
+        return PIFA_OK;
+    }
+    if (!dY || (dX == nullptr && dW_p == nullptr && dC == nullptr)) return dY ? PIFA_OK : PIFA_ERR_INVALID_ARG;
+    if ((dW_p && !X) || (dC && n_np > 0 && !Y)) return PIFA_ERR_INVALID_ARG;
+    pifa_status s = prepare_backward(h);
+    if (s != PIFA_OK) return s;
+
+    const int64_t M_pad = round_up(M, (int64_t)8), ldc = round_up(n_np, (int64_t)8);
+    // workspace regions (bf16 elements)
+    const int64_t e_gic = align_elems(M * ldc), e_gict = align_elems(n_np * M_pad), e_ypt = align_elems(r * M_pad),
+                  e_xt = align_elems(d_in * M_pad), e_spl = align_elems(M * 2 * r_pad),
+                  e_gpt = align_elems(r * M_pad);
+    const size_t part = std::max({split_bytes(M, r_pad, ldc), split_bytes(M, d_in, 2 * r_pad),
+                                  split_bytes(r, d_in, M_pad), split_bytes(n_np, r, M_pad)});
+    const size_t bf_bytes = (size_t)(e_gic + e_gict + e_ypt + e_xt + e_spl + e_gpt) * 2;
+    s = h->bws.ensure(bf_bytes + part, st);
+    if (s != PIFA_OK) return s;
+    bf16* base = (bf16*)h->bws.ptr;
+    bf16* gic = base;
+    bf16* gict = gic + e_gic;
+    bf16* ypt = gict + e_gict;
+    bf16* xt = ypt + e_ypt;
+    bf16* spl = xt + e_xt;
+    bf16* gpt = spl + e_spl;
+    float* partials = part ? (float*)((char*)h->bws.ptr + bf_bytes) : nullptr;
+    const bf16* G = (const bf16*)dY;
+    hipError_t e = hipSuccess;
+
+    {  // operands in K-contiguous form
+        TimedLaunch timed(kSiteBwdData, st);
+        if (n_np > 0) {
+            hipLaunchKernelGGL(gather_cols, dim3(grid_for(M * ldc)), dim3(256), 0, st, G, d_out, M, h->npiv, n_np,
+                               gic, ldc);
+            if ((e = hipGetLastError()) != hipSuccess) return PIFA_ERR_HIP;
+            if (dC && (e = launch_gather_transpose(G, d_out, M, h->npiv, n_np, gict, M_pad, st)) != hipSuccess)
+                return PIFA_ERR_HIP;
+            if (dC && (e = launch_gather_transpose((const bf16*)Y, d_out, M, h->piv, r, ypt, M_pad, st)) != hipSuccess)
+                return PIFA_ERR_HIP;
+        }
+        if (dW_p && (e = launch_gather_transpose((const bf16*)X, d_in, M, nullptr, d_in, xt, M_pad, st)) != hipSuccess)
+            return PIFA_ERR_HIP;
+    }
+    // G_p = G[:, I^c] C + G[:, I], as a bf16 pair and transposed
+    e = launch_gemm<bf16, true>(kSiteBwdGp, gic, ldc, M, (const bf16*)h->bwd_ct, 0, r_pad, ldc,
+                                GradPivotEpi{G, d_out, h->piv, r, r_pad, spl, 2 * r_pad, gpt, M_pad, M}, partials, st);
+    if (e != hipSuccess) return PIFA_ERR_HIP;
+    if (M_pad > M) {
+        hipLaunchKernelGGL(zero_cols, dim3(grid_for(r * (M_pad - M))), dim3(256), 0, st, gpt, r, M_pad, M);
+        if (hipGetLastError() != hipSuccess) return PIFA_ERR_HIP;
+    }
+    if (dX) {  // dX = [hi | lo] [W_p^T | W_p^T]^T
+        e = launch_gemm<bf16, true>(kSiteBwdDx, spl, 2 * r_pad, M, (const bf16*)h->bwd_wpt, 0, d_in, 2 * r_pad,
+                                    make_epi<bf16, kWsNone>((bf16*)dX, d_in, nullptr, d_in, 1.f, nullptr, 0, 0, 1.f,
+                                                            nullptr, M),
+                                    partials, st);
+        if (e != hipSuccess) return PIFA_ERR_HIP;
+    }
+    if (dW_p) {  // dW_p = G_p^T X
+        e = launch_gemm<bf16, false>(kSiteBwdDwp, gpt, M_pad, r, xt, M_pad, d_in, M_pad,
+                                     make_epi<float, kWsNone>(dW_p, d_in, nullptr, d_in, 1.f, nullptr, 0, 0, 1.f,
+                                                              nullptr, r),
+                                     partials, st);
+        if (e != hipSuccess) return PIFA_ERR_HIP;
+    }
+    if (dC && n_np > 0) {  // dC = G[:, I^c]^T Y_p
+        e = launch_gemm<bf16, false>(kSiteBwdDc, gict, M_pad, n_np, ypt, M_pad, r, M_pad,
+                                     make_epi<float, kWsNone>(dC, r, nullptr, r, 1.f, nullptr, 0, 0, 1.f, nullptr,
+                                                              n_np),
+                                     partials, st);
+        if (e != hipSuccess) return PIFA_ERR_HIP;
+    }
+    return PIFA_OK;
+}
+
+}  // extern "C"
+
+extern "C" {
 
 pifa_status pifa_group_create(int n, const void* const* W_p, const void* const* C,
                               const int32_t* const* pivot_idx, const int32_t* const* nonpivot_idx,

@@ -68,6 +68,7 @@ _SIGNATURES = {
     "lowrank_layer_forward": (_st, [_vp, _vp, _vp, _i64, _vp]),
     "lowrank_layer_reserve": (_st, [_vp, _i64]),
     "lowrank_layer_destroy": (_st, [_vp]),
+    "pifa_layer_backward": (_st, [_vp, _vp, _vp, _vp, _i64, _vp, _vp, _vp, _vp]),
     "pifa_group_create": (_st, [ctypes.c_int, ctypes.POINTER(_vp), ctypes.POINTER(_vp), ctypes.POINTER(_i32p),
                                 ctypes.POINTER(_i32p), ctypes.POINTER(pifa_dims), ctypes.c_int,
                                 ctypes.POINTER(_vp)]),
@@ -198,6 +199,16 @@ def pifa_layer_overflow_count(handle: int) -> int:
     out = _i64()
     _check("pifa_layer_overflow_count", lib().pifa_layer_overflow_count(handle, ctypes.byref(out)))
     return int(out.value)
+
+
+def pifa_layer_backward(handle: int, X, Y, dY, dX=None, dW_p=None, dC=None, M: int | None = None,
+                        stream=None) -> None:
+    """Gradients of the layer: dX (bf16 M x d_in), dW_p (fp32 r x d_in), dC (fp32 (d_out-r) x r);
+    each output may be None to skip it."""
+    M = dY.shape[0] if M is None else int(M)
+    _check("pifa_layer_backward", lib().pifa_layer_backward(
+        handle, _dev_ptr(X, "X"), _dev_ptr(Y, "Y"), _dev_ptr(dY, "dY"), M, _dev_ptr(dX, "dX"),
+        _dev_ptr(dW_p, "dW_p"), _dev_ptr(dC, "dC"), _stream(stream)))
 
 
 def dense_forward(W, X, Y, M: int | None = None, d_in: int | None = None, d_out: int | None = None,
