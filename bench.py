@@ -14,7 +14,7 @@ weights rotated through more than the 256 MB Infinity Cache), the same-engine
 low-rank U V and dense baselines, the dominant kernel's roofline (timed live
 with HIP events on its launch stream), the fp64 oracle timed on the host, and
 the grouped case (the MLP gate and up projections sharing X, as one group
-against two separate layers).
+against two separate layers) and the backward pass at the headline size.
 
 The layers are synthetic: Gaussian low-rank W' = U V (seeded), turned into
 PIFA form on the GPU by pifa_build_f64 (QR with column pivoting, timed and
@@ -291,6 +291,37 @@ def measure_group(seed):
     return out
 
 
+def measure_backward(wl: Workload, M: int, iters: int = 10, warmup: int = 3):
+    """pifa_layer_backward at M rows: dX, dW_p and dC from X, the forward's Y
+    and a random dY.  Useful FLOPs are twice the forward's (Sec. 3.3 cost for
+    each of the two transposed products)."""
+    import torch
+    pifa = wl.pifa
+    from paper_2501_19090_amd import inputs
+    h = wl.pifa_h[0]
+    x = torch.from_numpy(inputs.round_bf16(inputs.activations(M, wl.d_in, 31))[0].view(np.int16)).cuda().view(
+        torch.bfloat16)
+    g = torch.from_numpy(inputs.round_bf16(inputs.activations(M, wl.d_out, 32))[0].view(np.int16)).cuda().view(
+        torch.bfloat16)
+    y = torch.empty((M, wl.d_out), dtype=torch.bfloat16, device="cuda:0")
+    pifa.pifa_forward(h, x, y, M)
+    dx = torch.empty((M, wl.d_in), dtype=torch.bfloat16, device="cuda:0")
+    dwp = torch.empty((wl.r, wl.d_in), dtype=torch.float32, device="cuda:0")
+    dc = torch.empty((wl.d_out - wl.r, wl.r), dtype=torch.float32, device="cuda:0")
+    call = lambda: pifa.pifa_layer_backward(h, x, y, g, dx, dwp, dc, M)
+    call()  # builds the transposed weight copies and the workspace
+    torch.cuda.synchronize()
+    pifa.pifa_profile_reset()
+    pifa.pifa_profile_enable(True)
+    t = time_rotating([call], iters, warmup)
+    pifa.pifa_profile_enable(False)
+    kern = pifa.pifa_profile_read()
+    pifa.pifa_profile_reset()
+    flops = 2 * pifa_flops(M, wl.d_in, wl.d_out, wl.r)
+    return {"M": M, "us": 1e3 * t, "tflops": flops / (t * 1e9), "useful_flops": flops,
+            "kernels": {k: {"launches": n, "avg_us": 1e3 * v / n} for k, (n, v) in kern.items()}}
+
+
 def cpu_baseline(wl, M_full, budget_s=10.0):
     """The fp64 oracle's PIFA forward on a bounded row sample of the workload
     (the same bf16 layer the GPU runs)."""
@@ -425,6 +456,8 @@ def main():
     if not args.no_cpu:
         cpu = cpu_baseline(wl, M)
         log("cpu baseline:", json.dumps(cpu))
+    backward = measure_backward(wl, M)
+    log("backward:", json.dumps(backward))
     grouped = measure_group(inputs.config_seed(2))
     log("grouped:", json.dumps(grouped))
     build = {"ms": wl.build_ms, "report": wl.build_report,
@@ -449,6 +482,7 @@ def main():
         "decode": decode,
         "build": build,
         "grouped": grouped,
+        "backward": backward,
         "kernels": kernels,
         "paper_context": "arXiv 2501.19090 reports, on an NVIDIA RTX A6000 (d=8192, 65,536 rows), "
                          "24.2% memory saving and 24.6% lower time than the low-rank layer at r=d/2",

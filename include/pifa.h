@@ -153,9 +153,9 @@ pifa_status pifa_layer_overflow_count(pifa_handle h, int64_t* count);
  * layers only (PIFA_F32 returns PIFA_ERR_UNSUPPORTED).  The first call builds
  * transposed copies of W_p and C in the layer (synchronous); the handle's
  * backward workspace grows on demand (synchronising `stream`).  Calls on one
- * handle must not overlap.  G_p reaches dX as a bf16 pair (about 16
- * significant bits), since C makes that product cancel; the other products
- * take bf16 operands; all accumulate in fp32.
+ * handle must not overlap.  G_p reaches dX in fp16 with a power-of-two
+ * scale per row (C makes that product cancel, and bf16 is too coarse there);
+ * the other products take bf16 operands; all accumulate in fp32.
  */
 pifa_status pifa_layer_backward(pifa_handle h, const void* X, const void* Y, const void* dY, int64_t M,
                                 void* dX, float* dW_p, float* dC, void* stream);

@@ -13,10 +13,13 @@
 // the epilogue of the G_p product.
 //
 // Precision: G_p multiplies W_p in dX = G_p W_p with the same cancellation as
-// Y_p C^T in the forward (C rebuilds W_np from W_p), so G_p is handed to that
-// product as a bf16 pair hi + lo (about 16 significant bits) against W_p^T
-// stored twice along K.  dW_p and dC have no such cancellation and use bf16
-// operands; all products accumulate in fp32.
+// Y_p C^T in the forward (C rebuilds W_np from W_p): a bf16 G_p misses the
+// bf16 bar there (about 7e-3 measured on QR-pivoted layers), fp16 meets it
+// (about 2e-3).  G_p is therefore kept in fp32 and converted row by row to
+// fp16 times 2^s_m, s_m chosen from the row's largest |value|, against an
+// fp16 copy of W_p^T scaled by 2^c; the product is multiplied back by
+// 2^-(s_m + c), which is exact.  dW_p and dC have no such cancellation and
+// use bf16 operands; all products accumulate in fp32.
 #pragma once
 
 #include "common.hpp"
@@ -43,15 +46,15 @@ __device__ __forceinline__ float to_f32<f16>(f16 v) {
     return (float)v;
 }
 
-// dst = lane order of a (rows_log x cols_log) bf16 matrix whose element
+// dst = lane order of a (rows_log x cols_log) matrix of type TD whose element
 // (i, c) is src(c mod period, i) * scale, where src is a lane-ordered matrix
 // (src_kb column blocks per row group) of which rows < src_rows and columns
-// < src_cols are valid; everything else is zero.  Used for W_p^T stored twice
-// along K (period = r_pad) and for C^T in bf16 (period = cols_log, scale
-// undoing C's fp16 scale, exact for bf16-representable C).
-template <typename TS>
+// < src_cols are valid; everything else is zero.  Used for W_p^T in fp16
+// times 2^c and for C^T in bf16 (scale undoing C's fp16 scale, exact for
+// bf16-representable C); period = cols_log unless a copy repeats along K.
+template <typename TS, typename TD>
 __global__ void pack_transposed(const TS* __restrict__ src, int64_t src_kb, int64_t src_rows, int64_t src_cols,
-                                int64_t period, float scale, bf16* __restrict__ dst, int64_t rows_log,
+                                int64_t period, float scale, TD* __restrict__ dst, int64_t rows_log,
                                 int64_t cols_log) {
     const int64_t KB = packed_kblocks(cols_log);
     const int64_t nchunks = packed_groups(rows_log) * KB * kPackChunks;
@@ -63,7 +66,7 @@ __global__ void pack_transposed(const TS* __restrict__ src, int64_t src_kb, int6
         const int64_t g = blk / KB, b = blk % KB;
         const int64_t i = g * kPackRows + (l % 16);
         const int64_t k0 = b * kPackCols + 32 * (l / 16) + 8 * c;
-        uint16_t* out = reinterpret_cast<uint16_t*>(dst) + ch * 8;
+        TD* out = dst + ch * 8;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
             const int64_t k = k0 + e;
@@ -71,53 +74,65 @@ __global__ void pack_transposed(const TS* __restrict__ src, int64_t src_kb, int6
             float v = 0.f;
             if (i < rows_log && k < cols_log && s < src_rows && i < src_cols)
                 v = to_f32<TS>(src[lane_order_index(s, i, src_kb)]) * scale;
-            out[e] = f32_to_bf16_bits(v);
+            if constexpr (__is_same(TD, f16)) out[e] = (f16)v;
+            else reinterpret_cast<uint16_t*>(out)[e] = f32_to_bf16_bits(v);
         }
     }
 }
 
-// out[m * ld_out + j] = in[m * ld_in + idx[j]] for j < ncols, zero for
-// ncols <= j < ld_out (the K padding of a GEMM operand).
-__global__ void gather_cols(const bf16* __restrict__ in, int64_t ld_in, int64_t M, const int32_t* __restrict__ idx,
-                            int64_t ncols, bf16* __restrict__ out, int64_t ld_out) {
-    const uint16_t* src = reinterpret_cast<const uint16_t*>(in);
-    uint16_t* dst = reinterpret_cast<uint16_t*>(out);
-    const int64_t total = M * ld_out;
-    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
-         e += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t m = e / ld_out, j = e % ld_out;
-        dst[e] = j < ncols ? src[m * ld_in + idx[j]] : (uint16_t)0;
-    }
-}
-
-// out[j * ld_out + m] = in[m * ld_in + col(j)] for j < ncols and m < M, with
-// col(j) = idx[j] (or j when idx is null); zero for M <= m < ld_out.  64 x 64
-// tiles through LDS so both the reads (along j) and the writes (along m) are
-// row-contiguous.  Grid: (ceil(ld_out / 64), ceil(ncols / 64)), 256 threads.
+// One pass over a 64 x 64 tile of in[m][col(j)] (col(j) = idx[j], or j when
+// idx is null), for m < M and j < ncols, written
+//   row-major:  out_r[m * ld_r + j]  (j < ld_r; zero for j >= ncols), and/or
+//   transposed: out_t[j * ld_t + m]  (m < ld_t; zero for m >= M),
+// with 16-byte stores (ld_r, ld_t multiples of 8).  The gathered loads are
+// 2 bytes wide; with sorted indices neighbouring lanes read neighbouring
+// columns of one row.  Grid: (ceil(max(M, ld_t) / 64), ceil(max(ncols, ld_r) / 64)).
 constexpr int kTrTile = 64;
 
-__global__ __launch_bounds__(256) void gather_transpose(const bf16* __restrict__ in, int64_t ld_in, int64_t M,
-                                                        const int32_t* __restrict__ idx, int64_t ncols,
-                                                        bf16* __restrict__ out, int64_t ld_out) {
-    __shared__ uint16_t tile[kTrTile][kTrTile + 1];
+__global__ __launch_bounds__(256) void gather_tile(const bf16* __restrict__ in, int64_t ld_in, int64_t M,
+                                                   const int32_t* __restrict__ idx, int64_t ncols,
+                                                   bf16* __restrict__ out_r, int64_t ld_r, bf16* __restrict__ out_t,
+                                                   int64_t ld_t) {
+    __shared__ uint16_t tile[kTrTile][kTrTile + 2];
     const uint16_t* src = reinterpret_cast<const uint16_t*>(in);
-    uint16_t* dst = reinterpret_cast<uint16_t*>(out);
     const int64_t m0 = (int64_t)blockIdx.x * kTrTile, j0 = (int64_t)blockIdx.y * kTrTile;
     const int tid = threadIdx.x;
+    {
+        const int jj = tid % kTrTile;
+        const int64_t j = j0 + jj;
+        const int64_t cj = j < ncols ? (idx ? (int64_t)idx[j] : j) : 0;
 #pragma unroll
-    for (int i = 0; i < kTrTile * kTrTile / 256; ++i) {
-        const int t = tid + 256 * i, mm = t / kTrTile, jj = t % kTrTile;
-        const int64_t m = m0 + mm, j = j0 + jj;
-        uint16_t v = 0;
-        if (m < M && j < ncols) v = src[m * ld_in + (idx ? (int64_t)idx[j] : j)];
-        tile[mm][jj] = v;
+        for (int i = 0; i < kTrTile * kTrTile / 256; ++i) {
+            const int mm = tid / kTrTile + 4 * i;
+            const int64_t m = m0 + mm;
+            tile[mm][jj] = (m < M && j < ncols) ? src[m * ld_in + cj] : (uint16_t)0;
+        }
     }
     __syncthreads();
 #pragma unroll
-    for (int i = 0; i < kTrTile * kTrTile / 256; ++i) {
-        const int t = tid + 256 * i, jj = t / kTrTile, mm = t % kTrTile;
-        const int64_t m = m0 + mm, j = j0 + jj;
-        if (j < ncols && m < ld_out) dst[j * ld_out + m] = tile[mm][jj];
+    for (int i = 0; i < 2; ++i) {
+        const int ch = tid + 256 * i;  // 512 chunks of 8 elements per tile
+        const int a = ch / 8, b8 = (ch % 8) * 8;
+        if (out_r) {  // row m0 + a, columns j0 + b8 .. +7
+            const int64_t m = m0 + a, j = j0 + b8;
+            if (m < M && j < ld_r) {
+                uint16_t v[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) v[e] = tile[a][b8 + e];
+                *reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(out_r) + m * ld_r + j) =
+                    __builtin_bit_cast(u32x4, v);
+            }
+        }
+        if (out_t) {  // row j0 + a of the transpose, columns m0 + b8 .. +7
+            const int64_t j = j0 + a, m = m0 + b8;
+            if (j < ncols && m < ld_t) {
+                uint16_t v[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) v[e] = tile[b8 + e][a];
+                *reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(out_t) + j * ld_t + m) =
+                    __builtin_bit_cast(u32x4, v);
+            }
+        }
     }
 }
 
@@ -132,18 +147,16 @@ __global__ void zero_cols(bf16* __restrict__ p, int64_t rows, int64_t ld, int64_
 
 // Epilogue of G_p = G[:, I^c] C (+ G[:, I]): acc(m, j) for j < r_pad.
 //   * adds G[m, piv[j]] for j < r;
-//   * writes the bf16 pair hi = bf16(g), lo = bf16(g - hi) to
-//     split[m * lds + j] and split[m * lds + r_pad + j] (the A operand of
-//     dX = [hi | lo] [W_p^T | W_p^T]^T); padding columns j >= r get zeros;
-//   * writes hi transposed to gpt[j * ldt + m] for j < r (the A operand of
-//     dW_p = G_p^T X).
+//   * writes G_p in fp32 to gp[m * r_pad + j] (padding columns j >= r get
+//     zeros), for the row-wise fp16 conversion;
+//   * writes bf16(G_p) transposed to gpt[j * ldt + m] for j < r (the A
+//     operand of dW_p = G_p^T X).
 struct GradPivotEpi {
     const bf16* G;
     int64_t ldg;
     const int32_t* piv;
     int64_t r, r_pad;
-    bf16* split;
-    int64_t lds;
+    float* gp;
     bf16* gpt;
     int64_t ldt;
     int64_t M;
@@ -164,12 +177,60 @@ struct GradPivotEpi {
         if (m >= M || c.n >= r_pad) return;
         const uint16_t* g16 = reinterpret_cast<const uint16_t*>(G);
         const float g = c.piv_ok ? v + bf16_bits_to_f32(g16[m * ldg + c.src]) : 0.f;
-        const uint16_t hi = f32_to_bf16_bits(g);
-        const uint16_t lo = f32_to_bf16_bits(g - bf16_bits_to_f32(hi));
-        uint16_t* s16 = reinterpret_cast<uint16_t*>(split);
-        s16[m * lds + c.n] = hi;
-        s16[m * lds + r_pad + c.n] = lo;
-        if (c.piv_ok) reinterpret_cast<uint16_t*>(gpt)[c.n * ldt + m] = hi;
+        gp[m * r_pad + c.n] = g;
+        if (c.piv_ok) reinterpret_cast<uint16_t*>(gpt)[c.n * ldt + m] = f32_to_bf16_bits(g);
+    }
+};
+
+// Row m of gp (n = r_pad fp32 values, n % 4 == 0) -> fp16 out[m][:] times
+// 2^s_m with the row's largest |value| in [2^14, 2^15) (s_m = 0 for a zero
+// row), and inv[m] = 2^-s_m.  One workgroup of 256 threads per row.
+__global__ __launch_bounds__(256) void rows_to_f16(const float* __restrict__ gp, int64_t n, f16* __restrict__ out,
+                                                   float* __restrict__ inv) {
+    __shared__ float red[256 / kWave];
+    const int64_t m = blockIdx.x;
+    const f32x4* row = reinterpret_cast<const f32x4*>(gp + m * n);
+    const int64_t nq = n / 4;
+    float mx = 0.f;
+    for (int64_t q = threadIdx.x; q < nq; q += 256) {
+        const f32x4 v = row[q];
+        mx = fmaxf(mx, fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))));
+    }
+    for (int off = kWave / 2; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+    if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = mx;
+    __syncthreads();
+    mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    int s = 0;
+    if (mx > 0.f && __builtin_isfinite(mx)) {
+        int e = 0;
+        (void)frexpf(mx, &e);  // mx = f * 2^e, f in [0.5, 1)
+        s = 15 - e;            // mx * 2^s in [2^14, 2^15)
+        s = s < -100 ? -100 : (s > 100 ? 100 : s);
+    }
+    const float sc = ldexpf(1.f, s);
+    for (int64_t q = threadIdx.x; q < nq; q += 256) {
+        const f32x4 v = row[q];
+        f16 h[4] = {(f16)(v[0] * sc), (f16)(v[1] * sc), (f16)(v[2] * sc), (f16)(v[3] * sc)};
+        *reinterpret_cast<uint64_t*>(out + m * n + 4 * q) = __builtin_bit_cast(uint64_t, h);
+    }
+    if (threadIdx.x == 0) inv[m] = ldexpf(1.f, -s);
+}
+
+// Epilogue writing round(acc(m, n) * row_scale[m] * out_scale) to
+// out[m * ldo + n] (bf16) for m < M, n < N.
+struct RowScaleEpi {
+    bf16* out;
+    int64_t ldo, N;
+    const float* row_scale;
+    float out_scale;
+    int64_t M;
+    struct Col {
+        int64_t n;
+        bool ok;
+    };
+    __device__ __forceinline__ Col col(int64_t n) const { return Col{n, n < N}; }
+    __device__ __forceinline__ void store(int64_t m, const Col& c, float v) const {
+        if (m < M && c.ok) Store<bf16>::put(out + m * ldo + c.n, v * row_scale[m] * out_scale);
     }
 };
 

@@ -97,6 +97,7 @@ enum Site {
     kSiteBwdDx,
     kSiteBwdDwp,
     kSiteBwdDc,
+    kSiteBwdRows,
     kSiteCount
 };
 
@@ -106,7 +107,7 @@ const char* const kSiteNames[kSiteCount] = {
     "dense_f32",           "lowrank_gemm1_xv",    "lowrank_gemm2_tu",    "lowrank_gemv1_xv",
     "lowrank_gemv2_tu",    "lowrank_f32",         "pifa_group_gemm1",    "pifa_group_gemm2",
     "pifa_group_gemv1",    "pifa_group_gemv2",    "pifa_bwd_gather",     "pifa_bwd_gp",
-    "pifa_bwd_dx",         "pifa_bwd_dwp",        "pifa_bwd_dc"};
+    "pifa_bwd_dx",         "pifa_bwd_dwp",        "pifa_bwd_dc",         "pifa_bwd_rows_f16"};
 
 struct Profiler {
     std::mutex mu;
@@ -422,8 +423,9 @@ struct pifa_layer {
     GrowBuf ws;                // Y_p hand-off
     GrowBuf part;              // K-split partial products
     // backward, built on first use from the packed forward weights
-    void* bwd_wpt = nullptr;   // lane order of d_in x 2 r_pad: [W_p^T | W_p^T]
+    void* bwd_wpt = nullptr;   // lane order of d_in x r_pad: W_p^T in fp16 times 2^bwd_cw
     void* bwd_ct = nullptr;    // lane order of r_pad x ldc: C^T in bf16 (ldc = n_np rounded up to 8)
+    int bwd_cw = 0;
     GrowBuf bws;               // backward operands and partial products
 };
 
@@ -1057,20 +1059,26 @@ inline int64_t align_elems(int64_t n) { return round_up(n, (int64_t)128); }  // 
 pifa_status prepare_backward(pifa_layer* h) {
     if (h->bwd_wpt) return PIFA_OK;
     const int64_t ldc = round_up(h->n_np, (int64_t)8);
+    float mx = 0.f;
+    pifa_status s = absmax_bf16_host(h->Wp, packed_elems(h->r_pad, h->d_in), &mx);
+    if (s != PIFA_OK) return s;
+    // scale so that max|W_p| * 2^cw lies in [2^14, 2^15), as for C
+    const int cw = mx > 0.f ? std::max(-30, std::min(30, 14 - (int)std::floor(std::log2((double)mx)))) : 0;
     void* wpt = nullptr;
     void* ct = nullptr;
-    if (hipMalloc(&wpt, (size_t)packed_elems(h->d_in, 2 * h->r_pad) * 2) != hipSuccess) return PIFA_ERR_OOM;
+    if (hipMalloc(&wpt, (size_t)packed_elems(h->d_in, h->r_pad) * 2) != hipSuccess) return PIFA_ERR_OOM;
     if (h->n_np > 0 && hipMalloc(&ct, (size_t)packed_elems(h->r_pad, ldc) * 2) != hipSuccess) {
         (void)hipFree(wpt);
         return PIFA_ERR_OOM;
     }
-    const int64_t c1 = packed_groups(h->d_in) * packed_kblocks(2 * h->r_pad) * kPackChunks;
-    hipLaunchKernelGGL((pack_transposed<bf16>), dim3(grid_for(c1)), dim3(256), 0, 0, (const bf16*)h->Wp,
-                       packed_kblocks(h->d_in), h->r, h->d_in, h->r_pad, 1.f, (bf16*)wpt, h->d_in, 2 * h->r_pad);
+    const int64_t c1 = packed_groups(h->d_in) * packed_kblocks(h->r_pad) * kPackChunks;
+    hipLaunchKernelGGL((pack_transposed<bf16, f16>), dim3(grid_for(c1)), dim3(256), 0, 0, (const bf16*)h->Wp,
+                       packed_kblocks(h->d_in), h->r, h->d_in, h->r_pad, std::ldexp(1.0f, cw), (f16*)wpt, h->d_in,
+                       h->r_pad);
     bool ok = hipGetLastError() == hipSuccess;
     if (ok && ct) {
         const int64_t c2 = packed_groups(h->r_pad) * packed_kblocks(ldc) * kPackChunks;
-        hipLaunchKernelGGL((pack_transposed<f16>), dim3(grid_for(c2)), dim3(256), 0, 0, (const f16*)h->C,
+        hipLaunchKernelGGL((pack_transposed<f16, bf16>), dim3(grid_for(c2)), dim3(256), 0, 0, (const f16*)h->C,
                            packed_kblocks(h->r_pad), h->n_np, h->r, ldc, std::ldexp(1.0f, -h->c_log2), (bf16*)ct,
                            h->r_pad, ldc);
         ok = hipGetLastError() == hipSuccess;
@@ -1083,14 +1091,18 @@ pifa_status prepare_backward(pifa_layer* h) {
     }
     h->bwd_wpt = wpt;
     h->bwd_ct = ct;
+    h->bwd_cw = cw;
     return PIFA_OK;
 }
 
-hipError_t launch_gather_transpose(const bf16* in, int64_t ld_in, int64_t M, const int32_t* idx, int64_t ncols,
-                                   bf16* out, int64_t ld_out, hipStream_t st) {
-    if (ncols == 0 || ld_out == 0) return hipSuccess;
-    hipLaunchKernelGGL(gather_transpose, dim3((unsigned)ceil_div(ld_out, kTrTile), (unsigned)ceil_div(ncols, kTrTile)),
-                       dim3(256), 0, st, in, ld_in, M, idx, ncols, out, ld_out);
+// gather_tile over all of in's needed tiles (see backward.hpp).
+hipError_t launch_gather(const bf16* in, int64_t ld_in, int64_t M, const int32_t* idx, int64_t ncols, bf16* out_r,
+                         int64_t ld_r, bf16* out_t, int64_t ld_t, hipStream_t st) {
+    const int64_t mx = std::max(M, out_t ? ld_t : (int64_t)0);
+    const int64_t nx = std::max(ncols, out_r ? ld_r : (int64_t)0);
+    if (mx == 0 || nx == 0) return hipSuccess;
+    hipLaunchKernelGGL(gather_tile, dim3((unsigned)ceil_div(mx, kTrTile), (unsigned)ceil_div(nx, kTrTile)), dim3(256),
+                       0, st, in, ld_in, M, idx, ncols, out_r, ld_r, out_t, ld_t);
     return hipGetLastError();
 }
 
@@ -1115,53 +1127,55 @@ pifa_status pifa_layer_backward(pifa_handle h, const void* X, const void* Y, con
     if (s != PIFA_OK) return s;
 
     const int64_t M_pad = round_up(M, (int64_t)8), ldc = round_up(n_np, (int64_t)8);
-    // workspace regions (bf16 elements)
+    // workspace regions, in 2-byte elements (each a multiple of 256 bytes)
     const int64_t e_gic = align_elems(M * ldc), e_gict = align_elems(n_np * M_pad), e_ypt = align_elems(r * M_pad),
-                  e_xt = align_elems(d_in * M_pad), e_spl = align_elems(M * 2 * r_pad),
-                  e_gpt = align_elems(r * M_pad);
-    const size_t part = std::max({split_bytes(M, r_pad, ldc), split_bytes(M, d_in, 2 * r_pad),
+                  e_xt = align_elems(d_in * M_pad), e_gp32 = align_elems(2 * M * r_pad),
+                  e_gp16 = align_elems(M * r_pad), e_inv = align_elems(2 * M), e_gpt = align_elems(r * M_pad);
+    const size_t part = std::max({split_bytes(M, r_pad, ldc), split_bytes(M, d_in, r_pad),
                                   split_bytes(r, d_in, M_pad), split_bytes(n_np, r, M_pad)});
-    const size_t bf_bytes = (size_t)(e_gic + e_gict + e_ypt + e_xt + e_spl + e_gpt) * 2;
-    s = h->bws.ensure(bf_bytes + part, st);
+    const size_t main_bytes = (size_t)(e_gic + e_gict + e_ypt + e_xt + e_gp32 + e_gp16 + e_inv + e_gpt) * 2;
+    s = h->bws.ensure(main_bytes + part, st);
     if (s != PIFA_OK) return s;
-    bf16* base = (bf16*)h->bws.ptr;
-    bf16* gic = base;
+    bf16* gic = (bf16*)h->bws.ptr;
     bf16* gict = gic + e_gic;
     bf16* ypt = gict + e_gict;
     bf16* xt = ypt + e_ypt;
-    bf16* spl = xt + e_xt;
-    bf16* gpt = spl + e_spl;
-    float* partials = part ? (float*)((char*)h->bws.ptr + bf_bytes) : nullptr;
+    float* gp32 = (float*)(xt + e_xt);
+    f16* gp16 = (f16*)(xt + e_xt + e_gp32);
+    float* inv = (float*)(xt + e_xt + e_gp32 + e_gp16);
+    bf16* gpt = xt + e_xt + e_gp32 + e_gp16 + e_inv;
+    float* partials = part ? (float*)((char*)h->bws.ptr + main_bytes) : nullptr;
     const bf16* G = (const bf16*)dY;
     hipError_t e = hipSuccess;
 
-    {  // operands in K-contiguous form
+    {  // operands in K-contiguous form: G[:, I^c] (rows and transposed), Y_p^T, X^T
         TimedLaunch timed(kSiteBwdData, st);
-        if (n_np > 0) {
-            hipLaunchKernelGGL(gather_cols, dim3(grid_for(M * ldc)), dim3(256), 0, st, G, d_out, M, h->npiv, n_np,
-                               gic, ldc);
-            if ((e = hipGetLastError()) != hipSuccess) return PIFA_ERR_HIP;
-            if (dC && (e = launch_gather_transpose(G, d_out, M, h->npiv, n_np, gict, M_pad, st)) != hipSuccess)
-                return PIFA_ERR_HIP;
-            if (dC && (e = launch_gather_transpose((const bf16*)Y, d_out, M, h->piv, r, ypt, M_pad, st)) != hipSuccess)
-                return PIFA_ERR_HIP;
-        }
-        if (dW_p && (e = launch_gather_transpose((const bf16*)X, d_in, M, nullptr, d_in, xt, M_pad, st)) != hipSuccess)
+        if (n_np > 0 && (e = launch_gather(G, d_out, M, h->npiv, n_np, gic, ldc, dC ? gict : nullptr, M_pad, st)) !=
+                            hipSuccess)
+            return PIFA_ERR_HIP;
+        if (n_np > 0 && dC &&
+            (e = launch_gather((const bf16*)Y, d_out, M, h->piv, r, nullptr, 0, ypt, M_pad, st)) != hipSuccess)
+            return PIFA_ERR_HIP;
+        if (dW_p && (e = launch_gather((const bf16*)X, d_in, M, nullptr, d_in, nullptr, 0, xt, M_pad, st)) != hipSuccess)
             return PIFA_ERR_HIP;
     }
-    // G_p = G[:, I^c] C + G[:, I], as a bf16 pair and transposed
+    // G_p = G[:, I^c] C + G[:, I] in fp32, and bf16(G_p)^T
     e = launch_gemm<bf16, true>(kSiteBwdGp, gic, ldc, M, (const bf16*)h->bwd_ct, 0, r_pad, ldc,
-                                GradPivotEpi{G, d_out, h->piv, r, r_pad, spl, 2 * r_pad, gpt, M_pad, M}, partials, st);
+                                GradPivotEpi{G, d_out, h->piv, r, r_pad, gp32, gpt, M_pad, M}, partials, st);
     if (e != hipSuccess) return PIFA_ERR_HIP;
     if (M_pad > M) {
         hipLaunchKernelGGL(zero_cols, dim3(grid_for(r * (M_pad - M))), dim3(256), 0, st, gpt, r, M_pad, M);
         if (hipGetLastError() != hipSuccess) return PIFA_ERR_HIP;
     }
-    if (dX) {  // dX = [hi | lo] [W_p^T | W_p^T]^T
-        e = launch_gemm<bf16, true>(kSiteBwdDx, spl, 2 * r_pad, M, (const bf16*)h->bwd_wpt, 0, d_in, 2 * r_pad,
-                                    make_epi<bf16, kWsNone>((bf16*)dX, d_in, nullptr, d_in, 1.f, nullptr, 0, 0, 1.f,
-                                                            nullptr, M),
-                                    partials, st);
+    if (dX) {  // dX = (G_p 2^s_m in fp16) (W_p^T 2^cw in fp16)^T 2^-(s_m + cw)
+        {
+            TimedLaunch timed(kSiteBwdRows, st);
+            hipLaunchKernelGGL(rows_to_f16, dim3((unsigned)M), dim3(256), 0, st, gp32, r_pad, gp16, inv);
+            if (hipGetLastError() != hipSuccess) return PIFA_ERR_HIP;
+        }
+        e = launch_gemm<f16, true>(kSiteBwdDx, gp16, r_pad, M, (const f16*)h->bwd_wpt, 0, d_in, r_pad,
+                                   RowScaleEpi{(bf16*)dX, d_in, d_in, inv, std::ldexp(1.0f, -h->bwd_cw), M}, partials,
+                                   st);
         if (e != hipSuccess) return PIFA_ERR_HIP;
     }
     if (dW_p) {  // dW_p = G_p^T X
