@@ -47,8 +47,11 @@ typedef enum {
     PIFA_ERR_UNSUPPORTED = -3, /* a shape or alignment this build lacks  */
     PIFA_ERR_HIP = -4,         /* a HIP runtime call or launch failed    */
     PIFA_ERR_OOM = -5,         /* device memory allocation failed        */
-    PIFA_ERR_NOT_RANK_R = -6   /* pifa_build_f64: W' is not numerically  */
+    PIFA_ERR_NOT_RANK_R = -6,  /* pifa_build_f64: W' is not numerically  */
                                /* of rank r                              */
+    PIFA_ERR_NOT_SPD = -7      /* pifa_calib_reconstruct: a normal-      */
+                               /* equation matrix is not positive        */
+                               /* definite (too few calibration rows)    */
 } pifa_status;
 
 /* Layer shape: W is d_out x d_in with rank r, 1 <= r <= min(d_in, d_out)
@@ -64,6 +67,7 @@ typedef struct pifa_layer* pifa_handle;
 typedef struct lowrank_layer* lowrank_handle;
 typedef struct dense_layer* dense_handle;
 typedef struct pifa_group* pifa_group_handle;
+typedef struct pifa_calib* pifa_calib_handle;
 
 /* Human-readable name of a status code (static storage, never NULL). */
 const char* pifa_status_string(pifa_status s);
@@ -249,6 +253,55 @@ pifa_status lowrank_layer_forward(lowrank_handle h, const void* X, void* Y, int6
                                   void* stream);
 pifa_status lowrank_layer_reserve(lowrank_handle h, int64_t max_M);
 pifa_status lowrank_layer_destroy(lowrank_handle h);
+
+/*
+ * Online Error-Accumulation-Minimization reconstruction (Sec. 4; Part 1 of
+ * Algorithm "MPIFA" in the appendix "Experiment Details").  A calibration
+ * handle keeps the running sums of one layer with input width d_in = n:
+ *   S = sum_i x_u^i x_u^i^T   and   P = sum_i x_o^i x_u^i^T   (n x n, fp64),
+ * x_o from the dense data flow and x_u from the low-rank one.  The mixed
+ * target sum of the paper is T = sum_i y_t^i x_u^i^T = W (lam P + (1 - lam) S)
+ * (eq. mix_original_output, regrouped by associativity), so the dense
+ * weight is not needed until the solve and one handle serves any mix ratio.
+ */
+pifa_status pifa_calib_create(int64_t d_in, pifa_calib_handle* out);
+pifa_status pifa_calib_destroy(pifa_calib_handle c);
+
+/* Zero the sums (asynchronous on `stream`). */
+pifa_status pifa_calib_reset(pifa_calib_handle c, void* stream);
+
+/*
+ * Add one batch of B calibration rows (tokens): X_o and X_u device, bf16,
+ * B x d_in row-major, no alignment required (X_o may equal X_u).  The
+ * products run on the MFMA GEMM with fp32 accumulation over the batch; the
+ * batch results are added to the fp64 sums.  Asynchronous on `stream`; calls
+ * on one handle must not overlap.
+ */
+pifa_status pifa_calib_accumulate(pifa_calib_handle c, const void* X_o, const void* X_u, int64_t B,
+                                  void* stream);
+
+/* Copy the sums into device fp64 n x n buffers (either may be NULL). */
+pifa_status pifa_calib_read(pifa_calib_handle c, double* S, double* P, void* stream);
+
+/*
+ * Steps 5 and 6 of Algorithm "MPIFA" with the regularised V update
+ * (eq. lsq_v_reg), in fp64 on the device:
+ *   T     = W (lam P + (1 - lam) S)
+ *   U_r   = T V (V^T S V)^-1                                  (eq. lsq_online)
+ *   V_r^T = (U_r^T U_r)^-1 U_r^T (T + alpha W) (S + alpha I)^-1
+ * with the paper's V = Vt^T.  Squared Frobenius norms are read into the
+ * objectives, the only reading under which these closed forms are minimisers.
+ *   W     device fp64, d_out x d_in (the dense weight).
+ *   Vt    device fp64, r x d_in (V^T of the low-rank start U V^T).
+ *   U_r   device fp64, d_out x r (output).   Vt_r  device fp64, r x d_in (output).
+ * 1 <= r <= min(d_in, d_out).  The three symmetric systems are solved by
+ * Cholesky factorisation; a matrix that is not positive definite returns
+ * PIFA_ERR_NOT_SPD (outputs undefined).  Synchronises `stream` (it reads the
+ * factorisation status); work memory is owned by the handle.
+ */
+pifa_status pifa_calib_reconstruct(pifa_calib_handle c, const double* W, int64_t d_out, const double* Vt,
+                                   int64_t r, double lam, double alpha, double* U_r, double* Vt_r,
+                                   void* stream);
 
 /*
  * Algorithm "Pivoting Factorization" (Sec. 3.2) on the GPU, in fp64: QR with

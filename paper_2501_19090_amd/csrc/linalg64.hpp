@@ -1,0 +1,232 @@
+// fp64 dense linear algebra for the reconstruction solves of Sec. 4 (the
+// closed-form U and V updates of Algorithm "MPIFA", Part 1).  These run once
+// per layer on n x n and r x r systems; the hot part of the reconstruction is
+// the accumulation of the calibration sums, which runs on the MFMA GEMM.
+//
+//   gemm64        C = alpha op(A) op(B) + beta C with arbitrary element strides
+//                 (transposes are strides, no copies); optional lower-triangle
+//                 tiles only, for symmetric updates.
+//   Cholesky      A = L L^T, right-looking in 64-column blocks: diagonal block
+//                 in one workgroup's LDS, panel by forward substitution, trailing
+//                 update by gemm64 (lower tiles only).
+//   spd solve     L L^T X = B for many right-hand sides: blocked forward and
+//                 backward substitution with gemm64 updates.
+#pragma once
+
+#include "common.hpp"
+
+namespace pifa {
+
+constexpr int kG64 = 64;  // output tile
+constexpr int kG64K = 16; // K step
+
+// C[i*sc0 + j*sc1] = alpha * sum_k A[i*sa0 + k*sa1] * B[k*sb0 + j*sb1] + beta * C[...]
+// for i < Mr, j < Nc.  LOWER: only tiles whose first row >= first column
+// (tiles on the diagonal are computed whole).  beta == 0 ignores C's old value.
+// Grid: (ceil(Nc / 64), ceil(Mr / 64)), 256 threads, 4 x 4 outputs each.
+__global__ __launch_bounds__(256) void gemm64(int64_t Mr, int64_t Nc, int64_t K, double alpha, const double* __restrict__ A,
+                                              int64_t sa0, int64_t sa1, const double* __restrict__ B, int64_t sb0,
+                                              int64_t sb1, double beta, double* __restrict__ C, int64_t sc0, int64_t sc1,
+                                              int lower) {
+    const int64_t i0 = (int64_t)blockIdx.y * kG64, j0 = (int64_t)blockIdx.x * kG64;
+    if (lower && j0 > i0) return;
+    __shared__ double As[kG64K][kG64 + 1];
+    __shared__ double Bs[kG64K][kG64 + 1];
+    const int tid = threadIdx.x, tx = tid % 16, ty = tid / 16;
+    double acc[4][4] = {};
+    for (int64_t k0 = 0; k0 < K; k0 += kG64K) {
+        // 64 x 16 tile of A and 16 x 64 tile of B; consecutive threads walk the unit-stride axis
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int e = tid + 256 * q;
+            int ii, kk;
+            if (sa1 == 1) { ii = e / kG64K; kk = e % kG64K; }
+            else { kk = e / kG64; ii = e % kG64; }
+            const int64_t i = i0 + ii, k = k0 + kk;
+            As[kk][ii] = (i < Mr && k < K) ? A[i * sa0 + k * sa1] : 0.0;
+            int jj, kb;
+            if (sb1 == 1) { kb = e / kG64; jj = e % kG64; }
+            else { jj = e / kG64K; kb = e % kG64K; }
+            const int64_t j = j0 + jj, kB = k0 + kb;
+            Bs[kb][jj] = (j < Nc && kB < K) ? B[kB * sb0 + j * sb1] : 0.0;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < kG64K; ++kk) {
+            double a[4], b[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                a[u] = As[kk][ty + 16 * u];
+                b[u] = Bs[kk][tx + 16 * u];
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) acc[u][v] = fma(a[u], b[v], acc[u][v]);
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int64_t i = i0 + ty + 16 * u, j = j0 + tx + 16 * v;
+            if (i < Mr && j < Nc) {
+                double* c = C + i * sc0 + j * sc1;
+                *c = beta == 0.0 ? alpha * acc[u][v] : fma(alpha, acc[u][v], beta * *c);
+            }
+        }
+}
+
+// *out = 1e-13 * max_i A[i][i] (n x n, row stride ld): the smallest pivot a
+// factorisation accepts, i.e. a bound of about 1e13 on the condition number.
+// One workgroup of 256 threads.
+constexpr double kPivotTol = 1e-13;
+
+__global__ __launch_bounds__(256) void pivot_floor64(const double* __restrict__ A, int64_t n, int64_t ld,
+                                                     double* __restrict__ out) {
+    __shared__ double red[256];
+    double mx = 0.0;
+    for (int64_t i = threadIdx.x; i < n; i += 256) mx = fmax(mx, A[i * ld + i]);
+    red[threadIdx.x] = mx;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+        if ((int)threadIdx.x < w) red[threadIdx.x] = fmax(red[threadIdx.x], red[threadIdx.x + w]);
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) *out = kPivotTol * red[0];
+}
+
+// Unblocked Cholesky of the nb x nb (nb <= 64) block at A (row stride ld), in
+// place (lower triangle; the upper part is left as is).  One workgroup of 256
+// threads, block staged in LDS.  *info is set to 1 on a pivot that is not
+// finite or not above *floor (the matrix is not numerically positive definite).
+__global__ __launch_bounds__(256) void chol_diag(double* __restrict__ A, int64_t ld, int nb,
+                                                 const double* __restrict__ floor, int* __restrict__ info) {
+    __shared__ double L[kG64][kG64 + 1];
+    const int tid = threadIdx.x;
+    for (int e = tid; e < nb * nb; e += 256) L[e / nb][e % nb] = A[(int64_t)(e / nb) * ld + e % nb];
+    __syncthreads();
+    const double fl = *floor;
+    for (int j = 0; j < nb; ++j) {
+        const double d = L[j][j];
+        const bool ok = d > fl && d > 0.0 && __builtin_isfinite(d);
+        const double s = ok ? sqrt(d) : 1.0;
+        __syncthreads();
+        if (tid == 0) {
+            L[j][j] = s;
+            if (!ok) *info = 1;
+        }
+        for (int i = j + 1 + tid; i < nb; i += 256) L[i][j] /= s;
+        __syncthreads();
+        // trailing update of the lower triangle
+        const int w = nb - j - 1;
+        for (int e = tid; e < w * w; e += 256) {
+            const int i = j + 1 + e / w, c = j + 1 + e % w;
+            if (c <= i) L[i][c] -= L[i][j] * L[c][j];
+        }
+        __syncthreads();
+    }
+    for (int e = tid; e < nb * nb; e += 256) {
+        const int i = e / nb, c = e % nb;
+        if (c <= i) A[(int64_t)i * ld + c] = L[i][c];
+    }
+}
+
+// Panel of a blocked Cholesky: rows [0, nrows) of P (row stride ld, nb
+// columns) become P L11^-T, L11 being the nb x nb lower factor at Ld (row
+// stride ld).  One row per thread, 64 rows per workgroup.
+__global__ __launch_bounds__(64) void chol_panel(const double* __restrict__ Ld, double* __restrict__ P, int64_t ld,
+                                                 int nb, int64_t nrows) {
+    __shared__ double L[kG64][kG64 + 1];
+    for (int e = threadIdx.x; e < nb * nb; e += 64) L[e / nb][e % nb] = Ld[(int64_t)(e / nb) * ld + e % nb];
+    __syncthreads();
+    __shared__ double X[64][kG64 + 1];  // each thread's row, in LDS rather than scratch
+    const int64_t row = (int64_t)blockIdx.x * 64 + threadIdx.x;
+    if (row >= nrows) return;
+    double* x = X[threadIdx.x];
+    double* p = P + row * ld;
+    for (int j = 0; j < nb; ++j) {
+        double v = p[j];
+        for (int t = 0; t < j; ++t) v -= x[t] * L[j][t];
+        x[j] = v / L[j][j];
+    }
+    for (int j = 0; j < nb; ++j) p[j] = x[j];
+}
+
+// Triangular solve of one diagonal block for many right-hand sides: the nb
+// rows at B (row stride ldb, nrhs columns) become L11^-1 B (forward, TRANS =
+// 0) or L11^-T B (backward, TRANS = 1), L11 at Ld (row stride ld).  One
+// right-hand side per thread, 64 per workgroup.
+template <int TRANS>
+__global__ __launch_bounds__(64) void trsm_diag(const double* __restrict__ Ld, int64_t ld, int nb,
+                                                double* __restrict__ B, int64_t ldb, int64_t nrhs) {
+    __shared__ double L[kG64][kG64 + 1];
+    for (int e = threadIdx.x; e < nb * nb; e += 64) L[e / nb][e % nb] = Ld[(int64_t)(e / nb) * ld + e % nb];
+    __syncthreads();
+    __shared__ double X[64][kG64 + 1];  // each thread's right-hand side
+    const int64_t c = (int64_t)blockIdx.x * 64 + threadIdx.x;
+    if (c >= nrhs) return;
+    double* x = X[threadIdx.x];
+    for (int j = 0; j < nb; ++j) x[j] = B[(int64_t)j * ldb + c];
+    if (TRANS == 0) {
+        for (int j = 0; j < nb; ++j) {
+            double v = x[j];
+            for (int t = 0; t < j; ++t) v -= L[j][t] * x[t];
+            x[j] = v / L[j][j];
+        }
+    } else {
+        for (int j = nb - 1; j >= 0; --j) {
+            double v = x[j];
+            for (int t = j + 1; t < nb; ++t) v -= L[t][j] * x[t];
+            x[j] = v / L[j][j];
+        }
+    }
+    for (int j = 0; j < nb; ++j) B[(int64_t)j * ldb + c] = x[j];
+}
+
+// out = a * X + b * Y + d * I (n x n row-major; Y may be null, then b is ignored)
+__global__ void axpby_diag64(int64_t n, double a, const double* __restrict__ X, double b, const double* __restrict__ Y,
+                             double d, double* __restrict__ out) {
+    const int64_t total = n * n;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+        double v = a * X[e];
+        if (Y) v += b * Y[e];
+        if (e / n == e % n) v += d;
+        out[e] = v;
+    }
+}
+
+// out (cols x rows) = in^T (rows x cols), fp64, 32 x 32 LDS tiles.
+__global__ __launch_bounds__(256) void transpose64(const double* __restrict__ in, int64_t rows, int64_t cols,
+                                                   double* __restrict__ out) {
+    __shared__ double t[32][33];
+    const int64_t r0 = (int64_t)blockIdx.y * 32, c0 = (int64_t)blockIdx.x * 32;
+    const int tx = threadIdx.x % 32, ty = threadIdx.x / 32;
+    for (int k = ty; k < 32; k += 8) {
+        const int64_t r = r0 + k, c = c0 + tx;
+        t[k][tx] = (r < rows && c < cols) ? in[r * cols + c] : 0.0;
+    }
+    __syncthreads();
+    for (int k = ty; k < 32; k += 8) {
+        const int64_t c = c0 + k, r = r0 + tx;
+        if (c < cols && r < rows) out[c * rows + r] = t[tx][k];
+    }
+}
+
+// Epilogue for the MFMA GEMM: out[m * ld + n] += acc (the running fp64 sums
+// of the calibration statistics; fp32 products are accumulated in fp64).
+struct AccF64Epi {
+    double* out;
+    int64_t ld, N, M;
+    struct Col {
+        int64_t n;
+        bool ok;
+    };
+    __device__ __forceinline__ Col col(int64_t n) const { return Col{n, n < N}; }
+    __device__ __forceinline__ void store(int64_t m, const Col& c, float v) const {
+        if (m < M && c.ok) out[m * ld + c.n] += (double)v;
+    }
+};
+
+}  // namespace pifa

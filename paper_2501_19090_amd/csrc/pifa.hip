@@ -26,6 +26,7 @@
 #include "build.hpp"
 #include "gemv_skinny.hpp"
 #include "layout.hpp"
+#include "linalg64.hpp"
 #include "prepack.hpp"
 
 using namespace pifa;
@@ -98,6 +99,9 @@ enum Site {
     kSiteBwdDwp,
     kSiteBwdDc,
     kSiteBwdRows,
+    kSiteCalibGather,
+    kSiteCalibGram,
+    kSiteCalibSolve,
     kSiteCount
 };
 
@@ -107,7 +111,8 @@ const char* const kSiteNames[kSiteCount] = {
     "dense_f32",           "lowrank_gemm1_xv",    "lowrank_gemm2_tu",    "lowrank_gemv1_xv",
     "lowrank_gemv2_tu",    "lowrank_f32",         "pifa_group_gemm1",    "pifa_group_gemm2",
     "pifa_group_gemv1",    "pifa_group_gemv2",    "pifa_bwd_gather",     "pifa_bwd_gp",
-    "pifa_bwd_dx",         "pifa_bwd_dwp",        "pifa_bwd_dc",         "pifa_bwd_rows_f16"};
+    "pifa_bwd_dx",         "pifa_bwd_dwp",        "pifa_bwd_dc",         "pifa_bwd_rows_f16",
+    "pifa_calib_gather",   "pifa_calib_gram",     "pifa_calib_solve"};
 
 struct Profiler {
     std::mutex mu;
@@ -637,6 +642,7 @@ const char* pifa_status_string(pifa_status s) {
         case PIFA_ERR_HIP: return "PIFA_ERR_HIP";
         case PIFA_ERR_OOM: return "PIFA_ERR_OOM";
         case PIFA_ERR_NOT_RANK_R: return "PIFA_ERR_NOT_RANK_R";
+        case PIFA_ERR_NOT_SPD: return "PIFA_ERR_NOT_SPD";
     }
     return "PIFA_ERR_UNKNOWN";
 }
@@ -1193,6 +1199,239 @@ pifa_status pifa_layer_backward(pifa_handle h, const void* X, const void* Y, con
         if (e != hipSuccess) return PIFA_ERR_HIP;
     }
     return PIFA_OK;
+}
+
+}  // extern "C"
+
+extern "C" {
+
+}  // extern "C"
+
+// ===================================================================== reconstruction
+struct pifa_calib {
+    int device = 0;
+    int64_t n = 0;
+    double* S = nullptr;  // sum x_u x_u^T
+    double* P = nullptr;  // sum x_o x_u^T
+    int* info = nullptr;  // Cholesky status
+    GrowBuf ws;           // transposed batches and split partials
+    GrowBuf work;         // reconstruction operands
+};
+
+namespace {
+
+hipError_t gemm64_launch(hipStream_t st, int64_t Mr, int64_t Nc, int64_t K, double alpha, const double* A, int64_t sa0,
+                         int64_t sa1, const double* B, int64_t sb0, int64_t sb1, double beta, double* C, int64_t sc0,
+                         int64_t sc1, bool lower = false) {
+    if (Mr <= 0 || Nc <= 0) return hipSuccess;
+    hipLaunchKernelGGL(gemm64, dim3((unsigned)ceil_div(Nc, kG64), (unsigned)ceil_div(Mr, kG64)), dim3(256), 0, st, Mr,
+                       Nc, K, alpha, A, sa0, sa1, B, sb0, sb1, beta, C, sc0, sc1, lower ? 1 : 0);
+    return hipGetLastError();
+}
+
+// In-place lower Cholesky of the n x n matrix A (row stride ld); *info set on
+// failure.  floor: one device double of scratch for the pivot threshold.
+hipError_t cholesky64(double* A, int64_t n, int64_t ld, double* floor, int* info, hipStream_t st) {
+    hipLaunchKernelGGL(pivot_floor64, dim3(1), dim3(256), 0, st, (const double*)A, n, ld, floor);
+    for (int64_t kb = 0; kb < n; kb += kG64) {
+        const int nb = (int)std::min<int64_t>(kG64, n - kb);
+        double* Akk = A + kb * ld + kb;
+        hipLaunchKernelGGL(chol_diag, dim3(1), dim3(256), 0, st, Akk, ld, nb, (const double*)floor, info);
+        const int64_t rest = n - kb - nb;
+        if (rest > 0) {
+            double* L21 = A + (kb + nb) * ld + kb;
+            hipLaunchKernelGGL(chol_panel, dim3((unsigned)ceil_div(rest, (int64_t)64)), dim3(64), 0, st, Akk, L21, ld,
+                               nb, rest);
+            hipError_t e = gemm64_launch(st, rest, rest, nb, -1.0, L21, ld, 1, L21, 1, ld, 1.0,
+                                         A + (kb + nb) * ld + kb + nb, ld, 1, true);
+            if (e != hipSuccess) return e;
+        }
+    }
+    return hipGetLastError();
+}
+
+// B (n x nrhs, row stride ldb) <- (L L^T)^-1 B for the lower factor L (row stride ld).
+hipError_t spd_solve64(const double* L, int64_t n, int64_t ld, double* B, int64_t nrhs, int64_t ldb, hipStream_t st) {
+    const unsigned g = (unsigned)ceil_div(nrhs, (int64_t)64);
+    for (int64_t kb = 0; kb < n; kb += kG64) {  // L Y = B
+        const int nb = (int)std::min<int64_t>(kG64, n - kb);
+        hipLaunchKernelGGL((trsm_diag<0>), dim3(g), dim3(64), 0, st, L + kb * ld + kb, ld, nb, B + kb * ldb, ldb, nrhs);
+        const int64_t rest = n - kb - nb;
+        hipError_t e = gemm64_launch(st, rest, nrhs, nb, -1.0, L + (kb + nb) * ld + kb, ld, 1, B + kb * ldb, ldb, 1,
+                                     1.0, B + (kb + nb) * ldb, ldb, 1);
+        if (e != hipSuccess) return e;
+    }
+    for (int64_t kb = ((n - 1) / kG64) * kG64; kb >= 0; kb -= kG64) {  // L^T X = Y
+        const int nb = (int)std::min<int64_t>(kG64, n - kb);
+        hipLaunchKernelGGL((trsm_diag<1>), dim3(g), dim3(64), 0, st, L + kb * ld + kb, ld, nb, B + kb * ldb, ldb, nrhs);
+        hipError_t e = gemm64_launch(st, kb, nrhs, nb, -1.0, L + kb * ld, 1, ld, B + kb * ldb, ldb, 1, 1.0, B, ldb, 1);
+        if (e != hipSuccess) return e;
+    }
+    return hipGetLastError();
+}
+
+hipError_t transpose64_launch(const double* in, int64_t rows, int64_t cols, double* out, hipStream_t st) {
+    if (rows == 0 || cols == 0) return hipSuccess;
+    hipLaunchKernelGGL(transpose64, dim3((unsigned)ceil_div(cols, (int64_t)32), (unsigned)ceil_div(rows, (int64_t)32)),
+                       dim3(256), 0, st, in, rows, cols, out);
+    return hipGetLastError();
+}
+
+void free_calib(pifa_calib* c) {
+    if (!c) return;
+    if (c->S) (void)hipFree(c->S);
+    if (c->P) (void)hipFree(c->P);
+    if (c->info) (void)hipFree(c->info);
+    c->ws.release();
+    c->work.release();
+    delete c;
+}
+
+}  // namespace
+
+extern "C" {
+
+pifa_status pifa_calib_create(int64_t d_in, pifa_calib_handle* out) {
+    if (!out) return PIFA_ERR_INVALID_ARG;
+    *out = nullptr;
+    if (d_in < 1) return PIFA_ERR_INVALID_ARG;
+    if (d_in > 65536) return PIFA_ERR_UNSUPPORTED;
+    pifa_calib* c = new (std::nothrow) pifa_calib();
+    if (!c) return PIFA_ERR_OOM;
+    c->n = d_in;
+    const size_t b = (size_t)d_in * d_in * sizeof(double);
+    if (hipGetDevice(&c->device) != hipSuccess) { free_calib(c); return PIFA_ERR_HIP; }
+    if (hipMalloc(&c->S, b) != hipSuccess || hipMalloc(&c->P, b) != hipSuccess ||
+        hipMalloc(&c->info, sizeof(int)) != hipSuccess) {
+        free_calib(c);
+        return PIFA_ERR_OOM;
+    }
+    if (hipMemset(c->S, 0, b) != hipSuccess || hipMemset(c->P, 0, b) != hipSuccess ||
+        hipDeviceSynchronize() != hipSuccess) {
+        free_calib(c);
+        return PIFA_ERR_HIP;
+    }
+    *out = c;
+    return PIFA_OK;
+}
+
+pifa_status pifa_calib_destroy(pifa_calib_handle c) {
+    if (!c) return PIFA_OK;
+    (void)hipDeviceSynchronize();
+    free_calib(c);
+    return PIFA_OK;
+}
+
+pifa_status pifa_calib_reset(pifa_calib_handle c, void* stream) {
+    if (!c) return PIFA_ERR_INVALID_ARG;
+    const size_t b = (size_t)c->n * c->n * sizeof(double);
+    PIFA_HIP(hipMemsetAsync(c->S, 0, b, as_stream(stream)));
+    PIFA_HIP(hipMemsetAsync(c->P, 0, b, as_stream(stream)));
+    return PIFA_OK;
+}
+
+pifa_status pifa_calib_accumulate(pifa_calib_handle c, const void* X_o, const void* X_u, int64_t B, void* stream) {
+    if (!c || B < 0) return PIFA_ERR_INVALID_ARG;
+    if (B == 0) return PIFA_OK;
+    if (!X_o || !X_u) return PIFA_ERR_INVALID_ARG;
+    hipStream_t st = as_stream(stream);
+    const int64_t n = c->n, Bp = round_up(B, (int64_t)8);
+    const int64_t e_t = align_elems(n * Bp);
+    const size_t part = split_bytes(n, n, Bp);
+    pifa_status s = c->ws.ensure((size_t)(2 * e_t) * 2 + part, st);
+    if (s != PIFA_OK) return s;
+    bf16* xut = (bf16*)c->ws.ptr;
+    bf16* xot = xut + e_t;
+    float* partials = part ? (float*)((char*)c->ws.ptr + (size_t)(2 * e_t) * 2) : nullptr;
+    {
+        TimedLaunch timed(kSiteCalibGather, st);
+        if (launch_gather((const bf16*)X_u, n, B, nullptr, n, nullptr, 0, xut, Bp, st) != hipSuccess) return PIFA_ERR_HIP;
+        if (X_o != X_u &&
+            launch_gather((const bf16*)X_o, n, B, nullptr, n, nullptr, 0, xot, Bp, st) != hipSuccess)
+            return PIFA_ERR_HIP;
+    }
+    const bf16* xo = X_o == X_u ? xut : xot;
+    // S += X_u^T X_u and P += X_o^T X_u: rows of the transposed batches, K = tokens
+    if (launch_gemm<bf16, false>(kSiteCalibGram, xut, Bp, n, xut, Bp, n, Bp, AccF64Epi{c->S, n, n, n}, partials, st) !=
+        hipSuccess)
+        return PIFA_ERR_HIP;
+    if (launch_gemm<bf16, false>(kSiteCalibGram, xo, Bp, n, xut, Bp, n, Bp, AccF64Epi{c->P, n, n, n}, partials, st) !=
+        hipSuccess)
+        return PIFA_ERR_HIP;
+    return PIFA_OK;
+}
+
+pifa_status pifa_calib_read(pifa_calib_handle c, double* S, double* P, void* stream) {
+    if (!c) return PIFA_ERR_INVALID_ARG;
+    const size_t b = (size_t)c->n * c->n * sizeof(double);
+    if (S) PIFA_HIP(hipMemcpyAsync(S, c->S, b, hipMemcpyDeviceToDevice, as_stream(stream)));
+    if (P) PIFA_HIP(hipMemcpyAsync(P, c->P, b, hipMemcpyDeviceToDevice, as_stream(stream)));
+    return PIFA_OK;
+}
+
+pifa_status pifa_calib_reconstruct(pifa_calib_handle c, const double* W, int64_t d_out, const double* Vt, int64_t r,
+                                   double lam, double alpha, double* U_r, double* Vt_r, void* stream) {
+    if (!c || !W || !Vt || !U_r || !Vt_r || d_out < 1 || r < 1) return PIFA_ERR_INVALID_ARG;
+    const int64_t n = c->n, m = d_out;
+    if (r > n || r > m) return PIFA_ERR_INVALID_ARG;
+    hipStream_t st = as_stream(stream);
+    // work regions (fp64 elements, 32-element aligned)
+    auto al = [](int64_t e) { return round_up(e, (int64_t)32); };
+    const int64_t e_Z = al(n * n), e_T = al(m * n), e_SV = al(n * r), e_A = al(r * r), e_Bt = al(r * m),
+                  e_G = al(r * r), e_H = al(r * n), e_QT = al(n * r), e_Sa = al(n * n);
+    pifa_status s = c->work.ensure((size_t)(e_Z + e_T + e_SV + e_A + e_Bt + e_G + e_H + e_QT + e_Sa + 32) * 8, st);
+    if (s != PIFA_OK) return s;
+    double* Z = (double*)c->work.ptr;
+    double* T = Z + e_Z;
+    double* SV = T + e_T;
+    double* Ar = SV + e_SV;
+    double* Ut = Ar + e_A;  // (T V)^T, then U_r^T (r x m)
+    double* G = Ut + e_Bt;
+    double* H = G + e_G;    // U_r^T (T + a W), then Q = G^-1 H (r x n)
+    double* QT = H + e_H;   // Q^T, then V_r (n x r)
+    double* Sa = QT + e_QT; // S + a I, then its factor
+    double* floor = Sa + e_Sa;
+    TimedLaunch timed(kSiteCalibSolve, st);
+    hipError_t e;
+#define PIFA_GO(call)                              \
+    do {                                           \
+        if ((e = (call)) != hipSuccess) return PIFA_ERR_HIP; \
+    } while (0)
+    PIFA_HIP(hipMemsetAsync(c->info, 0, sizeof(int), st));
+    // T = W (lam P + (1 - lam) S)
+    hipLaunchKernelGGL(axpby_diag64, dim3(grid_for(n * n)), dim3(256), 0, st, n, lam, (const double*)c->P, 1.0 - lam,
+                       (const double*)c->S, 0.0, Z);
+    PIFA_GO(hipGetLastError());
+    PIFA_GO(gemm64_launch(st, m, n, n, 1.0, W, n, 1, Z, n, 1, 0.0, T, n, 1));
+    // A_r = V^T S V with V = Vt^T;  (T V)^T
+    PIFA_GO(gemm64_launch(st, n, r, n, 1.0, c->S, n, 1, Vt, 1, n, 0.0, SV, r, 1));
+    PIFA_GO(gemm64_launch(st, r, r, n, 1.0, Vt, n, 1, SV, r, 1, 0.0, Ar, r, 1));
+    PIFA_GO(gemm64_launch(st, r, m, n, 1.0, Vt, n, 1, T, 1, n, 0.0, Ut, m, 1));
+    // U_r^T = A_r^-1 (T V)^T   (A_r symmetric)
+    PIFA_GO(cholesky64(Ar, r, r, floor, c->info, st));
+    PIFA_GO(spd_solve64(Ar, r, r, Ut, m, m, st));
+    // G = U_r^T U_r;  H = U_r^T (T + a W)
+    PIFA_GO(gemm64_launch(st, r, r, m, 1.0, Ut, m, 1, Ut, 1, m, 0.0, G, r, 1));
+    PIFA_GO(gemm64_launch(st, r, n, m, 1.0, Ut, m, 1, T, n, 1, 0.0, H, n, 1));
+    PIFA_GO(gemm64_launch(st, r, n, m, alpha, Ut, m, 1, W, n, 1, 1.0, H, n, 1));
+    // Q = G^-1 H
+    PIFA_GO(cholesky64(G, r, r, floor, c->info, st));
+    PIFA_GO(spd_solve64(G, r, r, H, n, n, st));
+    // V_r = (S + a I)^-1 Q^T  (n x r), i.e. V_r^T = Q (S + a I)^-1
+    hipLaunchKernelGGL(axpby_diag64, dim3(grid_for(n * n)), dim3(256), 0, st, n, 1.0, (const double*)c->S, 0.0,
+                       (const double*)nullptr, alpha, Sa);
+    PIFA_GO(hipGetLastError());
+    PIFA_GO(transpose64_launch(H, r, n, QT, st));
+    PIFA_GO(cholesky64(Sa, n, n, floor, c->info, st));
+    PIFA_GO(spd_solve64(Sa, n, n, QT, r, r, st));
+    // outputs
+    PIFA_GO(transpose64_launch(Ut, r, m, U_r, st));
+    PIFA_GO(transpose64_launch(QT, n, r, Vt_r, st));
+#undef PIFA_GO
+    int info = 0;
+    PIFA_HIP(hipMemcpyAsync(&info, c->info, sizeof(int), hipMemcpyDeviceToHost, st));
+    PIFA_HIP(hipStreamSynchronize(st));
+    return info ? PIFA_ERR_NOT_SPD : PIFA_OK;
 }
 
 }  // extern "C"

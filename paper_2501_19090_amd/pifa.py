@@ -28,6 +28,7 @@ PIFA_ERR_UNSUPPORTED = -3
 PIFA_ERR_HIP = -4
 PIFA_ERR_OOM = -5
 PIFA_ERR_NOT_RANK_R = -6
+PIFA_ERR_NOT_SPD = -7
 
 
 class pifa_dims(ctypes.Structure):
@@ -78,6 +79,12 @@ _SIGNATURES = {
     "pifa_group_weight_bytes": (ctypes.c_size_t, [_vp]),
     "pifa_group_set_intermediate_scale": (_st, [_vp, ctypes.c_int]),
     "pifa_group_overflow_count": (_st, [_vp, ctypes.POINTER(_i64)]),
+    "pifa_calib_create": (_st, [_i64, ctypes.POINTER(_vp)]),
+    "pifa_calib_destroy": (_st, [_vp]),
+    "pifa_calib_reset": (_st, [_vp, _vp]),
+    "pifa_calib_accumulate": (_st, [_vp, _vp, _vp, _i64, _vp]),
+    "pifa_calib_read": (_st, [_vp, _vp, _vp, _vp]),
+    "pifa_calib_reconstruct": (_st, [_vp, _vp, _i64, _vp, _i64, ctypes.c_double, ctypes.c_double, _vp, _vp, _vp]),
     "pifa_build_f64": (_st, [_vp, pifa_dims, _vp, _vp, _i32p, _i32p, ctypes.POINTER(ctypes.c_double), _vp]),
     "pifa_profile_enable": (_st, [ctypes.c_int]),
     "pifa_profile_reset": (_st, []),
@@ -331,6 +338,45 @@ def pifa_group_overflow_count(handle: int) -> int:
     out = _i64()
     _check("pifa_group_overflow_count", lib().pifa_group_overflow_count(handle, ctypes.byref(out)))
     return int(out.value)
+
+
+def pifa_calib_create(d_in: int) -> int:
+    out = _vp()
+    _check("pifa_calib_create", lib().pifa_calib_create(int(d_in), ctypes.byref(out)))
+    return out.value
+
+
+def pifa_calib_destroy(handle: int) -> None:
+    _check("pifa_calib_destroy", lib().pifa_calib_destroy(handle))
+
+
+def pifa_calib_reset(handle: int, stream=None) -> None:
+    _check("pifa_calib_reset", lib().pifa_calib_reset(handle, _stream(stream)))
+
+
+def pifa_calib_accumulate(handle: int, X_o, X_u, B: int | None = None, stream=None) -> None:
+    B = X_u.shape[0] if B is None else int(B)
+    _check("pifa_calib_accumulate", lib().pifa_calib_accumulate(handle, _dev_ptr(X_o, "X_o"), _dev_ptr(X_u, "X_u"),
+                                                                B, _stream(stream)))
+
+
+def pifa_calib_read(handle: int, S=None, P=None, stream=None) -> None:
+    _check("pifa_calib_read", lib().pifa_calib_read(handle, _dev_ptr(S, "S"), _dev_ptr(P, "P"), _stream(stream)))
+
+
+def pifa_calib_reconstruct(handle: int, W, Vt, lam: float, alpha: float, U_r=None, Vt_r=None, stream=None):
+    """Returns (U_r, Vt_r) as device fp64 tensors (allocated when not given)."""
+    import torch
+    d_out, d_in = W.shape
+    r = Vt.shape[0]
+    if U_r is None:
+        U_r = torch.empty((d_out, r), dtype=torch.float64, device=W.device)
+    if Vt_r is None:
+        Vt_r = torch.empty((r, d_in), dtype=torch.float64, device=W.device)
+    _check("pifa_calib_reconstruct", lib().pifa_calib_reconstruct(
+        handle, _dev_ptr(W, "W"), int(d_out), _dev_ptr(Vt, "Vt"), int(r), float(lam), float(alpha),
+        _dev_ptr(U_r, "U_r"), _dev_ptr(Vt_r, "Vt_r"), _stream(stream)))
+    return U_r, Vt_r
 
 
 def pifa_build_f64(W, r: int, stream=None):

@@ -1,0 +1,112 @@
+"""Online reconstruction on the GPU (pifa_calib_*) against the oracle.
+
+The calibration sums S = sum x_u x_u^T and P = sum x_o x_u^T are fp64 sums of
+per-batch fp32 MFMA products of bf16 rows; against the oracle's fp64 sums of
+the same bits they agree to rel 1e-6 (fp32 accumulation over one batch,
+about sqrt(B) 2^-24).  U_r and V_r^T inherit that error times the condition
+of the systems (below 10 for the Gaussian calibration sets here): bar 1e-4.
+"""
+import numpy as np
+import pytest
+
+from oracle import reconstruct as rec
+from paper_2501_19090_amd import inputs
+
+from gpu_util import rel_fro, to_dev, torch_mod
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _cuda():
+    if not torch_mod().cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _calib_set(n, b, seed, same_flow=False):
+    xu_st, xu = inputs.round_to(inputs.activations(b, n, seed), "bf16")
+    if same_flow:
+        return xu_st, xu, xu_st, xu
+    xo64 = xu + 0.1 * inputs.activations(b, n, seed + 1)
+    xo_st, xo = inputs.round_to(xo64, "bf16")
+    return xo_st, xo, xu_st, xu
+
+
+def _gpu_run(n, W, Vt, xo_st, xu_st, batches, lam, alpha):
+    from paper_2501_19090_amd import pifa
+    torch = torch_mod()
+    h = pifa.pifa_calib_create(n)
+    try:
+        for a, b in zip(np.array_split(np.arange(xu_st.shape[0]), batches), [None] * batches):
+            pifa.pifa_calib_accumulate(h, to_dev(xo_st[a]), to_dev(xu_st[a]))
+        S = torch.empty((n, n), dtype=torch.float64, device="cuda:0")
+        P = torch.empty_like(S)
+        pifa.pifa_calib_read(h, S, P)
+        Wd = torch.from_numpy(W).cuda()
+        Vd = torch.from_numpy(np.ascontiguousarray(Vt)).cuda()
+        U_r, Vt_r = pifa.pifa_calib_reconstruct(h, Wd, Vd, lam, alpha)
+        torch.cuda.synchronize()
+        return S.cpu().numpy(), P.cpu().numpy(), U_r.cpu().numpy(), Vt_r.cpu().numpy()
+    finally:
+        pifa.pifa_calib_destroy(h)
+
+
+@pytest.mark.parametrize("n,m,r,b,batches", [(256, 320, 64, 1500, 3), (136, 96, 40, 701, 2), (512, 1024, 200, 2048, 4)])
+def test_reconstruct_matches_oracle(n, m, r, b, batches):
+    rng = np.random.default_rng(n + m)
+    W = rng.standard_normal((m, n)) / np.sqrt(n)
+    Vt = rng.standard_normal((r, n)) / np.sqrt(n)
+    xo_st, xo, xu_st, xu = _calib_set(n, b, seed=n)
+    lam, alpha = 0.25, 1e-3
+    S, P, U_r, Vt_r = _gpu_run(n, W, Vt, xo_st, xu_st, batches, lam, alpha)
+    assert rel_fro(S, xu.T @ xu) <= 1e-6
+    assert rel_fro(P, xo.T @ xu) <= 1e-6
+    acc = rec.OnlineAccumulator(W, lam)
+    acc.add(xo, xu)
+    U_o, Vt_o = rec.reconstruct(acc.S, acc.T, W, Vt, alpha)
+    assert rel_fro(U_r, U_o) <= 1e-4
+    assert rel_fro(Vt_r, Vt_o) <= 1e-4
+
+
+def test_rank_r_weight_recovered():
+    """One data flow and a rank-r W: U_r V_r^T reproduces W."""
+    n, m, r = 256, 192, 32
+    rng = np.random.default_rng(5)
+    W = (rng.standard_normal((m, r)) @ rng.standard_normal((r, n))) / n
+    Vt = rng.standard_normal((r, n)) / np.sqrt(n)
+    xo_st, _, xu_st, _ = _calib_set(n, 900, seed=7, same_flow=True)
+    _, _, U_r, Vt_r = _gpu_run(n, W, Vt, xu_st, xu_st, 2, 0.25, 1e-3)
+    assert rel_fro(U_r @ Vt_r, W) <= 1e-8
+
+
+def test_singular_gram_is_reported():
+    """A V with two equal rows makes V^T S V singular: PIFA_ERR_NOT_SPD."""
+    from paper_2501_19090_amd import pifa
+    n, m, r = 128, 96, 16
+    rng = np.random.default_rng(8)
+    W = rng.standard_normal((m, n)) / np.sqrt(n)
+    Vt = rng.standard_normal((r, n)) / np.sqrt(n)
+    Vt[3] = Vt[7]
+    _, _, xu_st, _ = _calib_set(n, 600, seed=9)
+    with pytest.raises(pifa.PifaError) as e:
+        _gpu_run(n, W, Vt, xu_st, xu_st, 1, 0.25, 1e-3)
+    assert e.value.status == pifa.PIFA_ERR_NOT_SPD
+
+
+def test_full_size_attention_layer():
+    """d_in = d_out = 4096, r = 2048 (the LLaMA-7B attention shape) with
+    8192 calibration rows in 4 batches of 2048 tokens."""
+    n, m, r, b = 4096, 4096, 2048, 8192
+    rng = np.random.default_rng(11)
+    W = rng.standard_normal((m, n)) / np.sqrt(n)
+    Vt = rng.standard_normal((r, n)) / np.sqrt(n)
+    xo_st, xo, xu_st, xu = _calib_set(n, b, seed=12)
+    lam, alpha = 0.25, 1e-3
+    S, P, U_r, Vt_r = _gpu_run(n, W, Vt, xo_st, xu_st, 4, lam, alpha)
+    S_o = xu.T @ xu
+    assert rel_fro(S, S_o) <= 1e-6
+    assert rel_fro(P, xo.T @ xu) <= 1e-6
+    T_o = W @ (lam * (xo.T @ xu) + (1 - lam) * S_o)
+    U_o, Vt_o = rec.reconstruct(S_o, T_o, W, Vt, alpha)
+    assert rel_fro(U_r, U_o) <= 1e-4
+    assert rel_fro(Vt_r, Vt_o) <= 1e-4
