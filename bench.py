@@ -14,7 +14,8 @@ weights rotated through more than the 256 MB Infinity Cache), the same-engine
 low-rank U V and dense baselines, the dominant kernel's roofline (timed live
 with HIP events on its launch stream), the fp64 oracle timed on the host, and
 the grouped case (the MLP gate and up projections sharing X, as one group
-against two separate layers) and the backward pass at the headline size.
+against two separate layers), the backward pass at the headline size, and the
+online reconstruction of Sec. 4 (calibration sums and closed-form solves).
 
 The layers are synthetic: Gaussian low-rank W' = U V (seeded), turned into
 PIFA form on the GPU by pifa_build_f64 (QR with column pivoting, timed and
@@ -322,6 +323,53 @@ def measure_backward(wl: Workload, M: int, iters: int = 10, warmup: int = 3):
             "kernels": {k: {"launches": n, "avg_us": 1e3 * v / n} for k, (n, v) in kern.items()}}
 
 
+def measure_reconstruct(n=4096, m=4096, r=2048, batch=2048, batches=8):
+    """Online reconstruction (Sec. 4) at the LLaMA-7B attention shape: the
+    calibration sums over `batches` batches of `batch` tokens (two n x n
+    products per batch with K = batch), then the closed-form U and V updates."""
+    import torch
+    from paper_2501_19090_amd import inputs, pifa
+    # distinct tokens in every batch: more calibration rows than d_in, as the
+    # sums must be positive definite (the paper uses 512 x 2048 tokens)
+    dev = lambda a: torch.from_numpy(inputs.round_bf16(a)[0].view(np.int16)).cuda().view(torch.bfloat16)
+    xus = [dev(inputs.activations(batch, n, 41 + 2 * i)) for i in range(batches)]
+    xos = [dev(inputs.activations(batch, n, 42 + 2 * i)) for i in range(batches)]
+    g = torch.Generator(device="cuda:0")
+    g.manual_seed(43)
+    W = torch.randn((m, n), dtype=torch.float64, device="cuda:0", generator=g) / math.sqrt(n)
+    Vt = torch.randn((r, n), dtype=torch.float64, device="cuda:0", generator=g) / math.sqrt(n)
+    h = pifa.pifa_calib_create(n)
+    try:
+        pifa.pifa_calib_accumulate(h, xos[0], xus[0])  # workspace
+        pifa.pifa_calib_reset(h)
+        torch.cuda.synchronize()
+        pifa.pifa_profile_reset()
+        pifa.pifa_profile_enable(True)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for xo, xu in zip(xos, xus):
+            pifa.pifa_calib_accumulate(h, xo, xu)
+        e1.record()
+        torch.cuda.synchronize()
+        t_acc = e0.elapsed_time(e1) / batches
+        pifa.pifa_profile_enable(False)
+        kern = pifa.pifa_profile_read()
+        pifa.pifa_profile_reset()
+        t0 = time.perf_counter()
+        pifa.pifa_calib_reconstruct(h, W, Vt, 0.25, 1e-3)
+        torch.cuda.synchronize()
+        t_solve = time.perf_counter() - t0
+    finally:
+        pifa.pifa_calib_destroy(h)
+    flops = 2 * 2.0 * n * n * batch
+    return {"workload": "calibration sums S, P for d_in=%d from batches of %d bf16 tokens; "
+                        "reconstruction to d_out=%d, r=%d in fp64" % (n, batch, m, r),
+            "accumulate_us_per_batch": 1e3 * t_acc, "tokens_per_s": batch / (t_acc * 1e-3),
+            "gram_tflops": flops / (t_acc * 1e9),
+            "solve_ms": 1e3 * t_solve,
+            "kernels": {k: {"launches": c, "avg_us": 1e3 * v / c} for k, (c, v) in kern.items()}}
+
+
 def cpu_baseline(wl, M_full, budget_s=10.0):
     """The fp64 oracle's PIFA forward on a bounded row sample of the workload
     (the same bf16 layer the GPU runs)."""
@@ -458,6 +506,8 @@ def main():
         log("cpu baseline:", json.dumps(cpu))
     backward = measure_backward(wl, M)
     log("backward:", json.dumps(backward))
+    reconstruct = measure_reconstruct()
+    log("reconstruct:", json.dumps(reconstruct))
     grouped = measure_group(inputs.config_seed(2))
     log("grouped:", json.dumps(grouped))
     build = {"ms": wl.build_ms, "report": wl.build_report,
@@ -483,6 +533,7 @@ def main():
         "build": build,
         "grouped": grouped,
         "backward": backward,
+        "reconstruct": reconstruct,
         "kernels": kernels,
         "paper_context": "arXiv 2501.19090 reports, on an NVIDIA RTX A6000 (d=8192, 65,536 rows), "
                          "24.2% memory saving and 24.6% lower time than the low-rank layer at r=d/2",
