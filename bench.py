@@ -129,6 +129,22 @@ class Workload:
         self.pifa_h, self.uv_h, self.dense_h = [], [], []
 
 
+def profiled(fn):
+    """Run fn with the library's per-launch HIP-event timing on; returns
+    {site: (launches, total ms)}.  Kept out of the timed runs, since the
+    events add about 10% to a step."""
+    from paper_2501_19090_amd import pifa
+    pifa.pifa_profile_reset()
+    pifa.pifa_profile_enable(True)
+    try:
+        fn()
+    finally:
+        pifa.pifa_profile_enable(False)
+    kern = pifa.pifa_profile_read()
+    pifa.pifa_profile_reset()
+    return kern
+
+
 def time_rotating(calls, iters, warmup):
     """Average ms per call, calls taken round-robin; torch events on the
     current stream (the stream every call launches on)."""
@@ -192,12 +208,8 @@ def measure(wl: Workload, M: int, iters: int, warmup: int, rotate: bool):
     p_calls = [lambda h=h: pifa.pifa_forward(h, x, y, M) for h in ph]
     u_calls = [lambda h=h: pifa.lowrank_layer_forward(h, x, y, M) for h in uh]
     d_calls = [lambda h=h: pifa.dense_layer_forward(h, x, y, M) for h in dh]
-    pifa.pifa_profile_reset()
-    pifa.pifa_profile_enable(True)
     t_eager = time_rotating(p_calls, iters, warmup)
-    pifa.pifa_profile_enable(False)
-    kern = pifa.pifa_profile_read()
-    pifa.pifa_profile_reset()
+    kern = profiled(lambda: time_rotating(p_calls, iters, 0))
     if rotate:
         per_graph = max(iters, 2 * len(ph))
         t_pifa = time_graph(p_calls, per_graph, 5)
@@ -312,12 +324,8 @@ def measure_backward(wl: Workload, M: int, iters: int = 10, warmup: int = 3):
     call = lambda: pifa.pifa_layer_backward(h, x, y, g, dx, dwp, dc, M)
     call()  # builds the transposed weight copies and the workspace
     torch.cuda.synchronize()
-    pifa.pifa_profile_reset()
-    pifa.pifa_profile_enable(True)
     t = time_rotating([call], iters, warmup)
-    pifa.pifa_profile_enable(False)
-    kern = pifa.pifa_profile_read()
-    pifa.pifa_profile_reset()
+    kern = profiled(lambda: time_rotating([call], iters, 0))
     flops = 2 * pifa_flops(M, wl.d_in, wl.d_out, wl.r)
     return {"M": M, "us": 1e3 * t, "tflops": flops / (t * 1e9), "useful_flops": flops,
             "kernels": {k: {"launches": n, "avg_us": 1e3 * v / n} for k, (n, v) in kern.items()}}
@@ -343,18 +351,21 @@ def measure_reconstruct(n=4096, m=4096, r=2048, batch=2048, batches=8):
         pifa.pifa_calib_accumulate(h, xos[0], xus[0])  # workspace
         pifa.pifa_calib_reset(h)
         torch.cuda.synchronize()
-        pifa.pifa_profile_reset()
-        pifa.pifa_profile_enable(True)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
+
+        def sweep_batches():
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for xo, xu in zip(xos, xus):
+                pifa.pifa_calib_accumulate(h, xo, xu)
+            e1.record()
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) / batches
+
+        t_acc = sweep_batches()
+        kern = profiled(sweep_batches)
+        pifa.pifa_calib_reset(h)
         for xo, xu in zip(xos, xus):
             pifa.pifa_calib_accumulate(h, xo, xu)
-        e1.record()
-        torch.cuda.synchronize()
-        t_acc = e0.elapsed_time(e1) / batches
-        pifa.pifa_profile_enable(False)
-        kern = pifa.pifa_profile_read()
-        pifa.pifa_profile_reset()
         t0 = time.perf_counter()
         pifa.pifa_calib_reconstruct(h, W, Vt, 0.25, 1e-3)
         torch.cuda.synchronize()
@@ -417,7 +428,7 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--full", action="store_true", help="also sweep every configuration")
     ap.add_argument("--out", default=os.path.join(ROOT, "gpurun_out", "bench_full.json"))
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
@@ -459,25 +470,34 @@ def main():
         log("profile run done")
         return
 
-    # ---- headline: K timed steps of the M = 4096 forward
+    # ---- headline: K timed steps of the M = 4096 forward (no per-launch
+    # events inside: they add about 10% to a step)
     for _ in range(args.warmup):
         pifa.pifa_forward(h, x, y, M, stream)
     torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for _ in range(args.steps):
+        pifa.pifa_forward(h, x, y, M, stream)
+    ev1.record()
+    torch.cuda.synchronize()
+    ms_step = ev0.elapsed_time(ev1) / args.steps
+    value = pifa_flops(M, d_in, d_out, r) / (ms_step * 1e9)
+    # ---- the same K steps again with each launch bracketed by HIP events on
+    # its stream: per-kernel durations for the roofline
     pifa.pifa_profile_reset()
     pifa.pifa_profile_enable(True)
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
     ev0.record()
     for _ in range(args.steps):
         pifa.pifa_forward(h, x, y, M, stream)
     ev1.record()
     torch.cuda.synchronize()
     pifa.pifa_profile_enable(False)
-    ms_step = ev0.elapsed_time(ev1) / args.steps
+    ms_step_instrumented = ev0.elapsed_time(ev1) / args.steps
     kern = pifa.pifa_profile_read()
     pifa.pifa_profile_reset()
-    value = pifa_flops(M, d_in, d_out, r) / (ms_step * 1e9)
-    log("prefill M=%d: %.1f us/step, %.1f TFLOP/s; kernels %s" % (M, 1e3 * ms_step, value, kern))
+    log("prefill M=%d: %.1f us/step (%.1f with per-launch events), %.1f TFLOP/s; kernels %s"
+        % (M, 1e3 * ms_step, 1e3 * ms_step_instrumented, value, kern))
 
     g1_n, g1_ms = kern["pifa_gemm1_xwp"]
     g1_us = 1e3 * g1_ms / g1_n
@@ -486,11 +506,13 @@ def main():
     traffic = traffic_from_profiles("pifa_gemm1_xwp")
     roofline = {"bound": "mfma", "kernel": "pifa_gemm1_xwp (X W_p^T, bf16 MFMA)", "achieved": achieved,
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
-                "traffic": traffic, "avg_us": g1_us, "algorithmic_flops_per_launch": g1_flops}
+                "traffic": traffic, "avg_us": g1_us, "algorithmic_flops_per_launch": g1_flops,
+                "timing": "HIP events around every launch on its stream, over K instrumented steps run "
+                          "right after the K timed steps (%.1f us/step with the events)" % (1e3 * ms_step_instrumented)}
     kernels = {k: {"launches": n, "avg_us": 1e3 * v / n} for k, (n, v) in kern.items()}
 
     # ---- baselines at the headline M, and the decode case
-    pre = measure(wl, M, max(10, args.steps // 2), 5, rotate=False)
+    pre = measure(wl, M, args.steps, 100, rotate=False)
     log("prefill baselines:", json.dumps(pre))
     dec = measure(wl, 1, 200, 20, rotate=True)
     log("decode:", json.dumps(dec))

@@ -111,7 +111,7 @@ __device__ __forceinline__ void gemm_nt_tile(const T* __restrict__ A, int64_t ld
     static_assert(BM * CPR % NT == 0 && BN * CPR % NT == 0, "tile does not split over threads");
     static_assert(WTM % 32 == 0 && WTN % 32 == 0 && KK >= 2, "bad warp tile");
     static_assert(!BPACK || ((BK == 64 || BK == 128) && BN % kPackRows == 0), "bad packed tile");
-    static_assert(PGR == 1 || PGR == 2, "prefetch depth");
+    static_assert(PGR >= 1 && PGR <= 4, "prefetch depth");
 
     __shared__ __attribute__((aligned(16))) T As[2][BM * LDK];
     __shared__ __attribute__((aligned(16))) T Bs[2][BN * LDK];
@@ -199,8 +199,8 @@ __device__ __forceinline__ void gemm_nt_tile(const T* __restrict__ A, int64_t ld
     // the last iterations touch a buffer nobody reads again.  A branch here
     // would make the compiler wait for every outstanding load at the join,
     // which serialises the prefetch.
-    gload(kbeg, S[0]);
-    if (PGR == 2) gload(kbeg + BK, S[PGR - 1]);
+#pragma unroll
+    for (int p = 0; p < PGR; ++p) gload(kbeg + (int64_t)p * BK, S[p]);
     sstore(0, S[0]);
     gload(kbeg + (int64_t)PGR * BK, S[0]);
     __syncthreads();
@@ -209,7 +209,7 @@ __device__ __forceinline__ void gemm_nt_tile(const T* __restrict__ A, int64_t ld
     // (after every wave has read its last fragments of this tile and written
     // the next one), so the next tile's first fragments are read while the
     // last MFMA step runs instead of after the barrier.
-    constexpr bool EARLY = PGR == 2;
+    constexpr bool EARLY = PGR >= 2;
     auto body = [&](int64_t kt, Stage& nxt) {  // nxt = S[(kt + 1) % PGR]
         const int cur = (int)(kt & 1);
 #pragma unroll
@@ -233,16 +233,15 @@ __device__ __forceinline__ void gemm_nt_tile(const T* __restrict__ A, int64_t ld
             lds_frag(cur ^ 1, 0, 0);
         }
     };
-    if constexpr (PGR == 1) {
-        for (int64_t kt = 0; kt < nk; ++kt) body(kt, S[0]);
-    } else {
-        int64_t kt = 0;
-        for (; kt + 1 < nk; kt += 2) {
-            body(kt, S[PGR - 1]);
-            body(kt + 1, S[0]);
-        }
-        if (kt < nk) body(kt, S[PGR - 1]);
+    // PGR iterations per trip so that every stage index is a constant
+    int64_t kt = 0;
+    for (; kt + PGR <= nk; kt += PGR) {
+#pragma unroll
+        for (int u = 0; u < PGR; ++u) body(kt + u, S[(u + 1) % PGR]);
     }
+#pragma unroll
+    for (int u = 0; u < PGR - 1; ++u)
+        if (kt + u < nk) body(kt + u, S[(u + 1) % PGR]);
 
     // 32x32 accumulator layout: lane holds column (lane % 32) and rows
     // 8*(v/4) + 4*(lane/32) + (v%4) for v = 0..15.
