@@ -87,9 +87,11 @@ struct ASplit32 {
 };
 
 // Sum the per-wave 16x16 tiles in LDS and hand the result to the epilogue;
-// wave t finishes activation tile t (t < MT).
+// wave t finishes activation tile t (t < MT).  Only weight rows n0 + [c_lo,
+// c_lo + c_cnt) are stored (a workgroup may own part of a 16-row group).
 template <int WAVES, int MT, typename Epi>
-__device__ __forceinline__ void skinny_finish(const f32x4 (&acc)[MT], int64_t n0, const Epi& epi) {
+__device__ __forceinline__ void skinny_finish(const f32x4 (&acc)[MT], int64_t n0, const Epi& epi, int c_lo = 0,
+                                              int c_cnt = 16) {
     static_assert(MT <= WAVES, "one finishing wave per tile");
     __shared__ f32x4 red[WAVES][MT][kWave];
     const int lane = threadIdx.x & (kWave - 1);
@@ -102,23 +104,30 @@ __device__ __forceinline__ void skinny_finish(const f32x4 (&acc)[MT], int64_t n0
 #pragma unroll
     for (int w = 1; w < WAVES; ++w) tot += red[w][wave][lane];
     // 16x16 accumulator layout: lane holds column (lane % 16), rows 4*(lane/16) + v
+    if ((unsigned)((lane & 15) - c_lo) >= (unsigned)c_cnt) return;
     const auto c = epi.col(n0 + (lane & 15));
 #pragma unroll
     for (int v = 0; v < 4; ++v) epi.store(16 * wave + 4 * (lane >> 4) + v, c, tot[v]);
 }
 
 // Weights in lane order (layout.hpp): B holds packed_elems(N, K) elements;
-// this workgroup owns 16-row group g of B.
-template <typename TB, int WAVES, int UNROLL, int MT, typename AL, typename Epi>
+// this workgroup owns rows [part * 16 / PARTS, (part + 1) * 16 / PARTS) of
+// 16-row group g of B.  PARTS > 1 spreads a narrow product over more
+// workgroups (the weight stream of each part is a set of 128-byte runs);
+// the lanes of the other parts feed zeros to the MFMA.
+template <typename TB, int WAVES, int UNROLL, int MT, int PARTS, typename AL, typename Epi>
 __device__ __forceinline__ void skinny_packed_group(const AL& al, const TB* __restrict__ B, int64_t K,
-                                                    const Epi& epi, int64_t g) {
+                                                    const Epi& epi, int64_t g, int part = 0) {
+    static_assert(PARTS == 1 || PARTS == 2 || PARTS == 4, "parts of a 16-row group");
     constexpr int OPS = AL::kOps;
+    constexpr int PROWS = kSkinnyRows / PARTS;
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
     const int64_t KB = packed_kblocks(K);
     const u32x4* blk = reinterpret_cast<const u32x4*>(B) + g * KB * kPackChunks;
     const int row = lane & 15;
     const int kq = (lane >> 4) * 32;
+    const bool mine = PARTS == 1 || row / PROWS == part;
 
     f32x4 acc[MT];
 #pragma unroll
@@ -129,7 +138,7 @@ __device__ __forceinline__ void skinny_packed_group(const AL& al, const TB* __re
         for (int u = 0; u < UNROLL; ++u) {
             const int64_t b = kb + (int64_t)u * WAVES;
 #pragma unroll
-            for (int c = 0; c < 4; ++c) bw[u][c] = b < KB ? blk[b * kPackChunks + c * kWave + lane] : zero16();
+            for (int c = 0; c < 4; ++c) bw[u][c] = (mine && b < KB) ? blk[b * kPackChunks + c * kWave + lane] : zero16();
         }
 #pragma unroll
         for (int u = 0; u < UNROLL; ++u)
@@ -143,14 +152,16 @@ __device__ __forceinline__ void skinny_packed_group(const AL& al, const TB* __re
                     for (int o = 0; o < OPS; ++o) acc[t] = Mfma<TB>::mma16(aw[o], bw[u][c], acc[t]);
                 }
     }
-    skinny_finish<WAVES, MT>(acc, g * kSkinnyRows, epi);
+    skinny_finish<WAVES, MT>(acc, g * kSkinnyRows, epi, part * PROWS, PROWS);
 }
 
-template <typename TB, int WAVES, int UNROLL, int MT, typename AL, typename Epi>
+// Grid: PARTS * packed_groups(N) workgroups.
+template <typename TB, int WAVES, int UNROLL, int MT, int PARTS, typename AL, typename Epi>
 __global__ __launch_bounds__(WAVES* kWave) void skinny_packed(AL al, const TB* __restrict__ B,
                                                              int64_t N, int64_t K, Epi epi) {
     (void)N;
-    skinny_packed_group<TB, WAVES, UNROLL, MT, AL, Epi>(al, B, K, epi, blockIdx.x);
+    skinny_packed_group<TB, WAVES, UNROLL, MT, PARTS, AL, Epi>(al, B, K, epi, blockIdx.x / PARTS,
+                                                               (int)(blockIdx.x % PARTS));
 }
 
 // Several weight streams with the same activation rows in one launch
@@ -178,7 +189,7 @@ __global__ __launch_bounds__(WAVES* kWave) void skinny_packed_grouped(SkinnyGrou
     int q = 0;
     while (q + 1 < grp.n && b >= grp.start[q + 1]) ++q;
     const SkinnyProblem<TB, AL, Epi>& p = grp.p[q];
-    skinny_packed_group<TB, WAVES, UNROLL, MT, AL, Epi>(p.al, p.B, p.K, p.epi, b - grp.start[q]);
+    skinny_packed_group<TB, WAVES, UNROLL, MT, 1, AL, Epi>(p.al, p.B, p.K, p.epi, b - grp.start[q]);
 }
 
 // Row-major weights (row stride ldb), for caller-owned matrices.

@@ -265,11 +265,22 @@ hipError_t launch_gemm_f32(int site, const float* A, int64_t lda, int64_t M, con
 
 // Weight-streaming launches: MT 16-row activation tiles cover M = al.M.
 // B in lane order (layout.hpp), logical N x K.
+// A narrow product (few 16-row groups) splits each group over 2 or 4
+// workgroups so the weight stream is spread over the whole chip.
 template <typename TB, int MT, typename AL, typename Epi>
 void skinny_packed_mt(const AL& al, const TB* B, int64_t N, int64_t K, const Epi& epi, hipStream_t st) {
     constexpr int U = MT == 1 ? kSkinnyUnroll : 1;
-    hipLaunchKernelGGL((skinny_packed<TB, kSkinnyWaves, U, MT, AL, Epi>), dim3((unsigned)packed_groups(N)),
-                       dim3(kSkinnyWaves * kWave), 0, st, al, B, N, K, epi);
+    const int64_t groups = packed_groups(N);
+    const dim3 blk(kSkinnyWaves * kWave);
+    if (groups >= kCus)
+        hipLaunchKernelGGL((skinny_packed<TB, kSkinnyWaves, U, MT, 1, AL, Epi>), dim3((unsigned)groups), blk, 0, st,
+                           al, B, N, K, epi);
+    else if (2 * groups >= kCus)
+        hipLaunchKernelGGL((skinny_packed<TB, kSkinnyWaves, U, MT, 2, AL, Epi>), dim3((unsigned)(2 * groups)), blk, 0,
+                           st, al, B, N, K, epi);
+    else
+        hipLaunchKernelGGL((skinny_packed<TB, kSkinnyWaves, U, MT, 4, AL, Epi>), dim3((unsigned)(4 * groups)), blk, 0,
+                           st, al, B, N, K, epi);
 }
 
 template <typename TB, typename AL, typename Epi>

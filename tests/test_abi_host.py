@@ -124,3 +124,39 @@ def test_forward_and_baselines_reject_bad_args():
     assert lib.lowrank_layer_destroy(None) == pifa.PIFA_OK
     assert lib.pifa_layer_set_intermediate_scale(None, 0) == pifa.PIFA_ERR_INVALID_ARG
     assert lib.pifa_layer_overflow_count(None, None) == pifa.PIFA_ERR_INVALID_ARG
+
+
+def test_status_strings_of_build_and_reconstruction():
+    assert pifa.pifa_status_string(pifa.PIFA_ERR_NOT_RANK_R) == "PIFA_ERR_NOT_RANK_R"
+    assert pifa.pifa_status_string(pifa.PIFA_ERR_NOT_SPD) == "PIFA_ERR_NOT_SPD"
+
+
+def test_group_backward_and_calibration_reject_bad_args_on_host():
+    """Argument errors of the grouped, backward and reconstruction entry points
+    are found before any device work."""
+    lib = pifa.lib()
+    out = ctypes.c_void_p()
+    dims = (pifa.pifa_dims * 2)(pifa.pifa_dims(64, 96, 32), pifa.pifa_dims(32, 96, 32))
+    ptrs = (ctypes.c_void_p * 2)(FAKE.value, FAKE.value)
+    piv, npiv = np.arange(32, dtype=np.int32), np.arange(32, 96, dtype=np.int32)  # a valid partition
+    pp = (pifa._i32p * 2)(piv.ctypes.data_as(pifa._i32p), piv.ctypes.data_as(pifa._i32p))
+    npp = (pifa._i32p * 2)(npiv.ctypes.data_as(pifa._i32p), npiv.ctypes.data_as(pifa._i32p))
+    inval = pifa.PIFA_ERR_INVALID_ARG
+    # group: no layers, too many layers, null handle slot, differing d_in, fp32
+    assert lib.pifa_group_create(0, ptrs, ptrs, pp, npp, dims, pifa.PIFA_BF16, ctypes.byref(out)) == inval
+    assert lib.pifa_group_create(9, ptrs, ptrs, pp, npp, dims, pifa.PIFA_BF16, ctypes.byref(out)) == inval
+    assert lib.pifa_group_create(1, ptrs, ptrs, pp, npp, dims, pifa.PIFA_BF16, None) == inval
+    assert lib.pifa_group_create(2, ptrs, ptrs, pp, npp, dims, pifa.PIFA_BF16, ctypes.byref(out)) == inval
+    assert lib.pifa_group_create(1, ptrs, ptrs, pp, npp, dims, pifa.PIFA_F32,
+                                 ctypes.byref(out)) == pifa.PIFA_ERR_UNSUPPORTED
+    assert lib.pifa_group_forward(None, FAKE, FAKE, 4, None) == inval
+    assert lib.pifa_group_reserve(None, 4) == inval
+    assert lib.pifa_group_destroy(None) == pifa.PIFA_OK
+    # backward and calibration
+    assert lib.pifa_layer_backward(None, FAKE, FAKE, FAKE, 4, FAKE, FAKE, FAKE, None) == inval
+    assert lib.pifa_calib_create(0, ctypes.byref(out)) == inval
+    assert lib.pifa_calib_create(64, None) == inval
+    assert lib.pifa_calib_accumulate(None, FAKE, FAKE, 8, None) == inval
+    assert lib.pifa_calib_reconstruct(None, FAKE, 8, FAKE, 4, 0.25, 1e-3, FAKE, FAKE, None) == inval
+    assert lib.pifa_calib_read(None, None, None, None) == inval
+    assert lib.pifa_calib_destroy(None) == pifa.PIFA_OK
