@@ -580,7 +580,7 @@ def run_full(args):
         wl = Workload(d_in, d_out, r, inputs.config_seed(cfg, lay))
         for M in Ms:
             rotate = M <= 128
-            res = measure(wl, M, 100 if rotate else 20, 10 if rotate else 3, rotate)
+            res = measure(wl, M, 100 if rotate else 20, 10 if rotate else 40, rotate)
             res.update({"config": name, "d_in": d_in, "d_out": d_out, "r": r, "build_ms": wl.build_ms,
                         "pifa_weight_bytes": wl.pifa_bytes, "uv_weight_bytes": wl.uv_bytes,
                         "dense_weight_bytes": wl.dense_bytes,
