@@ -97,7 +97,24 @@ __global__ __launch_bounds__(256) void gather_tile(const bf16* __restrict__ in, 
     const uint16_t* src = reinterpret_cast<const uint16_t*>(in);
     const int64_t m0 = (int64_t)blockIdx.x * kTrTile, j0 = (int64_t)blockIdx.y * kTrTile;
     const int tid = threadIdx.x;
-    {
+    if (!idx && (ld_in & 7) == 0 && (reinterpret_cast<uintptr_t>(in) & 15) == 0) {
+        // plain transpose of 16-byte aligned rows: 8 columns per load
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int ch = tid + 256 * i, mm = ch / 8, j8 = (ch % 8) * 8;
+            const int64_t m = m0 + mm, j = j0 + j8;
+            uint16_t v[8];
+            if (m < M && j + 8 <= ncols) {
+                const u32x4 w = *reinterpret_cast<const u32x4*>(src + m * ld_in + j);
+                __builtin_memcpy(v, &w, 16);
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) v[e] = (m < M && j + e < ncols) ? src[m * ld_in + j + e] : (uint16_t)0;
+            }
+#pragma unroll
+            for (int e = 0; e < 8; ++e) tile[mm][j8 + e] = v[e];
+        }
+    } else {
         const int jj = tid % kTrTile;
         const int64_t j = j0 + jj;
         const int64_t cj = j < ncols ? (idx ? (int64_t)idx[j] : j) : 0;
