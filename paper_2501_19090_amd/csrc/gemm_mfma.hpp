@@ -19,11 +19,24 @@
 // row-major (row stride ldb) or in the lane order of layout.hpp (BPACK).
 #pragma once
 
+#include <type_traits>
+
 #include "common.hpp"
 #include "epilogue.hpp"
 #include "layout.hpp"
 
 namespace pifa {
+
+// An epilogue with skip_tile(m0, n0, BM, BN) may drop whole output tiles
+// (the workgroup exits before any work).
+template <typename E, typename = void>
+struct SkipEpi {
+    static constexpr bool value = false;
+};
+template <typename E>
+struct SkipEpi<E, std::void_t<decltype(&E::skip_tile)>> {
+    static constexpr bool value = true;
+};
 
 template <typename T>
 struct Mfma;
@@ -117,6 +130,9 @@ __device__ __forceinline__ void gemm_nt_tile(const T* __restrict__ A, int64_t ld
     __shared__ __attribute__((aligned(16))) T Bs[2][BN * LDK];
 
     const int64_t m0 = tm * BM, n0 = tn * BN;
+    if constexpr (SkipEpi<Epi>::value) {
+        if (epi.skip_tile(m0, n0, BM, BN)) return;
+    }
 
     const auto ars = make_rsrc31(A + m0 * lda, ((M - m0 - 1) * lda + K) * (int64_t)sizeof(T));
     const int64_t KB = packed_kblocks(K);

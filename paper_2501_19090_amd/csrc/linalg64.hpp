@@ -216,9 +216,16 @@ __global__ __launch_bounds__(256) void transpose64(const double* __restrict__ in
 
 // Epilogue for the MFMA GEMM: out[m * ld + n] += acc (the running fp64 sums
 // of the calibration statistics; fp32 products are accumulated in fp64).
+// With lower_tiles, output tiles entirely above the diagonal are skipped (a
+// symmetric sum; symmetrize_lower64 fills them afterwards).
 struct AccF64Epi {
     double* out;
     int64_t ld, N, M;
+    bool lower_tiles;
+    __device__ __forceinline__ bool skip_tile(int64_t m0, int64_t n0, int BM, int BN) const {
+        (void)BN;
+        return lower_tiles && n0 >= m0 + BM;
+    }
     struct Col {
         int64_t n;
         bool ok;
@@ -228,5 +235,16 @@ struct AccF64Epi {
         if (m < M && c.ok) out[m * ld + c.n] += (double)v;
     }
 };
+
+
+// S[i][j] = S[j][i] for i < j (n x n row-major): completes a sum of which only
+// the lower triangle (and whole diagonal tiles) was accumulated.
+__global__ void symmetrize_lower64(double* __restrict__ S, int64_t n) {
+    const int64_t total = n * n;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t i = e / n, j = e % n;
+        if (i < j) S[e] = S[j * n + i];
+    }
+}
 
 }  // namespace pifa

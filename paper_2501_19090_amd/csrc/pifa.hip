@@ -1363,11 +1363,12 @@ pifa_status pifa_calib_accumulate(pifa_calib_handle c, const void* X_o, const vo
     }
     const bf16* xo = X_o == X_u ? xut : xot;
     // S += X_u^T X_u and P += X_o^T X_u: rows of the transposed batches, K = tokens
-    if (launch_gemm<bf16, false>(kSiteCalibGram, xut, Bp, n, xut, Bp, n, Bp, AccF64Epi{c->S, n, n, n}, partials, st) !=
-        hipSuccess)
+    // S is symmetric: only its lower tiles are accumulated (completed on read)
+    if (launch_gemm<bf16, false>(kSiteCalibGram, xut, Bp, n, xut, Bp, n, Bp, AccF64Epi{c->S, n, n, n, true}, partials,
+                                 st) != hipSuccess)
         return PIFA_ERR_HIP;
-    if (launch_gemm<bf16, false>(kSiteCalibGram, xo, Bp, n, xut, Bp, n, Bp, AccF64Epi{c->P, n, n, n}, partials, st) !=
-        hipSuccess)
+    if (launch_gemm<bf16, false>(kSiteCalibGram, xo, Bp, n, xut, Bp, n, Bp, AccF64Epi{c->P, n, n, n, false}, partials,
+                                 st) != hipSuccess)
         return PIFA_ERR_HIP;
     return PIFA_OK;
 }
@@ -1375,6 +1376,10 @@ pifa_status pifa_calib_accumulate(pifa_calib_handle c, const void* X_o, const vo
 pifa_status pifa_calib_read(pifa_calib_handle c, double* S, double* P, void* stream) {
     if (!c) return PIFA_ERR_INVALID_ARG;
     const size_t b = (size_t)c->n * c->n * sizeof(double);
+    if (S) {
+        hipLaunchKernelGGL(symmetrize_lower64, dim3(grid_for(c->n * c->n)), dim3(256), 0, as_stream(stream), c->S, c->n);
+        PIFA_HIP(hipGetLastError());
+    }
     if (S) PIFA_HIP(hipMemcpyAsync(S, c->S, b, hipMemcpyDeviceToDevice, as_stream(stream)));
     if (P) PIFA_HIP(hipMemcpyAsync(P, c->P, b, hipMemcpyDeviceToDevice, as_stream(stream)));
     return PIFA_OK;
@@ -1409,6 +1414,8 @@ pifa_status pifa_calib_reconstruct(pifa_calib_handle c, const double* W, int64_t
         if ((e = (call)) != hipSuccess) return PIFA_ERR_HIP; \
     } while (0)
     PIFA_HIP(hipMemsetAsync(c->info, 0, sizeof(int), st));
+    hipLaunchKernelGGL(symmetrize_lower64, dim3(grid_for(n * n)), dim3(256), 0, st, c->S, n);
+    PIFA_GO(hipGetLastError());
     // T = W (lam P + (1 - lam) S)
     hipLaunchKernelGGL(axpby_diag64, dim3(grid_for(n * n)), dim3(256), 0, st, n, lam, (const double*)c->P, 1.0 - lam,
                        (const double*)c->S, 0.0, Z);
