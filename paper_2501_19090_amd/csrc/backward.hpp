@@ -197,6 +197,30 @@ struct GradPivotEpi {
         gp[m * r_pad + c.n] = g;
         if (c.piv_ok) reinterpret_cast<uint16_t*>(gpt)[c.n * ldt + m] = f32_to_bf16_bits(g);
     }
+    // rows m .. m + 3 (m % 4 == 0) of column c: the transposed copy is one
+    // 8-byte store (ldt % 8 == 0)
+    __device__ __forceinline__ void store4(int64_t m, const Col& c, const float (&v)[4]) const {
+        if (c.n >= r_pad || m >= M) return;
+        const uint16_t* g16 = reinterpret_cast<const uint16_t*>(G);
+        uint16_t h[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const bool ok = m + e < M;
+            const float g = (c.piv_ok && ok) ? v[e] + bf16_bits_to_f32(g16[(m + e) * ldg + c.src]) : 0.f;
+            if (ok) gp[(m + e) * r_pad + c.n] = g;
+            h[e] = f32_to_bf16_bits(g);
+        }
+        if (c.piv_ok) {
+            uint16_t* dst = reinterpret_cast<uint16_t*>(gpt) + c.n * ldt + m;
+            if (m + 4 <= M) {
+                *reinterpret_cast<uint64_t*>(dst) = __builtin_bit_cast(uint64_t, h);
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (m + e < M) dst[e] = h[e];
+            }
+        }
+    }
 };
 
 // Row m of gp (n = r_pad fp32 values, n % 4 == 0) -> fp16 out[m][:] times

@@ -27,6 +27,17 @@
 
 namespace pifa {
 
+// An epilogue with store4(m, col, v[4]) takes the four consecutive rows
+// m .. m + 3 of one column that a lane of the 32x32 layout holds at once.
+template <typename E, typename = void>
+struct Store4Epi {
+    static constexpr bool value = false;
+};
+template <typename E>
+struct Store4Epi<E, std::void_t<decltype(&E::store4)>> {
+    static constexpr bool value = true;
+};
+
 // An epilogue with skip_tile(m0, n0, BM, BN) may drop whole output tiles
 // (the workgroup exits before any work).
 template <typename E, typename = void>
@@ -267,8 +278,17 @@ __device__ __forceinline__ void gemm_nt_tile(const T* __restrict__ A, int64_t ld
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
             const int64_t mb = m0 + wm * WTM + i * 32 + 4 * (lane >> 5);
+            if constexpr (Store4Epi<Epi>::value) {
 #pragma unroll
-            for (int v = 0; v < 16; ++v) epi.store(mb + 8 * (v >> 2) + (v & 3), c, acc[i][j][v]);
+                for (int q = 0; q < 4; ++q) {
+                    const float v4[4] = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                                         acc[i][j][4 * q + 3]};
+                    epi.store4(mb + 8 * q, c, v4);
+                }
+            } else {
+#pragma unroll
+                for (int v = 0; v < 16; ++v) epi.store(mb + 8 * (v >> 2) + (v & 3), c, acc[i][j][v]);
+            }
         }
     }
 }
