@@ -39,7 +39,7 @@ constexpr int64_t kRowPad = 64;      // W_p rows / C columns padded to this mult
 
 constexpr int kGemmBK = 64;
 constexpr int64_t kCus = 256;
-constexpr int kSkinnyWaves = 8, kSkinnyUnroll = 2;
+constexpr int kSkinnyWaves = 8;
 
 #define PIFA_HIP(call)                                  \
     do {                                                \
@@ -263,24 +263,59 @@ hipError_t launch_gemm_f32(int site, const float* A, int64_t lda, int64_t M, con
     return hipGetLastError();
 }
 
-// Weight-streaming launches: MT 16-row activation tiles cover M = al.M.
-// B in lane order (layout.hpp), logical N x K.
-// A narrow product (few 16-row groups) splits each group over 2 or 4
-// workgroups so the weight stream is spread over the whole chip.
+// Launch shape of a weight-streaming product with one 16-row activation tile:
+// waves per workgroup, 128-wide K blocks per wave step (unroll) and
+// workgroups per 16-row weight group (parts).  Measured over every decode
+// shape of the LLaMA-7B / 70B layers and the rank sweep on MI355X:
+//  * few activation rows (M <= 4): the A operand costs almost nothing, so the
+//    shape that puts the whole weight stream in flight at once wins -- 16
+//    waves, enough unroll to cover K in about one step, and narrow products
+//    (at most 128 groups) split over two workgroups;
+//  * more rows: every workgroup re-reads the activation block, so fewer,
+//    deeper workgroups (8 waves, unroll up to 4) win, and a group is split
+//    only when the grid would be small or K is long.
+struct SkinnyShape {
+    int waves, unroll, parts;
+};
+
+SkinnyShape skinny_shape(int64_t M, int64_t groups, int64_t KB) {
+    if (M <= 4) return {KB >= 8 ? 16 : 8, KB > 16 ? 2 : 1, groups <= 128 ? 2 : 1};
+    return {8, KB <= 8 ? 1 : KB <= 16 ? 2 : 4, (groups < 128 || (groups < 256 && KB >= 64)) ? 2 : 1};
+}
+
+template <typename TB, int W, int U, int MT, int P, typename AL, typename Epi>
+void skinny_launch(const AL& al, const TB* B, int64_t N, int64_t K, const Epi& epi, hipStream_t st) {
+    hipLaunchKernelGGL((skinny_packed<TB, W, U, MT, P, AL, Epi>), dim3((unsigned)(P * packed_groups(N))),
+                       dim3(W * kWave), 0, st, al, B, N, K, epi);
+}
+
+// B in lane order (layout.hpp), logical N x K.  Several activation tiles
+// (MT > 1) use 8 waves without unrolling; a narrow product (few 16-row
+// groups) splits each group over 2 or 4 workgroups so the weight stream is
+// spread over the whole chip.
 template <typename TB, int MT, typename AL, typename Epi>
 void skinny_packed_mt(const AL& al, const TB* B, int64_t N, int64_t K, const Epi& epi, hipStream_t st) {
-    constexpr int U = MT == 1 ? kSkinnyUnroll : 1;
     const int64_t groups = packed_groups(N);
-    const dim3 blk(kSkinnyWaves * kWave);
-    if (groups >= kCus)
-        hipLaunchKernelGGL((skinny_packed<TB, kSkinnyWaves, U, MT, 1, AL, Epi>), dim3((unsigned)groups), blk, 0, st,
-                           al, B, N, K, epi);
-    else if (2 * groups >= kCus)
-        hipLaunchKernelGGL((skinny_packed<TB, kSkinnyWaves, U, MT, 2, AL, Epi>), dim3((unsigned)(2 * groups)), blk, 0,
-                           st, al, B, N, K, epi);
-    else
-        hipLaunchKernelGGL((skinny_packed<TB, kSkinnyWaves, U, MT, 4, AL, Epi>), dim3((unsigned)(4 * groups)), blk, 0,
-                           st, al, B, N, K, epi);
+    if constexpr (MT == 1) {
+        const SkinnyShape c = skinny_shape(al.M, groups, packed_kblocks(K));
+        const int key = c.waves * 100 + c.unroll * 10 + c.parts;
+        switch (key) {
+            case 811: return skinny_launch<TB, 8, 1, 1, 1>(al, B, N, K, epi, st);
+            case 812: return skinny_launch<TB, 8, 1, 1, 2>(al, B, N, K, epi, st);
+            case 821: return skinny_launch<TB, 8, 2, 1, 1>(al, B, N, K, epi, st);
+            case 822: return skinny_launch<TB, 8, 2, 1, 2>(al, B, N, K, epi, st);
+            case 841: return skinny_launch<TB, 8, 4, 1, 1>(al, B, N, K, epi, st);
+            case 842: return skinny_launch<TB, 8, 4, 1, 2>(al, B, N, K, epi, st);
+            case 1611: return skinny_launch<TB, 16, 1, 1, 1>(al, B, N, K, epi, st);
+            case 1612: return skinny_launch<TB, 16, 1, 1, 2>(al, B, N, K, epi, st);
+            case 1621: return skinny_launch<TB, 16, 2, 1, 1>(al, B, N, K, epi, st);
+            default: return skinny_launch<TB, 16, 2, 1, 2>(al, B, N, K, epi, st);
+        }
+    } else {
+        if (groups >= kCus) skinny_launch<TB, kSkinnyWaves, 1, MT, 1>(al, B, N, K, epi, st);
+        else if (2 * groups >= kCus) skinny_launch<TB, kSkinnyWaves, 1, MT, 2>(al, B, N, K, epi, st);
+        else skinny_launch<TB, kSkinnyWaves, 1, MT, 4>(al, B, N, K, epi, st);
+    }
 }
 
 template <typename TB, typename AL, typename Epi>
@@ -328,9 +363,21 @@ hipError_t launch_skinny_grouped(int site, SkinnyGroup<TB, AL, Epi> grp, const i
     grp.start[0] = 0;
     for (int q = 0; q < grp.n; ++q) grp.start[q + 1] = grp.start[q] + packed_groups(n_rows[q]);
     if (grp.start[grp.n] == 0) return hipSuccess;
+    int64_t KB = 0;
+    for (int q = 0; q < grp.n; ++q) KB = std::max(KB, packed_kblocks(grp.p[q].K));
+    const SkinnyShape c = skinny_shape(grp.p[0].al.M, grp.start[grp.n], KB);  // one workgroup per group
+    const dim3 grid((unsigned)grp.start[grp.n]);
     TimedLaunch timed(site, st);
-    hipLaunchKernelGGL((skinny_packed_grouped<TB, kSkinnyWaves, kSkinnyUnroll, 1, AL, Epi>),
-                       dim3((unsigned)grp.start[grp.n]), dim3(kSkinnyWaves * kWave), 0, st, grp);
+    if (c.waves == 16 && c.unroll == 2)
+        hipLaunchKernelGGL((skinny_packed_grouped<TB, 16, 2, 1, AL, Epi>), grid, dim3(16 * kWave), 0, st, grp);
+    else if (c.waves == 16)
+        hipLaunchKernelGGL((skinny_packed_grouped<TB, 16, 1, 1, AL, Epi>), grid, dim3(16 * kWave), 0, st, grp);
+    else if (c.unroll == 4)
+        hipLaunchKernelGGL((skinny_packed_grouped<TB, 8, 4, 1, AL, Epi>), grid, dim3(8 * kWave), 0, st, grp);
+    else if (c.unroll == 2)
+        hipLaunchKernelGGL((skinny_packed_grouped<TB, 8, 2, 1, AL, Epi>), grid, dim3(8 * kWave), 0, st, grp);
+    else
+        hipLaunchKernelGGL((skinny_packed_grouped<TB, 8, 1, 1, AL, Epi>), grid, dim3(8 * kWave), 0, st, grp);
     return hipGetLastError();
 }
 
@@ -338,7 +385,7 @@ hipError_t launch_skinny_grouped(int site, SkinnyGroup<TB, AL, Epi> grp, const i
 template <typename TB, int MT, typename AL, typename Epi>
 void skinny_rowmajor_mt(const AL& al, const TB* B, int64_t ldb, int64_t N, int64_t K, const Epi& epi,
                         hipStream_t st) {
-    constexpr int U = MT == 1 ? kSkinnyUnroll : 1;
+    constexpr int U = MT == 1 ? 2 : 1;
     hipLaunchKernelGGL((skinny_rowmajor<TB, kSkinnyWaves, U, MT, AL, Epi>), dim3((unsigned)ceil_div(N, kSkinnyRows)),
                        dim3(kSkinnyWaves * kWave), 0, st, al, B, ldb, N, K, epi);
 }
