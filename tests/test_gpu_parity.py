@@ -18,7 +18,8 @@ from gpu_util import (DeviceLayer, activations, config_layer, from_dev, gaussian
 pytestmark = pytest.mark.gpu
 
 TOL = {"bf16": 5e-3, "f32": 1e-5}
-DECODE_AND_PREFILL_M = (1, 2, 7, 16, 17, 33, 64, 100, 128, 129, 300)
+# 4 / 5 straddle the decode launch-shape switch (few activation rows vs many)
+DECODE_AND_PREFILL_M = (1, 2, 4, 5, 7, 16, 17, 33, 64, 100, 128, 129, 300)
 
 
 @pytest.fixture(scope="module", autouse=True)
