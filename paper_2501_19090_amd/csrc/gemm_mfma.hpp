@@ -358,20 +358,43 @@ struct SplitEpi {
 };
 
 // Sum the S partial products in split order (deterministic) and apply the
-// real epilogue; one thread per 4 consecutive columns of a row.
+// real epilogue; one thread per 4 consecutive columns of a row.  When N is a
+// multiple of 4 the four partial values of a split arrive in one 16-byte
+// load and four splits are loaded before they are added, so that a thread
+// keeps several loads in flight; the additions happen in the same order
+// either way.
 template <typename Epi>
 __global__ __launch_bounds__(256) void split_reduce(const float* __restrict__ P, int S, int64_t M,
                                                     int64_t N, Epi epi) {
     const int64_t nq = ceil_div(N, 4);
+    const bool vec = (N & 3) == 0;
     for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < M * nq;
          q += (int64_t)gridDim.x * blockDim.x) {
         const int64_t m = q / nq, n0 = (q % nq) * 4;
         float v[4] = {0.f, 0.f, 0.f, 0.f};
-        for (int s = 0; s < S; ++s) {
-            const float* p = P + ((int64_t)s * M + m) * N + n0;
+        if (vec) {
+            const f32x4* p = reinterpret_cast<const f32x4*>(P + m * N + n0);
+            const int64_t stride = M * N / 4;  // one split, in 16-byte units
+            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+            int s = 0;
+            for (; s + 4 <= S; s += 4) {
+                const f32x4 a = p[s * stride], b = p[(s + 1) * stride], c = p[(s + 2) * stride],
+                            d = p[(s + 3) * stride];
+                acc += a;
+                acc += b;
+                acc += c;
+                acc += d;
+            }
+            for (; s < S; ++s) acc += p[s * stride];
 #pragma unroll
-            for (int e = 0; e < 4; ++e)
-                if (n0 + e < N) v[e] += p[e];
+            for (int e = 0; e < 4; ++e) v[e] = acc[e];
+        } else {
+            for (int s = 0; s < S; ++s) {
+                const float* p = P + ((int64_t)s * M + m) * N + n0;
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (n0 + e < N) v[e] += p[e];
+            }
         }
 #pragma unroll
         for (int e = 0; e < 4; ++e)

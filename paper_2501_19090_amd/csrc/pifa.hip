@@ -169,7 +169,11 @@ struct TimedLaunch {
 enum TileCfg : int { kTile256x256 = 0, kTile256x128 = 1, kTile128x128 = 2 };
 
 // K splitting for launches that would leave CUs idle: at most kMaxSplit
-// splits of at least two K tiles each, partials capped at kMaxPartialBytes.
+// splits of at least four K tiles each, with the fp32 partials (s M N 4
+// bytes, written and read back once) at most the weight bytes (N K 2) and
+// capped at kMaxPartialBytes.  Measured on the LLaMA-7B attention products
+// at M = 17..256: more splits than this fill more CUs but lose more to the
+// partials and the short K loops than they gain.
 constexpr int64_t kMaxSplit = 16;
 constexpr int64_t kMaxPartialBytes = 256ll << 20;
 
@@ -180,7 +184,8 @@ struct SplitPlan {
 SplitPlan split_plan(int64_t tiles, int64_t M, int64_t N, int64_t K) {
     SplitPlan p{1, K};
     if (tiles >= kCus) return p;
-    int64_t s = std::min<int64_t>({ceil_div(kCus, tiles), K / (2 * kGemmBK), kMaxSplit,
+    int64_t s = std::min<int64_t>({ceil_div(kCus, tiles), K / (4 * kGemmBK), kMaxSplit,
+                                   std::max<int64_t>(1, K / (2 * std::max<int64_t>(1, M))),
                                    kMaxPartialBytes / std::max<int64_t>(1, M * N * 4)});
     if (s <= 1) return p;
     p.k_split = round_up(ceil_div(K, s), kGemmBK);
