@@ -170,10 +170,10 @@ enum TileCfg : int { kTile256x256 = 0, kTile256x128 = 1, kTile128x128 = 2 };
 
 // K splitting for launches that would leave CUs idle: at most kMaxSplit
 // splits of at least four K tiles each, with the fp32 partials (s M N 4
-// bytes, written and read back once) at most the weight bytes (N K 2) and
-// capped at kMaxPartialBytes.  Measured on the LLaMA-7B attention products
-// at M = 17..256: more splits than this fill more CUs but lose more to the
-// partials and the short K loops than they gain.
+// bytes, written and read back once) at most the operand bytes ((M + N) K 2)
+// and capped at kMaxPartialBytes.  Measured on the LLaMA-7B attention
+// products at M = 17..256: more splits than this fill more CUs but lose more
+// to the partials and the short K loops than they gain.
 constexpr int64_t kMaxSplit = 16;
 constexpr int64_t kMaxPartialBytes = 256ll << 20;
 
@@ -185,7 +185,7 @@ SplitPlan split_plan(int64_t tiles, int64_t M, int64_t N, int64_t K) {
     SplitPlan p{1, K};
     if (tiles >= kCus) return p;
     int64_t s = std::min<int64_t>({ceil_div(kCus, tiles), K / (4 * kGemmBK), kMaxSplit,
-                                   std::max<int64_t>(1, K / (2 * std::max<int64_t>(1, M))),
+                                   std::max<int64_t>(1, K * (M + N) / (2 * std::max<int64_t>(1, M * N))),
                                    kMaxPartialBytes / std::max<int64_t>(1, M * N * 4)});
     if (s <= 1) return p;
     p.k_split = round_up(ceil_div(K, s), kGemmBK);
