@@ -273,6 +273,15 @@ struct RowScaleEpi {
     __device__ __forceinline__ void store(int64_t m, const Col& c, float v) const {
         if (m < M && c.ok) Store<bf16>::put(out + m * ldo + c.n, v * row_scale[m] * out_scale);
     }
+    // rows m .. m + 3 (m % 4 == 0) of column c: one 16-byte load of their
+    // scales (row_scale holds M rounded up to 4 values)
+    __device__ __forceinline__ void store4(int64_t m, const Col& c, const float (&v)[4]) const {
+        if (m >= M || !c.ok) return;
+        const f32x4 s = *reinterpret_cast<const f32x4*>(row_scale + m);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            if (m + e < M) Store<bf16>::put(out + (m + e) * ldo + c.n, v[e] * s[e] * out_scale);
+    }
 };
 
 }  // namespace pifa
