@@ -163,7 +163,7 @@ __global__ void zero_cols(bf16* __restrict__ p, int64_t rows, int64_t ld, int64_
 }
 
 // Epilogue of G_p = G[:, I^c] C (+ G[:, I]): acc(m, j) for j < r_pad.
-//   * adds G[m, piv[j]] for j < r;
+//   * the accumulator starts from G[m, piv[j]] for j < r (init);
 //   * writes G_p in fp32 to gp[m * r_pad + j] (padding columns j >= r get
 //     zeros), for the row-wise fp16 conversion;
 //   * writes bf16(G_p) transposed to gpt[j * ldt + m] for j < r (the A
@@ -190,10 +190,14 @@ struct GradPivotEpi {
         c.src = c.piv_ok ? (int64_t)piv[n] : 0;
         return c;
     }
+    // the product starts from G[m, piv[n]] (the G[:, I] term)
+    __device__ __forceinline__ float init(int64_t m, const Col& c) const {
+        const uint16_t* g16 = reinterpret_cast<const uint16_t*>(G);
+        return (c.piv_ok && m < M) ? bf16_bits_to_f32(g16[m * ldg + c.src]) : 0.f;
+    }
     __device__ __forceinline__ void store(int64_t m, const Col& c, float v) const {
         if (m >= M || c.n >= r_pad) return;
-        const uint16_t* g16 = reinterpret_cast<const uint16_t*>(G);
-        const float g = c.piv_ok ? v + bf16_bits_to_f32(g16[m * ldg + c.src]) : 0.f;
+        const float g = c.piv_ok ? v : 0.f;
         gp[m * r_pad + c.n] = g;
         if (c.piv_ok) reinterpret_cast<uint16_t*>(gpt)[c.n * ldt + m] = f32_to_bf16_bits(g);
     }
@@ -201,12 +205,11 @@ struct GradPivotEpi {
     // 8-byte store (ldt % 8 == 0)
     __device__ __forceinline__ void store4(int64_t m, const Col& c, const float (&v)[4]) const {
         if (c.n >= r_pad || m >= M) return;
-        const uint16_t* g16 = reinterpret_cast<const uint16_t*>(G);
         uint16_t h[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const bool ok = m + e < M;
-            const float g = (c.piv_ok && ok) ? v[e] + bf16_bits_to_f32(g16[(m + e) * ldg + c.src]) : 0.f;
+            const float g = (c.piv_ok && ok) ? v[e] : 0.f;
             if (ok) gp[(m + e) * r_pad + c.n] = g;
             h[e] = f32_to_bf16_bits(g);
         }

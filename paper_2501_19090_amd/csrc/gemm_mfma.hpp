@@ -27,6 +27,19 @@
 
 namespace pifa {
 
+// An epilogue with init(m, col) gives the starting value of acc(m, n) (the
+// product is added to it): the GEMM loads it before its K loop, where the
+// load latency hides behind the first tiles' loads, and split_reduce starts
+// its sum with it.
+template <typename E, typename = void>
+struct InitEpi {
+    static constexpr bool value = false;
+};
+template <typename E>
+struct InitEpi<E, std::void_t<decltype(&E::init)>> {
+    static constexpr bool value = true;
+};
+
 // An epilogue with store4(m, col, v[4]) takes the four consecutive rows
 // m .. m + 3 of one column that a lane of the 32x32 layout holds at once.
 template <typename E, typename = void>
@@ -205,6 +218,19 @@ __device__ __forceinline__ void gemm_nt_tile(const T* __restrict__ A, int64_t ld
     for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j) acc[i][j] = f32x16{};
+    if constexpr (InitEpi<Epi>::value) {
+        // 32x32 accumulator layout (see the epilogue below)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const auto c = epi.col(n0 + wn * WTN + j * 32 + (lane & 31));
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                const int64_t mb = m0 + wm * WTM + i * 32 + 4 * (lane >> 5);
+#pragma unroll
+                for (int v = 0; v < 16; ++v) acc[i][j][v] = epi.init(mb + 8 * (v >> 2) + (v & 3), c);
+            }
+        }
+    }
 
     // 32x32x16 operands: lane supplies row (lane % 32), K values 8*(lane/32) .. +7
     const int frag_row = lane & 31, frag_k = (lane >> 5) * 8;
@@ -357,8 +383,9 @@ struct SplitEpi {
     }
 };
 
-// Sum the S partial products in split order (deterministic) and apply the
-// real epilogue; one thread per 4 consecutive columns of a row.  When N is a
+// Sum the S partial products in split order (deterministic; after the
+// epilogue's starting value, if it has one) and apply the real epilogue; one
+// thread per 4 consecutive columns of a row.  When N is a
 // multiple of 4 the four partial values of a split arrive in one 16-byte
 // load and four splits are loaded before they are added, so that a thread
 // keeps several loads in flight; the additions happen in the same order
@@ -372,10 +399,15 @@ __global__ __launch_bounds__(256) void split_reduce(const float* __restrict__ P,
          q += (int64_t)gridDim.x * blockDim.x) {
         const int64_t m = q / nq, n0 = (q % nq) * 4;
         float v[4] = {0.f, 0.f, 0.f, 0.f};
+        if constexpr (InitEpi<Epi>::value) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (n0 + e < N) v[e] = epi.init(m, epi.col(n0 + e));
+        }
         if (vec) {
             const f32x4* p = reinterpret_cast<const f32x4*>(P + m * N + n0);
             const int64_t stride = M * N / 4;  // one split, in 16-byte units
-            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+            f32x4 acc = {v[0], v[1], v[2], v[3]};
             int s = 0;
             for (; s + 4 <= S; s += 4) {
                 const f32x4 a = p[s * stride], b = p[(s + 1) * stride], c = p[(s + 2) * stride],

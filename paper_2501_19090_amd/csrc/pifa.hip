@@ -229,11 +229,15 @@ hipError_t launch_gemm(int site, const T* A, int64_t lda, int64_t M, const T* B,
                        int64_t N, int64_t K, Epi epi, float* partials, hipStream_t st) {
     if (M == 0 || N == 0) return hipSuccess;
     TimedLaunch timed(site, st);
-    const TileCfg cfg = pick_tile(M, N);
+    TileCfg cfg = pick_tile(M, N);
+    // an epilogue that loads the accumulators' starting values needs more
+    // registers than the 256 x 256 tile has left (it spills there)
+    if (InitEpi<Epi>::value && cfg == kTile256x256) cfg = kTile256x128;
     if (cfg == kTile256x256) {
-        hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 256, kGemmBK, 2, 4, BPACK, 1, Epi>),
-                           dim3((unsigned)(ceil_div(M, 256) * ceil_div(N, 256))), dim3(8 * kWave), 0, st, A, lda,
-                           M, B, ldb, N, K, K, epi);
+        if constexpr (!InitEpi<Epi>::value)
+            hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 256, kGemmBK, 2, 4, BPACK, 1, Epi>),
+                               dim3((unsigned)(ceil_div(M, 256) * ceil_div(N, 256))), dim3(8 * kWave), 0, st, A,
+                               lda, M, B, ldb, N, K, K, epi);
     } else if (cfg == kTile256x128) {
         hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 128, kGemmBK, 4, 2, BPACK, 2, Epi>),
                            dim3((unsigned)(ceil_div(M, 256) * ceil_div(N, 128))), dim3(8 * kWave), 0, st, A, lda,
