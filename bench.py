@@ -436,8 +436,8 @@ def main():
                     help="only the headline steps plus one calibration copy of 512 MiB (for counter passes)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU only: this PIFA layer build has no multi-GPU path "
-              "(run with --gpus 1).", file=sys.stderr)
+        print("bench.py measures one GPU only (run with --gpus 1): sharding the PIFA layer over "
+              "several GPUs is not implemented.", file=sys.stderr)
         sys.exit(2)
 
     import torch
