@@ -433,7 +433,8 @@ def main():
     ap.add_argument("--out", default=os.path.join(ROOT, "gpurun_out", "bench_full.json"))
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--profile-run", action="store_true",
-                    help="only the headline steps plus one calibration copy of 512 MiB (for counter passes)")
+                    help="only the headline forward (warmup, then steps) plus one calibration copy of 512 MiB "
+                         "(for rocprofv3 runs)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only (run with --gpus 1): sharding the PIFA layer over "
@@ -463,6 +464,9 @@ def main():
         src = torch.empty(512 << 20, dtype=torch.uint8, device="cuda:0")
         dst = torch.empty_like(src)
         dst.copy_(src)
+        torch.cuda.synchronize()
+        for _ in range(args.warmup):
+            pifa.pifa_forward(h, x, y, M, stream)
         torch.cuda.synchronize()
         for _ in range(args.steps):
             pifa.pifa_forward(h, x, y, M, stream)
@@ -580,7 +584,9 @@ def run_full(args):
         wl = Workload(d_in, d_out, r, inputs.config_seed(cfg, lay))
         for M in Ms:
             rotate = M <= 128
-            res = measure(wl, M, 100 if rotate else 20, 10 if rotate else 40, rotate)
+            # prefill rows: 200 warm-up launches per layer so the clocks have
+            # settled under the load being timed (about 150 launches at 4096 rows)
+            res = measure(wl, M, 100 if rotate else 50, 10 if rotate else 200, rotate)
             res.update({"config": name, "d_in": d_in, "d_out": d_out, "r": r, "build_ms": wl.build_ms,
                         "pifa_weight_bytes": wl.pifa_bytes, "uv_weight_bytes": wl.uv_bytes,
                         "dense_weight_bytes": wl.dense_bytes,
@@ -593,6 +599,18 @@ def run_full(args):
         del wl
         import torch
         torch.cuda.empty_cache()
+    # small batches of the attention shape, where K is split across CUs
+    name = "B_attn_4096"
+    cfg, lay, d_in, d_out, r, dt, Ms, kind = inputs.CONFIGS[name]
+    wl = Workload(d_in, d_out, r, inputs.config_seed(cfg, lay))
+    for M in (17, 32, 64, 256, 512):
+        res = measure(wl, M, 100, 200, False)
+        res.update({"config": name + "_small_batch", "d_in": d_in, "d_out": d_out, "r": r,
+                    "pifa_frac_mfma": res["pifa_tflops"] / PEAK_BF16_TFLOPS,
+                    "pifa_frac_hbm": res["pifa_gbps"] / PEAK_HBM_GBPS})
+        log(json.dumps({k: (round(v, 4) if isinstance(v, float) else v) for k, v in res.items() if k != "kernels"}))
+        rows.append(res)
+    wl.close()
     return rows
 
 

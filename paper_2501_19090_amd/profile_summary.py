@@ -3,8 +3,12 @@
     python -m paper_2501_19090_amd.profile_summary stats  <kernel_stats.csv> <out.md> <command...>
     python -m paper_2501_19090_amd.profile_summary traffic <fetch_dir> <write_dir> <kernel-substring>
            <launch-name> <out.txt> <command...>
+    python -m paper_2501_19090_amd.profile_summary steady <kernel_trace.csv> <N> <out.md> <kernel-substring>...
 
 `stats` turns a --kernel-trace --stats CSV into a short markdown table.
+`steady` appends to <out.md> the average duration of the last N dispatches
+of each kernel whose name contains a given substring (the timed steps that
+follow the warm-up, as bench.py times them).
 `traffic` reads two --pmc passes (FETCH_SIZE, then WRITE_SIZE; KiB per
 dispatch), takes the average for the kernel whose name contains
 <kernel-substring>, and scales it by what the same counters read for the
@@ -41,6 +45,21 @@ def stats(csv_path: str, out_md: str, command: str) -> None:
             _short(r["Name"]), r["Calls"], float(r["AverageNs"]) / 1e3, float(r["MinNs"]) / 1e3,
             float(r["MaxNs"]) / 1e3, float(r["Percentage"])))
     with open(out_md, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
+def steady(trace_csv: str, n: int, out_md: str, subs) -> None:
+    rows = list(csv.DictReader(open(trace_csv)))
+    lines = ["", "Steady state: average of the last %d dispatches of each kernel (after the warm-up):" % n, "",
+             "| kernel | dispatches averaged | avg us |", "|---|---:|---:|"]
+    for sub in subs:
+        d = [(int(r["Start_Timestamp"]), int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+             for r in rows if sub in r["Kernel_Name"]]
+        d.sort()
+        last = [x for _, x in d[-n:]]
+        if last:
+            lines.append("| `%s` | %d | %.2f |" % (_short(sub), len(last), sum(last) / len(last) / 1e3))
+    with open(out_md, "a") as f:
         f.write("\n".join(lines) + "\n")
 
 
@@ -92,6 +111,8 @@ if __name__ == "__main__":
     mode = sys.argv[1]
     if mode == "stats":
         stats(sys.argv[2], sys.argv[3], " ".join(sys.argv[4:]))
+    elif mode == "steady":
+        steady(sys.argv[2], int(sys.argv[3]), sys.argv[4], sys.argv[5:])
     elif mode == "traffic":
         traffic(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5], sys.argv[6], " ".join(sys.argv[7:]))
     else:
