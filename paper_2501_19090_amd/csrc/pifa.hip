@@ -230,11 +230,14 @@ hipError_t launch_gemm(int site, const T* A, int64_t lda, int64_t M, const T* B,
     if (M == 0 || N == 0) return hipSuccess;
     TimedLaunch timed(site, st);
     TileCfg cfg = pick_tile(M, N);
-    // an epilogue that loads the accumulators' starting values needs more
-    // registers than the 256 x 256 tile has left (it spills there)
-    if (InitEpi<Epi>::value && cfg == kTile256x256) cfg = kTile256x128;
+    // epilogues that load the accumulators' starting values, or add into
+    // fp64 / store fp32 outputs, need more registers than the 256 x 256 tile
+    // has left (it spills there)
+    constexpr bool kWideOk = !InitEpi<Epi>::value && !std::is_same<Epi, AccF64Epi>::value &&
+                             !std::is_same<Epi, ScatterEpi<float, kWsNone>>::value;
+    if (!kWideOk && cfg == kTile256x256) cfg = kTile256x128;
     if (cfg == kTile256x256) {
-        if constexpr (!InitEpi<Epi>::value)
+        if constexpr (kWideOk)
             hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 256, kGemmBK, 2, 4, BPACK, 1, Epi>),
                                dim3((unsigned)(ceil_div(M, 256) * ceil_div(N, 256))), dim3(8 * kWave), 0, st, A,
                                lda, M, B, ldb, N, K, K, epi);
