@@ -66,7 +66,7 @@ class Workload:
         import torch
         from paper_2501_19090_amd import inputs, pifa
         self.torch, self.pifa = torch, pifa
-        self.d_in, self.d_out, self.r = d_in, d_out, r
+        self.d_in, self.d_out, self.r, self.seed = d_in, d_out, r, seed
         dev = torch.device("cuda:0")
         U, V = inputs.lowrank_factors(d_out, d_in, r, seed)
         U64 = torch.from_numpy(U).to(dev)
@@ -400,11 +400,38 @@ def cpu_baseline(wl, M_full, budget_s=10.0):
     t0 = time.perf_counter()
     oracle.pifa_forward(X[:rows], piv, npiv, Wp, C, d_out=d_out, threads=threads)
     dt = time.perf_counter() - t0
+    # one thread, on a sample sized from the threaded rate (about 3 s)
+    rows1 = int(min(M_full, max(4, rows * 3.0 / (dt * threads))))
+    t0 = time.perf_counter()
+    oracle.pifa_forward(X[:rows1], piv, npiv, Wp, C, d_out=d_out, threads=1)
+    dt1 = time.perf_counter() - t0
+    # the oracle's build (QRCP + coefficient solve) of the same W' = U V
+    U, V = inputs.lowrank_factors(d_out, d_in, r, wl.seed)
+    W = U @ V
+    del U, V
+    t0 = time.perf_counter()
+    b = oracle.build_pifa(W, r, threads=threads)
+    build_s = time.perf_counter() - t0
+    same_pivots = bool(np.array_equal(np.asarray(b["pivot_idx"]), np.asarray(piv)))
+    del W, b
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
+    except OSError:
+        pass
     return {"value": pifa_flops(rows, d_in, d_out, r) / dt / 1e12, "unit": "TFLOP/s", "cores": threads,
             "kind": "oracle",
             "sample": "fp64 PIFA forward of the same 4096x4096 r=2048 layer on %d of %d activation rows "
                       "(%.1f s, %d OpenMP threads; rows are independent, so throughput scales to the batch)"
-                      % (rows, M_full, dt, threads)}
+                      % (rows, M_full, dt, threads),
+            "single_thread": {"value": pifa_flops(rows1, d_in, d_out, r) / dt1 / 1e12, "unit": "TFLOP/s",
+                              "sample": "%d rows, %.1f s" % (rows1, dt1)},
+            "build_s": build_s,
+            "build": "oracle QRCP + coefficient solve of the 4096x4096 rank-2048 W' (fp64, %d threads); "
+                     "pivot set identical to the GPU build: %s" % (threads, same_pivots),
+            "cpu_model": model, "nproc": os.cpu_count(),
+            "affinity": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else None}
 
 
 def traffic_from_profiles(kernel: str):
@@ -432,10 +459,14 @@ def main():
     ap.add_argument("--full", action="store_true", help="also sweep every configuration")
     ap.add_argument("--out", default=os.path.join(ROOT, "gpurun_out", "bench_full.json"))
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--profile-m", type=int, default=4096,
+                    help="with --profile-run: activation rows of the profiled forward (1..4096)")
     ap.add_argument("--profile-run", action="store_true",
                     help="only the headline forward (warmup, then steps) plus one calibration copy of 512 MiB "
                          "(for rocprofv3 runs)")
     args = ap.parse_args()
+    if not 1 <= args.profile_m <= 4096:
+        ap.error("--profile-m must be in 1..4096")
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only (run with --gpus 1): sharding the PIFA layer over "
               "several GPUs is not implemented.", file=sys.stderr)
@@ -465,6 +496,11 @@ def main():
         dst = torch.empty_like(src)
         dst.copy_(src)
         torch.cuda.synchronize()
+        if args.profile_m != M:  # the same layer at another batch size
+            M = args.profile_m
+            x = x[:M].contiguous()
+            y = torch.empty((M, d_out), dtype=torch.bfloat16, device="cuda:0")
+            pifa.pifa_layer_reserve(h, M)
         for _ in range(args.warmup):
             pifa.pifa_forward(h, x, y, M, stream)
         torch.cuda.synchronize()

@@ -4,8 +4,12 @@
     python -m paper_2501_19090_amd.profile_summary traffic <fetch_dir> <write_dir> <kernel-substring>
            <launch-name> <out.txt> <command...>
     python -m paper_2501_19090_amd.profile_summary steady <kernel_trace.csv> <N> <out.md> <kernel-substring>...
+    python -m paper_2501_19090_amd.profile_summary counters <out.md> <title> <command> <dir> <kernel-substring>...
 
 `stats` turns a --kernel-trace --stats CSV into a short markdown table.
+`counters` appends to <out.md> a table of every counter a --pmc pass in <dir>
+collected, averaged over the dispatches of each kernel whose name contains a
+given substring.
 `steady` appends to <out.md> the average duration of the last N dispatches
 of each kernel whose name contains a given substring (the timed steps that
 follow the warm-up, as bench.py times them).
@@ -63,6 +67,48 @@ def steady(trace_csv: str, n: int, out_md: str, subs) -> None:
         f.write("\n".join(lines) + "\n")
 
 
+def counters(out_md: str, title: str, command: str, dirname: str, subs) -> None:
+    files = glob.glob(os.path.join(dirname, "**", "*counter_collection.csv"), recursive=True)
+    rows = [r for fn in files for r in csv.DictReader(open(fn))]
+    names = sorted({r["Counter_Name"] for r in rows})
+    # FETCH_SIZE / WRITE_SIZE (KiB) also as MB scaled by the calibration copy
+    scale = {}
+    for n in ("FETCH_SIZE", "WRITE_SIZE"):
+        cv = [float(r["Counter_Value"]) for r in rows if r["Counter_Name"] == n and _is_copy(r["Kernel_Name"])]
+        if n in names and cv:
+            scale[n] = COPY_BYTES / (max(cv) * 1024.0)
+    cols = names + ["%s MB" % n for n in names if n in scale] + ["avg us"]
+    lines = ["", "## " + title, "", "Command (run from the repository root on the GPU host):", "", "```", command,
+             "```", "", "| kernel | dispatches | " + " | ".join(cols) + " |",
+             "|---|---:|" + "---:|" * len(cols)]
+    for sub in subs:
+        sel = [r for r in rows if sub in r["Kernel_Name"]]
+        if not sel:
+            continue
+        disp = len({r.get("Dispatch_Id", r.get("Correlation_Id", i)) for i, r in enumerate(sel)})
+        avg = {}
+        for n in names:
+            v = [float(r["Counter_Value"]) for r in sel if r["Counter_Name"] == n]
+            avg[n] = sum(v) / len(v) if v else None
+        vals = ["%.4g" % avg[n] if avg[n] is not None else "" for n in names]
+        vals += ["%.2f" % (avg[n] * 1024.0 * scale[n] / 1e6) for n in names if n in scale]
+        dur = {r.get("Dispatch_Id", i): int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for i, r in enumerate(sel)}
+        vals.append("%.2f" % (sum(dur.values()) / len(dur) / 1e3))
+        lines.append("| `%s` | %d | %s |" % (_short(sub), disp, " | ".join(vals)))
+    if scale:
+        lines.append("")
+        lines.append("MB columns: the KiB counts times %s, the factors that map the counters of the run's "
+                     "%d MiB device copy to its true bytes." % (
+                         ", ".join("%s %.4f" % (n, f) for n, f in scale.items()), COPY_BYTES >> 20))
+    lines.append("avg us: dispatch durations under counter collection (slower than unprofiled runs).")
+    with open(out_md, "a") as f:
+        f.write("\n".join(lines) + "\n")
+
+
+def _is_copy(name: str) -> bool:
+    return "copyBuffer" in name or ("elementwise_kernel" in name and "copy" in name)
+
+
 def _counter(dirname: str, counter: str):
     files = glob.glob(os.path.join(dirname, "**", "*counter_collection.csv"), recursive=True)
     out = []
@@ -83,7 +129,7 @@ def traffic(fetch_dir, write_dir, kernel_sub, launch_name, out_txt, command):
     write = _counter(write_dir, "WRITE_SIZE")
     k_fetch, nf = _avg(fetch, lambda n: kernel_sub in n)
     k_write, nw = _avg(write, lambda n: kernel_sub in n)
-    is_copy = lambda n: "copyBuffer" in n or "elementwise_kernel" in n and "copy" in n
+    is_copy = _is_copy
     # the calibration copy is the largest copy dispatch in the run
     c_fetch = max((x for n, x in fetch if is_copy(n)), default=None)
     c_write = max((x for n, x in write if is_copy(n)), default=None)
@@ -111,6 +157,8 @@ if __name__ == "__main__":
     mode = sys.argv[1]
     if mode == "stats":
         stats(sys.argv[2], sys.argv[3], " ".join(sys.argv[4:]))
+    elif mode == "counters":
+        counters(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5], sys.argv[6:])
     elif mode == "steady":
         steady(sys.argv[2], int(sys.argv[3]), sys.argv[4], sys.argv[5:])
     elif mode == "traffic":
