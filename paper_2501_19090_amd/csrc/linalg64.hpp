@@ -99,90 +99,187 @@ __global__ __launch_bounds__(256) void pivot_floor64(const double* __restrict__ 
 
 // Unblocked Cholesky of the nb x nb (nb <= 64) block at A (row stride ld), in
 // place (lower triangle; the upper part is left as is).  One workgroup of 256
-// threads, block staged in LDS.  *info is set to 1 on a pivot that is not
-// finite or not above *floor (the matrix is not numerically positive definite).
+// threads, block staged in LDS; thread (ty, tx) of a 16 x 16 grid owns rows
+// ty + 16a and columns tx + 16b (a, b < 4) of the trailing update, so no
+// index is divided.  Step j: every thread reads the pivot and the column
+// values it needs, a barrier, then the scaled column and the rank-1 update
+// are written.  *info is set to 1 on a pivot that is not finite or not above
+// *floor (the matrix is not numerically positive definite).
 __global__ __launch_bounds__(256) void chol_diag(double* __restrict__ A, int64_t ld, int nb,
                                                  const double* __restrict__ floor, int* __restrict__ info) {
     __shared__ double L[kG64][kG64 + 1];
-    const int tid = threadIdx.x;
-    for (int e = tid; e < nb * nb; e += 256) L[e / nb][e % nb] = A[(int64_t)(e / nb) * ld + e % nb];
+    const int tid = threadIdx.x, tx = tid % 16, ty = tid / 16;
+    {  // thread t loads column t % 64 of rows t / 64 + 4 k: 16 independent loads
+        const int c = tid % kG64, r0 = tid / kG64;
+#pragma unroll
+        for (int k = 0; k < kG64 / 4; ++k) {
+            const int i = r0 + 4 * k;
+            if (i < nb && c < nb) L[i][c] = A[(int64_t)i * ld + c];
+        }
+    }
     __syncthreads();
     const double fl = *floor;
     for (int j = 0; j < nb; ++j) {
         const double d = L[j][j];
         const bool ok = d > fl && d > 0.0 && __builtin_isfinite(d);
         const double s = ok ? sqrt(d) : 1.0;
+        const double inv = 1.0 / s;  // one division per step; the column is scaled by multiplication
+        double li[4], lc[4];
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+            li[a] = L[ty + 16 * a][j] * inv;
+            lc[a] = L[tx + 16 * a][j] * inv;
+        }
+        const double cj = tid > j && tid < nb ? L[tid][j] * inv : 0.0;
         __syncthreads();
         if (tid == 0) {
             L[j][j] = s;
             if (!ok) *info = 1;
         }
-        for (int i = j + 1 + tid; i < nb; i += 256) L[i][j] /= s;
-        __syncthreads();
-        // trailing update of the lower triangle
-        const int w = nb - j - 1;
-        for (int e = tid; e < w * w; e += 256) {
-            const int i = j + 1 + e / w, c = j + 1 + e % w;
-            if (c <= i) L[i][c] -= L[i][j] * L[c][j];
-        }
+        if (tid > j && tid < nb) L[tid][j] = cj;
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+                const int i = ty + 16 * a, c = tx + 16 * b;
+                if (c > j && c <= i && i < nb) L[i][c] -= li[a] * lc[b];
+            }
         __syncthreads();
     }
-    for (int e = tid; e < nb * nb; e += 256) {
-        const int i = e / nb, c = e % nb;
-        if (c <= i) A[(int64_t)i * ld + c] = L[i][c];
+    {
+        const int c = tid % kG64, r0 = tid / kG64;
+#pragma unroll
+        for (int k = 0; k < kG64 / 4; ++k) {
+            const int i = r0 + 4 * k;
+            if (i < nb && c <= i) A[(int64_t)i * ld + c] = L[i][c];
+        }
+    }
+}
+
+// Loads the nb x nb block at Ld (row stride ld) into L and the reciprocals
+// of its diagonal into inv (a workgroup of one wave; the caller
+// synchronises).
+template <int NB>
+__device__ __forceinline__ void load_lower_block(const double* __restrict__ Ld, int64_t ld, int nb,
+                                                 double (&L)[NB][NB + 1], double (&inv)[NB]) {
+    static_assert(NB == kWave, "one column per lane of a one-wave workgroup");
+    // lane t loads column t: NB independent, coalesced loads in flight at once
+    const int t = threadIdx.x;
+#pragma unroll
+    for (int i = 0; i < NB; ++i)
+        if (i < nb && t < nb) L[i][t] = Ld[(int64_t)i * ld + t];
+    if (t < nb) inv[t] = 1.0 / Ld[(int64_t)t * ld + t];
+}
+
+// Forward substitution x <- L^-1 x for the nb x nb lower factor in LDS, x
+// in registers (64 entries, those >= nb unused): column by column, so the
+// updates of one step are independent of one another and the LDS reads of
+// the column pipeline instead of each waiting for the previous product.
+// inv holds the reciprocals of L's diagonal.
+// A full block (nb == NB) takes a branch-free, fully unrolled path; a
+// partial one (the last block of a matrix whose size is not a multiple of 64)
+// an ordinary loop.
+template <int NB>
+__device__ __forceinline__ void lower_solve_regs(const double (&L)[NB][NB + 1], const double (&inv)[NB], int nb,
+                                                 double (&x)[NB]) {
+    if (nb == NB) {
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+            x[j] = x[j] * inv[j];
+#pragma unroll
+            for (int i = j + 1; i < NB; ++i) x[i] -= L[i][j] * x[j];
+        }
+    } else {
+        double y[NB];
+#pragma unroll
+        for (int i = 0; i < NB; ++i) y[i] = x[i];
+        for (int j = 0; j < nb; ++j) {
+            double xj = 0.0;
+#pragma unroll
+            for (int i = 0; i < NB; ++i)
+                if (i == j) xj = y[i] * inv[j];
+#pragma unroll
+            for (int i = 0; i < NB; ++i) {
+                if (i == j) y[i] = xj;
+                else if (i > j && i < nb) y[i] -= L[i][j] * xj;
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < NB; ++i) x[i] = y[i];
+    }
+}
+
+// Backward substitution x <- L^-T x (same conventions as lower_solve_regs).
+template <int NB>
+__device__ __forceinline__ void lower_t_solve_regs(const double (&L)[NB][NB + 1], const double (&inv)[NB], int nb,
+                                                   double (&x)[NB]) {
+    if (nb == NB) {
+#pragma unroll
+        for (int j = NB - 1; j >= 0; --j) {
+            x[j] = x[j] * inv[j];
+#pragma unroll
+            for (int i = 0; i < j; ++i) x[i] -= L[j][i] * x[j];
+        }
+    } else {
+        for (int j = nb - 1; j >= 0; --j) {
+            double xj = 0.0;
+#pragma unroll
+            for (int i = 0; i < NB; ++i)
+                if (i == j) xj = x[i] * inv[j];
+#pragma unroll
+            for (int i = 0; i < NB; ++i) {
+                if (i == j) x[i] = xj;
+                else if (i < j) x[i] -= L[j][i] * xj;
+            }
+        }
     }
 }
 
 // Panel of a blocked Cholesky: rows [0, nrows) of P (row stride ld, nb
 // columns) become P L11^-T, L11 being the nb x nb lower factor at Ld (row
-// stride ld).  One row per thread, 64 rows per workgroup.
+// stride ld): row p solves L11 x = p^T.  One row per thread, in registers.
 __global__ __launch_bounds__(64) void chol_panel(const double* __restrict__ Ld, double* __restrict__ P, int64_t ld,
                                                  int nb, int64_t nrows) {
     __shared__ double L[kG64][kG64 + 1];
-    for (int e = threadIdx.x; e < nb * nb; e += 64) L[e / nb][e % nb] = Ld[(int64_t)(e / nb) * ld + e % nb];
+    __shared__ double inv[kG64];
+    load_lower_block<kG64>(Ld, ld, nb, L, inv);
     __syncthreads();
-    __shared__ double X[64][kG64 + 1];  // each thread's row, in LDS rather than scratch
     const int64_t row = (int64_t)blockIdx.x * 64 + threadIdx.x;
     if (row >= nrows) return;
-    double* x = X[threadIdx.x];
     double* p = P + row * ld;
-    for (int j = 0; j < nb; ++j) {
-        double v = p[j];
-        for (int t = 0; t < j; ++t) v -= x[t] * L[j][t];
-        x[j] = v / L[j][j];
-    }
-    for (int j = 0; j < nb; ++j) p[j] = x[j];
+    double x[kG64];
+#pragma unroll
+    for (int j = 0; j < kG64; ++j) x[j] = j < nb ? p[j] : 0.0;
+    lower_solve_regs<kG64>(L, inv, nb, x);
+#pragma unroll
+    for (int j = 0; j < kG64; ++j)
+        if (j < nb) p[j] = x[j];
 }
 
 // Triangular solve of one diagonal block for many right-hand sides: the nb
 // rows at B (row stride ldb, nrhs columns) become L11^-1 B (forward, TRANS =
 // 0) or L11^-T B (backward, TRANS = 1), L11 at Ld (row stride ld).  One
-// right-hand side per thread, 64 per workgroup.
+// right-hand side per thread, in registers, column by column as in
+// lower_solve_regs.
 template <int TRANS>
 __global__ __launch_bounds__(64) void trsm_diag(const double* __restrict__ Ld, int64_t ld, int nb,
                                                 double* __restrict__ B, int64_t ldb, int64_t nrhs) {
     __shared__ double L[kG64][kG64 + 1];
-    for (int e = threadIdx.x; e < nb * nb; e += 64) L[e / nb][e % nb] = Ld[(int64_t)(e / nb) * ld + e % nb];
+    __shared__ double inv[kG64];
+    load_lower_block<kG64>(Ld, ld, nb, L, inv);
     __syncthreads();
-    __shared__ double X[64][kG64 + 1];  // each thread's right-hand side
     const int64_t c = (int64_t)blockIdx.x * 64 + threadIdx.x;
     if (c >= nrhs) return;
-    double* x = X[threadIdx.x];
-    for (int j = 0; j < nb; ++j) x[j] = B[(int64_t)j * ldb + c];
-    if (TRANS == 0) {
-        for (int j = 0; j < nb; ++j) {
-            double v = x[j];
-            for (int t = 0; t < j; ++t) v -= L[j][t] * x[t];
-            x[j] = v / L[j][j];
-        }
-    } else {
-        for (int j = nb - 1; j >= 0; --j) {
-            double v = x[j];
-            for (int t = j + 1; t < nb; ++t) v -= L[t][j] * x[t];
-            x[j] = v / L[j][j];
-        }
-    }
-    for (int j = 0; j < nb; ++j) B[(int64_t)j * ldb + c] = x[j];
+    double x[kG64];
+#pragma unroll
+    for (int j = 0; j < kG64; ++j) x[j] = j < nb ? B[(int64_t)j * ldb + c] : 0.0;
+    if (TRANS == 0)
+        lower_solve_regs<kG64>(L, inv, nb, x);
+    else  // L^T x = b: last row first; column j of L^T is row j of L
+        lower_t_solve_regs<kG64>(L, inv, nb, x);
+#pragma unroll
+    for (int j = 0; j < kG64; ++j)
+        if (j < nb) B[(int64_t)j * ldb + c] = x[j];
 }
 
 // out = a * X + b * Y + d * I (n x n row-major; Y may be null, then b is ignored)
