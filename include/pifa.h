@@ -17,6 +17,9 @@
  *   - Matrices are dense, row-major, contiguous, with no padding between rows.
  *   - "device" pointers are HIP device memory on the current device;
  *     "host" pointers are ordinary host memory.
+ *   - A handle belongs to the device that was current when it was created;
+ *     every call taking it returns PIFA_ERR_WRONG_DEVICE if another device
+ *     is current (destroy calls excepted).
  *   - Element type is given by a pifa_dtype: PIFA_BF16 (bfloat16 storage,
  *     fp32 accumulation) or PIFA_F32.  X, Y and the weights share the dtype.
  *   - bf16 requires d_in to be a multiple of 8 (16-byte rows); f32 accepts
@@ -44,14 +47,16 @@ typedef enum {
     PIFA_ERR_INVALID_ARG = -1, /* null pointer, bad size or dtype        */
     PIFA_ERR_BAD_INDEX = -2,   /* index out of range, duplicate, or the  */
                                /* two sets do not partition [0, d_out)   */
-    PIFA_ERR_UNSUPPORTED = -3, /* a shape or alignment this build lacks  */
+    PIFA_ERR_UNSUPPORTED = -3, /* a shape or alignment the kernels lack  */
     PIFA_ERR_HIP = -4,         /* a HIP runtime call or launch failed    */
     PIFA_ERR_OOM = -5,         /* device memory allocation failed        */
     PIFA_ERR_NOT_RANK_R = -6,  /* pifa_build_f64: W' is not numerically  */
                                /* of rank r                              */
-    PIFA_ERR_NOT_SPD = -7      /* pifa_calib_reconstruct: a normal-      */
+    PIFA_ERR_NOT_SPD = -7,     /* pifa_calib_reconstruct: a normal-      */
                                /* equation matrix is not positive        */
                                /* definite (too few calibration rows)    */
+    PIFA_ERR_WRONG_DEVICE = -8 /* a handle used while another device is  */
+                               /* current than the one it was created on */
 } pifa_status;
 
 /* Layer shape: W is d_out x d_in with rank r, 1 <= r <= min(d_in, d_out)

@@ -48,6 +48,21 @@ constexpr int kSkinnyWaves = 8;
 
 inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// A handle's memory lives on the device current at its creation; launching
+// its kernels with another device current would touch that memory from the
+// wrong GPU, so such calls are refused.
+pifa_status check_device(int dev) {
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess) return PIFA_ERR_HIP;
+    return cur == dev ? PIFA_OK : PIFA_ERR_WRONG_DEVICE;
+}
+
+#define PIFA_ON_DEVICE(dev)                      \
+    do {                                         \
+        const pifa_status s_ = check_device(dev); \
+        if (s_ != PIFA_OK) return s_;            \
+    } while (0)
 inline size_t esize(pifa_dtype dt) { return dt == PIFA_BF16 ? 2 : 4; }
 inline bool valid_dtype(pifa_dtype dt) { return dt == PIFA_BF16 || dt == PIFA_F32; }
 
@@ -713,6 +728,7 @@ const char* pifa_status_string(pifa_status s) {
         case PIFA_ERR_OOM: return "PIFA_ERR_OOM";
         case PIFA_ERR_NOT_RANK_R: return "PIFA_ERR_NOT_RANK_R";
         case PIFA_ERR_NOT_SPD: return "PIFA_ERR_NOT_SPD";
+        case PIFA_ERR_WRONG_DEVICE: return "PIFA_ERR_WRONG_DEVICE";
     }
     return "PIFA_ERR_UNKNOWN";
 }
@@ -841,6 +857,7 @@ pifa_status pifa_layer_destroy(pifa_handle h) {
 
 pifa_status pifa_layer_reserve(pifa_handle h, int64_t max_M) {
     if (!h || max_M < 0) return PIFA_ERR_INVALID_ARG;
+    PIFA_ON_DEVICE(h->device);
     const size_t need = std::max(pifa_ws_bytes(h, max_M), pifa_ws_bytes(h, std::min<int64_t>(max_M, kDecodeMaxM)));
     pifa_status s = h->ws.ensure(need, 0);
     if (s != PIFA_OK) return s;
@@ -878,6 +895,7 @@ pifa_status pifa_forward(pifa_handle h, const void* X, void* Y, int64_t M, void*
     if (!h || M < 0) return PIFA_ERR_INVALID_ARG;
     if (M == 0) return PIFA_OK;
     if (!X || !Y) return PIFA_ERR_INVALID_ARG;
+    PIFA_ON_DEVICE(h->device);
     if (h->dtype == PIFA_BF16 && !aligned16(X)) return PIFA_ERR_UNSUPPORTED;
     hipStream_t st = as_stream(stream);
     pifa_status s = h->ws.ensure(pifa_ws_bytes(h, M), st);
@@ -995,6 +1013,7 @@ pifa_status dense_layer_forward(dense_handle h, const void* X, void* Y, int64_t 
     if (!h || M < 0) return PIFA_ERR_INVALID_ARG;
     if (M == 0) return PIFA_OK;
     if (!X || !Y) return PIFA_ERR_INVALID_ARG;
+    PIFA_ON_DEVICE(h->device);
     if (h->dtype == PIFA_BF16 && !aligned16(X)) return PIFA_ERR_UNSUPPORTED;
     hipStream_t st = as_stream(stream);
     pifa_status s = h->part.ensure(dense_part_bytes(h->dtype, M, h->d_in, h->d_out), st);
@@ -1006,6 +1025,7 @@ pifa_status dense_layer_forward(dense_handle h, const void* X, void* Y, int64_t 
 
 pifa_status dense_layer_reserve(dense_handle h, int64_t max_M) {
     if (!h || max_M < 0) return PIFA_ERR_INVALID_ARG;
+    PIFA_ON_DEVICE(h->device);
     size_t part = 0;
     for (int64_t m = kDecodeMaxM + 1; m <= max_M; m = m < 4096 ? m + 1 : m * 2)
         part = std::max(part, dense_part_bytes(h->dtype, std::min(m, max_M), h->d_in, h->d_out));
@@ -1090,6 +1110,7 @@ pifa_status lowrank_layer_create(const void* U, const void* V, pifa_dims dims, p
 
 pifa_status lowrank_layer_reserve(lowrank_handle h, int64_t max_M) {
     if (!h || max_M < 0) return PIFA_ERR_INVALID_ARG;
+    PIFA_ON_DEVICE(h->device);
     const size_t need = std::max(lowrank_ws_bytes(h->dtype, max_M, h->r_pad),
                                  lowrank_ws_bytes(h->dtype, std::min<int64_t>(max_M, kDecodeMaxM), h->r_pad));
     pifa_status s = h->ws.ensure(need, 0);
@@ -1106,6 +1127,7 @@ pifa_status lowrank_layer_forward(lowrank_handle h, const void* X, void* Y, int6
     if (!h || M < 0) return PIFA_ERR_INVALID_ARG;
     if (M == 0) return PIFA_OK;
     if (!X || !Y) return PIFA_ERR_INVALID_ARG;
+    PIFA_ON_DEVICE(h->device);
     if (h->dtype == PIFA_BF16 && !aligned16(X)) return PIFA_ERR_UNSUPPORTED;
     hipStream_t st = as_stream(stream);
     pifa_status s = h->ws.ensure(lowrank_ws_bytes(h->dtype, M, h->r_pad), st);
@@ -1190,6 +1212,7 @@ pifa_status pifa_layer_backward(pifa_handle h, const void* X, const void* Y, con
                                 void* dX, float* dW_p, float* dC, void* stream) {
     if (!h || M < 0) return PIFA_ERR_INVALID_ARG;
     if (h->dtype != PIFA_BF16) return PIFA_ERR_UNSUPPORTED;
+    PIFA_ON_DEVICE(h->device);
     hipStream_t st = as_stream(stream);
     const int64_t r = h->r, n_np = h->n_np, d_in = h->d_in, d_out = h->d_out, r_pad = h->r_pad;
     if (M == 0) {  // the gradient of an empty batch
@@ -1394,6 +1417,7 @@ pifa_status pifa_calib_destroy(pifa_calib_handle c) {
 
 pifa_status pifa_calib_reset(pifa_calib_handle c, void* stream) {
     if (!c) return PIFA_ERR_INVALID_ARG;
+    PIFA_ON_DEVICE(c->device);
     const size_t b = (size_t)c->n * c->n * sizeof(double);
     PIFA_HIP(hipMemsetAsync(c->S, 0, b, as_stream(stream)));
     PIFA_HIP(hipMemsetAsync(c->P, 0, b, as_stream(stream)));
@@ -1404,6 +1428,7 @@ pifa_status pifa_calib_accumulate(pifa_calib_handle c, const void* X_o, const vo
     if (!c || B < 0) return PIFA_ERR_INVALID_ARG;
     if (B == 0) return PIFA_OK;
     if (!X_o || !X_u) return PIFA_ERR_INVALID_ARG;
+    PIFA_ON_DEVICE(c->device);
     hipStream_t st = as_stream(stream);
     const int64_t n = c->n, Bp = round_up(B, (int64_t)8);
     const int64_t e_t = align_elems(n * Bp);
@@ -1434,6 +1459,7 @@ pifa_status pifa_calib_accumulate(pifa_calib_handle c, const void* X_o, const vo
 
 pifa_status pifa_calib_read(pifa_calib_handle c, double* S, double* P, void* stream) {
     if (!c) return PIFA_ERR_INVALID_ARG;
+    PIFA_ON_DEVICE(c->device);
     const size_t b = (size_t)c->n * c->n * sizeof(double);
     if (S) {
         hipLaunchKernelGGL(symmetrize_lower64, dim3(grid_for(c->n * c->n)), dim3(256), 0, as_stream(stream), c->S, c->n);
@@ -1447,6 +1473,7 @@ pifa_status pifa_calib_read(pifa_calib_handle c, double* S, double* P, void* str
 pifa_status pifa_calib_reconstruct(pifa_calib_handle c, const double* W, int64_t d_out, const double* Vt, int64_t r,
                                    double lam, double alpha, double* U_r, double* Vt_r, void* stream) {
     if (!c || !W || !Vt || !U_r || !Vt_r || d_out < 1 || r < 1) return PIFA_ERR_INVALID_ARG;
+    PIFA_ON_DEVICE(c->device);
     const int64_t n = c->n, m = d_out;
     if (r > n || r > m) return PIFA_ERR_INVALID_ARG;
     hipStream_t st = as_stream(stream);
@@ -1586,6 +1613,7 @@ pifa_status pifa_group_destroy(pifa_group_handle g) {
 
 pifa_status pifa_group_reserve(pifa_group_handle g, int64_t max_M) {
     if (!g || max_M < 0) return PIFA_ERR_INVALID_ARG;
+    PIFA_ON_DEVICE(g->device);
     pifa_status s = g->ws.ensure(std::max(group_ws_bytes(g, max_M),
                                           group_ws_bytes(g, std::min<int64_t>(max_M, kDecodeMaxM))), 0);
     if (s != PIFA_OK) return s;
@@ -1623,6 +1651,7 @@ pifa_status pifa_group_forward(pifa_group_handle g, const void* X, void* Y, int6
     if (!g || M < 0) return PIFA_ERR_INVALID_ARG;
     if (M == 0) return PIFA_OK;
     if (!X || !Y) return PIFA_ERR_INVALID_ARG;
+    PIFA_ON_DEVICE(g->device);
     if (!aligned16(X)) return PIFA_ERR_UNSUPPORTED;
     hipStream_t st = as_stream(stream);
     pifa_status s = g->ws.ensure(group_ws_bytes(g, M), st);

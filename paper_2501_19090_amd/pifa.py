@@ -29,6 +29,7 @@ PIFA_ERR_HIP = -4
 PIFA_ERR_OOM = -5
 PIFA_ERR_NOT_RANK_R = -6
 PIFA_ERR_NOT_SPD = -7
+PIFA_ERR_WRONG_DEVICE = -8
 
 
 class pifa_dims(ctypes.Structure):

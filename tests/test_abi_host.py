@@ -129,6 +129,7 @@ def test_forward_and_baselines_reject_bad_args():
 def test_status_strings_of_build_and_reconstruction():
     assert pifa.pifa_status_string(pifa.PIFA_ERR_NOT_RANK_R) == "PIFA_ERR_NOT_RANK_R"
     assert pifa.pifa_status_string(pifa.PIFA_ERR_NOT_SPD) == "PIFA_ERR_NOT_SPD"
+    assert pifa.pifa_status_string(pifa.PIFA_ERR_WRONG_DEVICE) == "PIFA_ERR_WRONG_DEVICE"
 
 
 def test_group_backward_and_calibration_reject_bad_args_on_host():
