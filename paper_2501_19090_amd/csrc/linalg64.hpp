@@ -4,78 +4,124 @@
 // the accumulation of the calibration sums, which runs on the MFMA GEMM.
 //
 //   gemm64        C = alpha op(A) op(B) + beta C with arbitrary element strides
-//                 (transposes are strides, no copies); optional lower-triangle
-//                 tiles only, for symmetric updates.
+//                 (transposes are strides, no copies) on fp64 MFMA tiles;
+//                 optional lower-triangle tiles only, for symmetric updates.
 //   Cholesky      A = L L^T, right-looking in 64-column blocks: diagonal block
 //                 in one workgroup's LDS, panel by forward substitution, trailing
 //                 update by gemm64 (lower tiles only).
 //   spd solve     L L^T X = B for many right-hand sides: blocked forward and
-//                 backward substitution with gemm64 updates.
+//                 backward substitution; each diagonal block is applied as its
+//                 explicit inverse (tri_inv_blocks), so every step is a gemm64.
 #pragma once
 
 #include "common.hpp"
 
 namespace pifa {
 
-constexpr int kG64 = 64;  // output tile
-constexpr int kG64K = 16; // K step
+constexpr int kG64 = 64;  // block size of the factorisations and solves
+
+typedef double f64x4 __attribute__((ext_vector_type(4)));
 
 // C[i*sc0 + j*sc1] = alpha * sum_k A[i*sa0 + k*sa1] * B[k*sb0 + j*sb1] + beta * C[...]
-// for i < Mr, j < Nc.  LOWER: only tiles whose first row >= first column
-// (tiles on the diagonal are computed whole).  beta == 0 ignores C's old value.
-// Grid: (ceil(Nc / 64), ceil(Mr / 64)), 256 threads, 4 x 4 outputs each.
-__global__ __launch_bounds__(256) void gemm64(int64_t Mr, int64_t Nc, int64_t K, double alpha, const double* __restrict__ A,
-                                              int64_t sa0, int64_t sa1, const double* __restrict__ B, int64_t sb0,
-                                              int64_t sb1, double beta, double* __restrict__ C, int64_t sc0, int64_t sc1,
-                                              int lower) {
-    const int64_t i0 = (int64_t)blockIdx.y * kG64, j0 = (int64_t)blockIdx.x * kG64;
+// for i < Mr, j < Nc, on v_mfma_f64_16x16x4_f64.  LOWER: only tiles whose
+// first row >= first column (tiles on the diagonal are computed whole).
+// beta == 0 ignores C's old value.
+// Tile BT x BT, K step BK, 16 waves in a 4 x 4 grid (1024 threads), each a
+// (BT/4) x (BT/4) block of 16 x 16 MFMA outputs.  Both operands are staged
+// k-major in LDS ([k][i] and [k][j]), so any stride pattern loads with the
+// unit-stride axis across consecutive threads and every fragment read is
+// unit-stride.  MFMA lane layout: lane l supplies A[l % 16][l / 16] and
+// B[l / 16][l % 16]; element v of the result is D[4 v + l / 16][l % 16].
+// Each output is one fp64 FMA chain over k in ascending order.
+// Grid: (ceil(Nc / BT), ceil(Mr / BT)).
+template <int BT, int BK>
+__global__ __launch_bounds__(1024) void gemm64(int64_t Mr, int64_t Nc, int64_t K, double alpha,
+                                               const double* __restrict__ A, int64_t sa0, int64_t sa1,
+                                               const double* __restrict__ B, int64_t sb0, int64_t sb1, double beta,
+                                               double* __restrict__ C, int64_t sc0, int64_t sc1, int lower) {
+    constexpr int NT = 1024, LD = BT + 1, PT = BT * BK / NT;
+    constexpr int WT = BT / 4, TT = WT / 16;
+    static_assert(PT >= 1 && BT * BK % NT == 0 && WT % 16 == 0 && BK % 4 == 0, "bad fp64 tile");
+    const int64_t i0 = (int64_t)blockIdx.y * BT, j0 = (int64_t)blockIdx.x * BT;
     if (lower && j0 > i0) return;
-    __shared__ double As[kG64K][kG64 + 1];
-    __shared__ double Bs[kG64K][kG64 + 1];
-    const int tid = threadIdx.x, tx = tid % 16, ty = tid / 16;
-    double acc[4][4] = {};
-    for (int64_t k0 = 0; k0 < K; k0 += kG64K) {
-        // 64 x 16 tile of A and 16 x 64 tile of B; consecutive threads walk the unit-stride axis
+    __shared__ double As[2][BK * LD];
+    __shared__ double Bs[2][BK * LD];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 2, wn = wave & 3;
+    const bool a_k1 = sa1 == 1, b_j1 = sb1 == 1;
+    // element e of a staged tile: (row ii, depth kk) of A, (depth kb, column jj) of B
+    auto a_at = [&](int e, int& ii, int& kk) {
+        ii = a_k1 ? e / BK : e % BT;
+        kk = a_k1 ? e % BK : e / BT;
+    };
+    auto b_at = [&](int e, int& kb, int& jj) {
+        jj = b_j1 ? e % BT : e / BK;
+        kb = b_j1 ? e / BT : e % BK;
+    };
+    double ra[PT], rb[PT];
+    auto gload = [&](int64_t k0) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int e = tid + 256 * q;
-            int ii, kk;
-            if (sa1 == 1) { ii = e / kG64K; kk = e % kG64K; }
-            else { kk = e / kG64; ii = e % kG64; }
-            const int64_t i = i0 + ii, k = k0 + kk;
-            As[kk][ii] = (i < Mr && k < K) ? A[i * sa0 + k * sa1] : 0.0;
-            int jj, kb;
-            if (sb1 == 1) { kb = e / kG64; jj = e % kG64; }
-            else { jj = e / kG64K; kb = e % kG64K; }
-            const int64_t j = j0 + jj, kB = k0 + kb;
-            Bs[kb][jj] = (j < Nc && kB < K) ? B[kB * sb0 + j * sb1] : 0.0;
+        for (int q = 0; q < PT; ++q) {
+            int ii, kk, kb, jj;
+            a_at(tid + NT * q, ii, kk);
+            b_at(tid + NT * q, kb, jj);
+            const int64_t i = i0 + ii, ka = k0 + kk, j = j0 + jj, kB = k0 + kb;
+            ra[q] = (i < Mr && ka < K) ? A[i * sa0 + ka * sa1] : 0.0;
+            rb[q] = (j < Nc && kB < K) ? B[kB * sb0 + j * sb1] : 0.0;
         }
-        __syncthreads();
+    };
+    auto sstore = [&](int buf) {
 #pragma unroll
-        for (int kk = 0; kk < kG64K; ++kk) {
-            double a[4], b[4];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                a[u] = As[kk][ty + 16 * u];
-                b[u] = Bs[kk][tx + 16 * u];
-            }
-#pragma unroll
-            for (int u = 0; u < 4; ++u)
-#pragma unroll
-                for (int v = 0; v < 4; ++v) acc[u][v] = fma(a[u], b[v], acc[u][v]);
+        for (int q = 0; q < PT; ++q) {
+            int ii, kk, kb, jj;
+            a_at(tid + NT * q, ii, kk);
+            b_at(tid + NT * q, kb, jj);
+            As[buf][kk * LD + ii] = ra[q];
+            Bs[buf][kb * LD + jj] = rb[q];
         }
+    };
+    f64x4 acc[TT][TT];
+#pragma unroll
+    for (int a = 0; a < TT; ++a)
+#pragma unroll
+        for (int b = 0; b < TT; ++b) acc[a][b] = f64x4{0.0, 0.0, 0.0, 0.0};
+    const int64_t nk = (K + BK - 1) / BK;
+    gload(0);
+    sstore(0);
+    __syncthreads();
+    const int fr = lane & 15, fk = lane >> 4;
+    for (int64_t kt = 0; kt < nk; ++kt) {
+        const int cur = (int)(kt & 1);
+        if (kt + 1 < nk) gload((kt + 1) * BK);  // in flight during this tile's MFMAs
+#pragma unroll
+        for (int s = 0; s < BK / 4; ++s) {
+            double fa[TT], fb[TT];
+#pragma unroll
+            for (int a = 0; a < TT; ++a) fa[a] = As[cur][(s * 4 + fk) * LD + wm * WT + a * 16 + fr];
+#pragma unroll
+            for (int b = 0; b < TT; ++b) fb[b] = Bs[cur][(s * 4 + fk) * LD + wn * WT + b * 16 + fr];
+#pragma unroll
+            for (int a = 0; a < TT; ++a)
+#pragma unroll
+                for (int b = 0; b < TT; ++b)
+                    acc[a][b] = __builtin_amdgcn_mfma_f64_16x16x4f64(fa[a], fb[b], acc[a][b], 0, 0, 0);
+        }
+        // the other buffer was last read before the previous barrier
+        if (kt + 1 < nk) sstore(cur ^ 1);
         __syncthreads();
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+    for (int a = 0; a < TT; ++a)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int64_t i = i0 + ty + 16 * u, j = j0 + tx + 16 * v;
-            if (i < Mr && j < Nc) {
-                double* c = C + i * sc0 + j * sc1;
-                *c = beta == 0.0 ? alpha * acc[u][v] : fma(alpha, acc[u][v], beta * *c);
+        for (int b = 0; b < TT; ++b)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int64_t i = i0 + wm * WT + a * 16 + 4 * v + fk, j = j0 + wn * WT + b * 16 + fr;
+                if (i < Mr && j < Nc) {
+                    double* c = C + i * sc0 + j * sc1;
+                    *c = beta == 0.0 ? alpha * acc[a][b][v] : fma(alpha, acc[a][b][v], beta * *c);
+                }
             }
-        }
 }
 
 // *out = 1e-13 * max_i A[i][i] (n x n, row stride ld): the smallest pivot a
@@ -209,32 +255,6 @@ __device__ __forceinline__ void lower_solve_regs(const double (&L)[NB][NB + 1], 
     }
 }
 
-// Backward substitution x <- L^-T x (same conventions as lower_solve_regs).
-template <int NB>
-__device__ __forceinline__ void lower_t_solve_regs(const double (&L)[NB][NB + 1], const double (&inv)[NB], int nb,
-                                                   double (&x)[NB]) {
-    if (nb == NB) {
-#pragma unroll
-        for (int j = NB - 1; j >= 0; --j) {
-            x[j] = x[j] * inv[j];
-#pragma unroll
-            for (int i = 0; i < j; ++i) x[i] -= L[j][i] * x[j];
-        }
-    } else {
-        for (int j = nb - 1; j >= 0; --j) {
-            double xj = 0.0;
-#pragma unroll
-            for (int i = 0; i < NB; ++i)
-                if (i == j) xj = x[i] * inv[j];
-#pragma unroll
-            for (int i = 0; i < NB; ++i) {
-                if (i == j) x[i] = xj;
-                else if (i < j) x[i] -= L[j][i] * xj;
-            }
-        }
-    }
-}
-
 // Panel of a blocked Cholesky: rows [0, nrows) of P (row stride ld, nb
 // columns) become P L11^-T, L11 being the nb x nb lower factor at Ld (row
 // stride ld): row p solves L11 x = p^T.  One row per thread, in registers.
@@ -256,30 +276,27 @@ __global__ __launch_bounds__(64) void chol_panel(const double* __restrict__ Ld, 
         if (j < nb) p[j] = x[j];
 }
 
-// Triangular solve of one diagonal block for many right-hand sides: the nb
-// rows at B (row stride ldb, nrhs columns) become L11^-1 B (forward, TRANS =
-// 0) or L11^-T B (backward, TRANS = 1), L11 at Ld (row stride ld).  One
-// right-hand side per thread, in registers, column by column as in
-// lower_solve_regs.
-template <int TRANS>
-__global__ __launch_bounds__(64) void trsm_diag(const double* __restrict__ Ld, int64_t ld, int nb,
-                                                double* __restrict__ B, int64_t ldb, int64_t nrhs) {
-    __shared__ double L[kG64][kG64 + 1];
+// Inverses of the diagonal blocks of a lower factor: block b (rows and
+// columns [64 b, 64 b + nb)) of the n x n factor L (row stride ld) goes to
+// Linv[b * 64 * 64 ...] as a dense 64 x 64 row-major block, zero above the
+// diagonal and outside nb x nb.  One one-wave workgroup per block; lane t
+// solves L_bb y = e_t, column t of the inverse, in registers.
+__global__ __launch_bounds__(64) void tri_inv_blocks(const double* __restrict__ L, int64_t ld, int64_t n,
+                                                     double* __restrict__ Linv) {
+    __shared__ double Ls[kG64][kG64 + 1];
     __shared__ double inv[kG64];
-    load_lower_block<kG64>(Ld, ld, nb, L, inv);
+    const int64_t kb = (int64_t)blockIdx.x * kG64;
+    const int nb = (int)(n - kb < kG64 ? n - kb : kG64);
+    load_lower_block<kG64>(L + kb * ld + kb, ld, nb, Ls, inv);
     __syncthreads();
-    const int64_t c = (int64_t)blockIdx.x * 64 + threadIdx.x;
-    if (c >= nrhs) return;
+    const int t = threadIdx.x;
     double x[kG64];
 #pragma unroll
-    for (int j = 0; j < kG64; ++j) x[j] = j < nb ? B[(int64_t)j * ldb + c] : 0.0;
-    if (TRANS == 0)
-        lower_solve_regs<kG64>(L, inv, nb, x);
-    else  // L^T x = b: last row first; column j of L^T is row j of L
-        lower_t_solve_regs<kG64>(L, inv, nb, x);
+    for (int i = 0; i < kG64; ++i) x[i] = i == t ? 1.0 : 0.0;
+    if (t < nb) lower_solve_regs<kG64>(Ls, inv, nb, x);
+    double* out = Linv + (int64_t)blockIdx.x * kG64 * kG64;
 #pragma unroll
-    for (int j = 0; j < kG64; ++j)
-        if (j < nb) B[(int64_t)j * ldb + c] = x[j];
+    for (int i = 0; i < kG64; ++i) out[i * kG64 + t] = (t < nb && i < nb) ? x[i] : 0.0;
 }
 
 // out = a * X + b * Y + d * I (n x n row-major; Y may be null, then b is ignored)

@@ -1317,8 +1317,16 @@ hipError_t gemm64_launch(hipStream_t st, int64_t Mr, int64_t Nc, int64_t K, doub
                          int64_t sa1, const double* B, int64_t sb0, int64_t sb1, double beta, double* C, int64_t sc0,
                          int64_t sc1, bool lower = false) {
     if (Mr <= 0 || Nc <= 0) return hipSuccess;
-    hipLaunchKernelGGL(gemm64, dim3((unsigned)ceil_div(Nc, kG64), (unsigned)ceil_div(Mr, kG64)), dim3(256), 0, st, Mr,
-                       Nc, K, alpha, A, sa0, sa1, B, sb0, sb1, beta, C, sc0, sc1, lower ? 1 : 0);
+    // 128 x 128 tiles when they fill the chip and K is deep (about 60
+    // TFLOP/s on the 4096-sized products, against 55 with 64 x 64 tiles);
+    // 64 x 64 tiles otherwise, e.g. the blocked updates with K = 64
+    if (!lower && K >= 512 && ceil_div(Mr, (int64_t)128) * ceil_div(Nc, (int64_t)128) >= kCus)
+        hipLaunchKernelGGL((gemm64<128, 8>), dim3((unsigned)ceil_div(Nc, (int64_t)128), (unsigned)ceil_div(Mr, (int64_t)128)),
+                           dim3(1024), 0, st, Mr, Nc, K, alpha, A, sa0, sa1, B, sb0, sb1, beta, C, sc0, sc1, 0);
+    else
+        hipLaunchKernelGGL((gemm64<64, 16>), dim3((unsigned)ceil_div(Nc, (int64_t)64), (unsigned)ceil_div(Mr, (int64_t)64)),
+                           dim3(1024), 0, st, Mr, Nc, K, alpha, A, sa0, sa1, B, sb0, sb1, beta, C, sc0, sc1,
+                           lower ? 1 : 0);
     return hipGetLastError();
 }
 
@@ -1343,24 +1351,37 @@ hipError_t cholesky64(double* A, int64_t n, int64_t ld, double* floor, int* info
     return hipGetLastError();
 }
 
-// B (n x nrhs, row stride ldb) <- (L L^T)^-1 B for the lower factor L (row stride ld).
-hipError_t spd_solve64(const double* L, int64_t n, int64_t ld, double* B, int64_t nrhs, int64_t ldb, hipStream_t st) {
-    const unsigned g = (unsigned)ceil_div(nrhs, (int64_t)64);
-    for (int64_t kb = 0; kb < n; kb += kG64) {  // L Y = B
-        const int nb = (int)std::min<int64_t>(kG64, n - kb);
-        hipLaunchKernelGGL((trsm_diag<0>), dim3(g), dim3(64), 0, st, L + kb * ld + kb, ld, nb, B + kb * ldb, ldb, nrhs);
-        const int64_t rest = n - kb - nb;
-        hipError_t e = gemm64_launch(st, rest, nrhs, nb, -1.0, L + (kb + nb) * ld + kb, ld, 1, B + kb * ldb, ldb, 1,
-                                     1.0, B + (kb + nb) * ldb, ldb, 1);
-        if (e != hipSuccess) return e;
+// B (n x nrhs, row stride ldb) <- (L L^T)^-1 B for the lower factor L (row
+// stride ld).  Linv: ceil(n / 64) * 64 * 64 doubles of scratch for the
+// inverted diagonal blocks; X: n * nrhs doubles of scratch (row stride nrhs).
+// Forward, L Y = B into X: Y_k = L_kk^-1 B_k, then the rows below lose
+// L_ik Y_k.  Backward, L^T Z = Y into B: Z_k = L_kk^-T Y_k, then the rows
+// above lose L_ki^T Z_k.  Multiplying by the inverted 64 x 64 blocks instead
+// of substituting keeps every step on the MFMA GEMM; the blocks of a
+// Cholesky factor of a matrix with condition number kappa have condition
+// numbers of at most sqrt(kappa), which bounds what the explicit inverses add
+// to the substitution's rounding error.
+hipError_t spd_solve64(const double* L, int64_t n, int64_t ld, double* B, int64_t nrhs, int64_t ldb, double* Linv,
+                       double* X, hipStream_t st) {
+    const int64_t nblk = ceil_div(n, (int64_t)kG64);
+    hipLaunchKernelGGL(tri_inv_blocks, dim3((unsigned)nblk), dim3(64), 0, st, L, ld, n, Linv);
+    hipError_t e = hipGetLastError();
+    for (int64_t kb = 0; kb < n && e == hipSuccess; kb += kG64) {
+        const int64_t nb = std::min<int64_t>(kG64, n - kb), rest = n - kb - nb;
+        const double* Li = Linv + (kb / kG64) * kG64 * kG64;
+        e = gemm64_launch(st, nb, nrhs, nb, 1.0, Li, kG64, 1, B + kb * ldb, ldb, 1, 0.0, X + kb * nrhs, nrhs, 1);
+        if (e == hipSuccess)
+            e = gemm64_launch(st, rest, nrhs, nb, -1.0, L + (kb + nb) * ld + kb, ld, 1, X + kb * nrhs, nrhs, 1, 1.0,
+                              B + (kb + nb) * ldb, ldb, 1);
     }
-    for (int64_t kb = ((n - 1) / kG64) * kG64; kb >= 0; kb -= kG64) {  // L^T X = Y
-        const int nb = (int)std::min<int64_t>(kG64, n - kb);
-        hipLaunchKernelGGL((trsm_diag<1>), dim3(g), dim3(64), 0, st, L + kb * ld + kb, ld, nb, B + kb * ldb, ldb, nrhs);
-        hipError_t e = gemm64_launch(st, kb, nrhs, nb, -1.0, L + kb * ld, 1, ld, B + kb * ldb, ldb, 1, 1.0, B, ldb, 1);
-        if (e != hipSuccess) return e;
+    for (int64_t kb = (nblk - 1) * kG64; kb >= 0 && e == hipSuccess; kb -= kG64) {
+        const int64_t nb = std::min<int64_t>(kG64, n - kb);
+        const double* Li = Linv + (kb / kG64) * kG64 * kG64;
+        e = gemm64_launch(st, nb, nrhs, nb, 1.0, Li, 1, kG64, X + kb * nrhs, nrhs, 1, 0.0, B + kb * ldb, ldb, 1);
+        if (e == hipSuccess)
+            e = gemm64_launch(st, kb, nrhs, nb, -1.0, L + kb * ld, 1, ld, B + kb * ldb, ldb, 1, 1.0, X, nrhs, 1);
     }
-    return hipGetLastError();
+    return e;
 }
 
 hipError_t transpose64_launch(const double* in, int64_t rows, int64_t cols, double* out, hipStream_t st) {
@@ -1480,8 +1501,10 @@ pifa_status pifa_calib_reconstruct(pifa_calib_handle c, const double* W, int64_t
     // work regions (fp64 elements, 32-element aligned)
     auto al = [](int64_t e) { return round_up(e, (int64_t)32); };
     const int64_t e_Z = al(n * n), e_T = al(m * n), e_SV = al(n * r), e_A = al(r * r), e_Bt = al(r * m),
-                  e_G = al(r * r), e_H = al(r * n), e_QT = al(n * r), e_Sa = al(n * n);
-    pifa_status s = c->work.ensure((size_t)(e_Z + e_T + e_SV + e_A + e_Bt + e_G + e_H + e_QT + e_Sa + 32) * 8, st);
+                  e_G = al(r * r), e_H = al(r * n), e_QT = al(n * r), e_Sa = al(n * n),
+                  e_X = al(std::max(r * m, r * n)), e_Li = ceil_div(n, (int64_t)kG64) * kG64 * kG64;
+    pifa_status s = c->work.ensure(
+        (size_t)(e_Z + e_T + e_SV + e_A + e_Bt + e_G + e_H + e_QT + e_Sa + e_X + e_Li + 32) * 8, st);
     if (s != PIFA_OK) return s;
     double* Z = (double*)c->work.ptr;
     double* T = Z + e_Z;
@@ -1492,7 +1515,9 @@ pifa_status pifa_calib_reconstruct(pifa_calib_handle c, const double* W, int64_t
     double* H = G + e_G;    // U_r^T (T + a W), then Q = G^-1 H (r x n)
     double* QT = H + e_H;   // Q^T, then V_r (n x r)
     double* Sa = QT + e_QT; // S + a I, then its factor
-    double* floor = Sa + e_Sa;
+    double* X = Sa + e_Sa;  // scratch of the solves
+    double* Linv = X + e_X; // their inverted diagonal blocks
+    double* floor = Linv + e_Li;
     TimedLaunch timed(kSiteCalibSolve, st);
     hipError_t e;
 #define PIFA_GO(call)                              \
@@ -1513,21 +1538,21 @@ pifa_status pifa_calib_reconstruct(pifa_calib_handle c, const double* W, int64_t
     PIFA_GO(gemm64_launch(st, r, m, n, 1.0, Vt, n, 1, T, 1, n, 0.0, Ut, m, 1));
     // U_r^T = A_r^-1 (T V)^T   (A_r symmetric)
     PIFA_GO(cholesky64(Ar, r, r, floor, c->info, st));
-    PIFA_GO(spd_solve64(Ar, r, r, Ut, m, m, st));
+    PIFA_GO(spd_solve64(Ar, r, r, Ut, m, m, Linv, X, st));
     // G = U_r^T U_r;  H = U_r^T (T + a W)
     PIFA_GO(gemm64_launch(st, r, r, m, 1.0, Ut, m, 1, Ut, 1, m, 0.0, G, r, 1));
     PIFA_GO(gemm64_launch(st, r, n, m, 1.0, Ut, m, 1, T, n, 1, 0.0, H, n, 1));
     PIFA_GO(gemm64_launch(st, r, n, m, alpha, Ut, m, 1, W, n, 1, 1.0, H, n, 1));
     // Q = G^-1 H
     PIFA_GO(cholesky64(G, r, r, floor, c->info, st));
-    PIFA_GO(spd_solve64(G, r, r, H, n, n, st));
+    PIFA_GO(spd_solve64(G, r, r, H, n, n, Linv, X, st));
     // V_r = (S + a I)^-1 Q^T  (n x r), i.e. V_r^T = Q (S + a I)^-1
     hipLaunchKernelGGL(axpby_diag64, dim3(grid_for(n * n)), dim3(256), 0, st, n, 1.0, (const double*)c->S, 0.0,
                        (const double*)nullptr, alpha, Sa);
     PIFA_GO(hipGetLastError());
     PIFA_GO(transpose64_launch(H, r, n, QT, st));
     PIFA_GO(cholesky64(Sa, n, n, floor, c->info, st));
-    PIFA_GO(spd_solve64(Sa, n, n, QT, r, r, st));
+    PIFA_GO(spd_solve64(Sa, n, n, QT, r, r, Linv, X, st));
     // outputs
     PIFA_GO(transpose64_launch(Ut, r, m, U_r, st));
     PIFA_GO(transpose64_launch(QT, n, r, Vt_r, st));
