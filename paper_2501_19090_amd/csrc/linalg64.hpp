@@ -202,101 +202,102 @@ __global__ __launch_bounds__(256) void chol_diag(double* __restrict__ A, int64_t
     }
 }
 
-// Loads the nb x nb block at Ld (row stride ld) into L and the reciprocals
-// of its diagonal into inv (a workgroup of one wave; the caller
-// synchronises).
-template <int NB>
+constexpr int kWin = 8;  // columns per pass of the windowed substitution
+
+// Loads the nb x nb lower block at Ld (row stride ld) into rows [0, 64) of
+// L, zero everywhere else (columns >= nb, rows >= nb up to 127), and the
+// reciprocals of its diagonal into inv (zero past nb).  One wave, lane t
+// loading column t (coalesced loads, all in flight at once); the caller
+// synchronises.
 __device__ __forceinline__ void load_lower_block(const double* __restrict__ Ld, int64_t ld, int nb,
-                                                 double (&L)[NB][NB + 1], double (&inv)[NB]) {
-    static_assert(NB == kWave, "one column per lane of a one-wave workgroup");
-    // lane t loads column t: NB independent, coalesced loads in flight at once
+                                                 double (&L)[2 * kG64][kG64 + 1], double (&inv)[kG64]) {
     const int t = threadIdx.x;
+    const bool col_ok = t < nb;
 #pragma unroll
-    for (int i = 0; i < NB; ++i)
-        if (i < nb && t < nb) L[i][t] = Ld[(int64_t)i * ld + t];
-    if (t < nb) inv[t] = 1.0 / Ld[(int64_t)t * ld + t];
+    for (int i = 0; i < kG64; ++i) {
+        const double v = Ld[(int64_t)(i < nb ? i : 0) * ld + (col_ok ? t : 0)];  // in bounds, no branch
+        L[i][t] = (i < nb && col_ok) ? v : 0.0;
+    }
+#pragma unroll
+    for (int i = kG64; i < 2 * kG64; ++i) L[i][t] = 0.0;
+    inv[t] = t < nb ? 1.0 / Ld[(int64_t)t * ld + t] : 0.0;
 }
 
-// Forward substitution x <- L^-1 x for the nb x nb lower factor in LDS, x
-// in registers (64 entries, those >= nb unused): column by column, so the
-// updates of one step are independent of one another and the LDS reads of
-// the column pipeline instead of each waiting for the previous product.
-// inv holds the reciprocals of L's diagonal.
-// A full block (nb == NB) takes a branch-free, fully unrolled path; a
-// partial one (the last block of a matrix whose size is not a multiple of 64)
-// an ordinary loop.
-template <int NB>
-__device__ __forceinline__ void lower_solve_regs(const double (&L)[NB][NB + 1], const double (&inv)[NB], int nb,
-                                                 double (&x)[NB]) {
-    if (nb == NB) {
+// Forward substitution x <- L^-1 x for the lower block in LDS (as
+// load_lower_block leaves it), one right-hand side per lane in w.  Columns
+// are eliminated kWin at a time, each against every later row (the rows past
+// the block read the zero padding); after a pass the kWin finished values
+// go to out(j, value) and the window shifts down by kWin.  The loop body is
+// the same for every pass, so its code stays in the instruction cache; a
+// fully unrolled elimination is about 58 KB of straight-line code that each
+// wave fetches once, which bounded the kernels at about 40 us per call.
+template <typename Out>
+__device__ __forceinline__ void lower_solve_window(const double (&L)[2 * kG64][kG64 + 1], const double (&inv)[kG64],
+                                                   double (&w)[kG64], Out&& out) {
+#pragma unroll 1
+    for (int j0 = 0; j0 < kG64; j0 += kWin) {
 #pragma unroll
-        for (int j = 0; j < NB; ++j) {
-            x[j] = x[j] * inv[j];
+        for (int t = 0; t < kWin; ++t) {
+            const double xt = w[t] * inv[j0 + t];
+            w[t] = xt;
+            // 16 rows at a time: the scheduler would otherwise hoist every
+            // LDS read of the pass above the first FMA and run out of registers
 #pragma unroll
-            for (int i = j + 1; i < NB; ++i) x[i] -= L[i][j] * x[j];
-        }
-    } else {
-        double y[NB];
+            for (int i0 = 0; i0 < kG64; i0 += 16) {
 #pragma unroll
-        for (int i = 0; i < NB; ++i) y[i] = x[i];
-        for (int j = 0; j < nb; ++j) {
-            double xj = 0.0;
-#pragma unroll
-            for (int i = 0; i < NB; ++i)
-                if (i == j) xj = y[i] * inv[j];
-#pragma unroll
-            for (int i = 0; i < NB; ++i) {
-                if (i == j) y[i] = xj;
-                else if (i > j && i < nb) y[i] -= L[i][j] * xj;
+                for (int i = i0; i < i0 + 16; ++i)
+                    if (i > t) w[i] -= L[j0 + i][j0 + t] * xt;
+                __builtin_amdgcn_sched_barrier(0);
             }
         }
 #pragma unroll
-        for (int i = 0; i < NB; ++i) x[i] = y[i];
+        for (int t = 0; t < kWin; ++t) out(j0 + t, w[t]);
+#pragma unroll
+        for (int i = 0; i < kG64 - kWin; ++i) w[i] = w[i + kWin];
+#pragma unroll
+        for (int i = kG64 - kWin; i < kG64; ++i) w[i] = 0.0;
     }
 }
 
-// Panel of a blocked Cholesky: rows [0, nrows) of P (row stride ld, nb
-// columns) become P L11^-T, L11 being the nb x nb lower factor at Ld (row
-// stride ld): row p solves L11 x = p^T.  One row per thread, in registers.
+// Panel of a blocked Cholesky: rows [0, nrows) of P (row stride ld, 64
+// columns) become P L11^-T, L11 being the 64 x 64 lower factor at Ld (row
+// stride ld): row p solves L11 x = p^T.  One row per lane.  Only full
+// diagonal blocks have a panel below them (a block narrower than 64 is the
+// last one of its matrix).
 __global__ __launch_bounds__(64) void chol_panel(const double* __restrict__ Ld, double* __restrict__ P, int64_t ld,
-                                                 int nb, int64_t nrows) {
-    __shared__ double L[kG64][kG64 + 1];
+                                                 int64_t nrows) {
+    __shared__ double L[2 * kG64][kG64 + 1];
     __shared__ double inv[kG64];
-    load_lower_block<kG64>(Ld, ld, nb, L, inv);
+    load_lower_block(Ld, ld, kG64, L, inv);
     __syncthreads();
     const int64_t row = (int64_t)blockIdx.x * 64 + threadIdx.x;
     if (row >= nrows) return;
     double* p = P + row * ld;
-    double x[kG64];
+    double w[kG64];
 #pragma unroll
-    for (int j = 0; j < kG64; ++j) x[j] = j < nb ? p[j] : 0.0;
-    lower_solve_regs<kG64>(L, inv, nb, x);
-#pragma unroll
-    for (int j = 0; j < kG64; ++j)
-        if (j < nb) p[j] = x[j];
+    for (int j = 0; j < kG64; ++j) w[j] = p[j];
+    lower_solve_window(L, inv, w, [&](int j, double v) { p[j] = v; });
 }
 
 // Inverses of the diagonal blocks of a lower factor: block b (rows and
 // columns [64 b, 64 b + nb)) of the n x n factor L (row stride ld) goes to
 // Linv[b * 64 * 64 ...] as a dense 64 x 64 row-major block, zero above the
 // diagonal and outside nb x nb.  One one-wave workgroup per block; lane t
-// solves L_bb y = e_t, column t of the inverse, in registers.
+// solves L_bb y = e_t, column t of the inverse.
 __global__ __launch_bounds__(64) void tri_inv_blocks(const double* __restrict__ L, int64_t ld, int64_t n,
                                                      double* __restrict__ Linv) {
-    __shared__ double Ls[kG64][kG64 + 1];
+    __shared__ double Ls[2 * kG64][kG64 + 1];
     __shared__ double inv[kG64];
     const int64_t kb = (int64_t)blockIdx.x * kG64;
     const int nb = (int)(n - kb < kG64 ? n - kb : kG64);
-    load_lower_block<kG64>(L + kb * ld + kb, ld, nb, Ls, inv);
+    load_lower_block(L + kb * ld + kb, ld, nb, Ls, inv);
     __syncthreads();
     const int t = threadIdx.x;
-    double x[kG64];
+    double w[kG64];
 #pragma unroll
-    for (int i = 0; i < kG64; ++i) x[i] = i == t ? 1.0 : 0.0;
-    if (t < nb) lower_solve_regs<kG64>(Ls, inv, nb, x);
+    for (int i = 0; i < kG64; ++i) w[i] = (i == t && t < nb) ? 1.0 : 0.0;
     double* out = Linv + (int64_t)blockIdx.x * kG64 * kG64;
-#pragma unroll
-    for (int i = 0; i < kG64; ++i) out[i * kG64 + t] = (t < nb && i < nb) ? x[i] : 0.0;
+    lower_solve_window(Ls, inv, w, [&](int j, double v) { out[j * kG64 + t] = v; });
 }
 
 // out = a * X + b * Y + d * I (n x n row-major; Y may be null, then b is ignored)

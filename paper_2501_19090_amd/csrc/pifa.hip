@@ -1341,8 +1341,9 @@ hipError_t cholesky64(double* A, int64_t n, int64_t ld, double* floor, int* info
         const int64_t rest = n - kb - nb;
         if (rest > 0) {
             double* L21 = A + (kb + nb) * ld + kb;
+            // rest > 0: this block is a full one (nb == 64)
             hipLaunchKernelGGL(chol_panel, dim3((unsigned)ceil_div(rest, (int64_t)64)), dim3(64), 0, st, Akk, L21, ld,
-                               nb, rest);
+                               rest);
             hipError_t e = gemm64_launch(st, rest, rest, nb, -1.0, L21, ld, 1, L21, 1, ld, 1.0,
                                          A + (kb + nb) * ld + kb + nb, ld, 1, true);
             if (e != hipSuccess) return e;
