@@ -249,6 +249,33 @@ def test_deterministic_and_stream_ordered():
         lay.close()
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_non_finite_inputs_stay_in_their_rows(dtype):
+    """A NaN or an Inf in a row of X makes every output of that row non-finite
+    (the products and the fp16 hand-off carry them), and leaves every other
+    row bit-identical to the run without them (rows are independent), in the
+    decode, split-K and prefill launch shapes."""
+    torch = torch_mod()
+    piv, npiv, Wp, C, _, _ = gaussian_layer(512, 768, 256, 8)
+    lay = DeviceLayer(piv, npiv, Wp, C, dtype)
+    try:
+        for M in (1, 5, 16, 100, 700):
+            x_dev, _ = activations(M, 512, 21 + M, dtype)
+            y_clean = lay.forward(x_dev)
+            x_bad = x_dev.clone()
+            bad = {0: float("nan")} if M == 1 else {0: float("nan"), M - 1: float("inf")}
+            for row, v in bad.items():
+                x_bad[row, 5 + row % 7] = v
+            y = lay.forward(x_bad)
+            for row in bad:
+                assert not bool(torch.isfinite(y[row]).any()), (M, row)
+            keep = [m for m in range(M) if m not in bad]
+            if keep:
+                assert torch.equal(y[keep], y_clean[keep]), M
+    finally:
+        lay.close()
+
+
 def _exchanged_pivot_set(W, piv, npiv, swaps: int):
     """A second valid pivot set: starting from QRCP's, repeatedly swap the
     pivot j and non-pivot k with the largest |C[k, j]| (a basis exchange that
