@@ -221,7 +221,9 @@ pifa_status pifa_group_overflow_count(pifa_group_handle g, int64_t* count);
 /*
  * Dense baseline (Sec. 3.3, 2 m n b FLOPs): Y = X W^T.
  *   W device d_out x d_in; X device M x d_in; Y device M x d_out.
- * Reads the caller's row-major W directly (no workspace).
+ * Reads the caller's row-major W directly (no copy).  Products too small to
+ * fill the GPU split K through the library's shared per-device workspace,
+ * as lowrank_uv_forward does: calls on different streams must not overlap.
  */
 pifa_status dense_forward(const void* W, const void* X, void* Y, int64_t M, int64_t d_in,
                           int64_t d_out, pifa_dtype dtype, void* stream);

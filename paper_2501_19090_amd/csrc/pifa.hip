@@ -66,14 +66,15 @@ pifa_status check_device(int dev) {
 inline size_t esize(pifa_dtype dt) { return dt == PIFA_BF16 ? 2 : 4; }
 inline bool valid_dtype(pifa_dtype dt) { return dt == PIFA_BF16 || dt == PIFA_F32; }
 
-// A device buffer that only grows; growing waits for `st` first so no kernel
-// in flight still uses the old allocation.
+// A device buffer that only grows; growing waits for `st` (or, for a buffer
+// shared by calls on any stream, the whole device) first so no kernel in
+// flight still uses the old allocation.
 struct GrowBuf {
     void* ptr = nullptr;
     size_t bytes = 0;
-    pifa_status ensure(size_t need, hipStream_t st) {
+    pifa_status ensure(size_t need, hipStream_t st, bool any_stream = false) {
         if (need <= bytes) return PIFA_OK;
-        PIFA_HIP(hipStreamSynchronize(st));
+        PIFA_HIP(any_stream ? hipDeviceSynchronize() : hipStreamSynchronize(st));
         if (ptr) PIFA_HIP(hipFree(ptr));
         ptr = nullptr;
         bytes = 0;
@@ -469,6 +470,9 @@ pifa_status absmax_bf16_host(const void* src, int64_t n, float* out) {
 }
 
 // ------------------------------------------------------------------ shared workspace
+// Workspace of the stateless baselines, one per device.  Growing it waits
+// for the whole device; the calls that use it must not overlap on the GPU
+// (the same rule as for one handle used from several streams).
 struct DeviceScratch {
     std::mutex mu;
     GrowBuf inter;  // intermediate X V^T of the stateless low-rank baseline
@@ -974,7 +978,7 @@ pifa_status dense_forward(const void* W, const void* X, void* Y, int64_t M, int6
     PIFA_HIP(hipGetDevice(&dev));
     DeviceScratch& ds = device_scratch(dev);
     std::lock_guard<std::mutex> g(ds.mu);
-    s = ds.part.ensure(dense_part_bytes(dtype, M, d_in, d_out), st);
+    s = ds.part.ensure(dense_part_bytes(dtype, M, d_in, d_out), st, true);
     if (s != PIFA_OK) return s;
     return dense_run<false>(dtype, W, X, Y, M, d_in, d_out, (float*)ds.part.ptr, st);
 }
@@ -1057,8 +1061,8 @@ pifa_status lowrank_uv_forward(const void* U, const void* V, const void* X, void
     PIFA_HIP(hipGetDevice(&dev));
     DeviceScratch& ds = device_scratch(dev);
     std::lock_guard<std::mutex> g(ds.mu);
-    s = ds.inter.ensure(lowrank_ws_bytes(dtype, M, dims.r), st);
-    if (s == PIFA_OK) s = ds.part.ensure(lowrank_part_bytes(dtype, M, dims.d_in, dims.d_out, dims.r), st);
+    s = ds.inter.ensure(lowrank_ws_bytes(dtype, M, dims.r), st, true);
+    if (s == PIFA_OK) s = ds.part.ensure(lowrank_part_bytes(dtype, M, dims.d_in, dims.d_out, dims.r), st, true);
     if (s != PIFA_OK) return s;
     return lowrank_run<false>(dtype, U, V, X, Y, M, dims.d_in, dims.d_out, dims.r, ds.inter.ptr,
                               (float*)ds.part.ptr, st);
