@@ -138,6 +138,47 @@ def _dev_ptr(t, name: str) -> int | None:
     return t.data_ptr()
 
 
+# Dimensions of the live handles created through this module.  The library
+# takes raw pointers and cannot see how large a tensor is, so the calls below
+# check that each buffer holds the bytes the call will read or write (a short
+# buffer would be accessed past its end on the GPU).  Handles created
+# elsewhere are passed through unchecked.
+_dims: dict = {}
+_dims_lock = threading.Lock()
+
+
+def _esize(dt: int) -> int:
+    return 2 if dt == PIFA_BF16 else 4
+
+
+def _need(t, nbytes: int, name: str) -> None:
+    if t is not None and t.numel() * t.element_size() < nbytes:
+        raise ValueError("%s holds %d bytes, the call needs %d" % (name, t.numel() * t.element_size(), nbytes))
+
+
+def _remember(handle: int, **dims) -> int:
+    with _dims_lock:
+        _dims[handle] = dims
+    return handle
+
+
+def _recall(handle: int):
+    with _dims_lock:
+        return _dims.get(handle)
+
+
+def _forget(handle: int) -> None:
+    with _dims_lock:
+        _dims.pop(handle, None)
+
+
+def _check_io(handle: int, X, Y, M: int) -> None:
+    d = _recall(handle)
+    if d is not None and M > 0:
+        _need(X, M * d["d_in"] * _esize(d["dt"]), "X")
+        _need(Y, M * d["d_out"] * _esize(d["dt"]), "Y")
+
+
 def _host_i32(a):
     if a is None:
         return None, None
@@ -174,13 +215,17 @@ def pifa_layer_create(W_p, C, pivot_idx, nonpivot_idx, dims, dtype: int | None =
     dt = _dtype_code(W_p) if dtype is None else int(dtype)
     piv, pp = _host_i32(pivot_idx)
     npv, npp = _host_i32(nonpivot_idx)
+    d_in, d_out, r = (int(v) for v in dims)
+    _need(W_p, r * d_in * _esize(dt), "W_p")
+    _need(C, max(d_out - r, 0) * r * _esize(dt), "C")
     out = _vp()
     _check("pifa_layer_create", lib().pifa_layer_create(
         _dev_ptr(W_p, "W_p"), _dev_ptr(C, "C"), pp, npp, pifa_dims(*dims), dt, ctypes.byref(out)))
-    return out.value
+    return _remember(out.value, d_in=d_in, d_out=d_out, r=r, dt=dt)
 
 
 def pifa_layer_destroy(handle: int) -> None:
+    _forget(handle)
     _check("pifa_layer_destroy", lib().pifa_layer_destroy(handle))
 
 
@@ -190,6 +235,7 @@ def pifa_layer_reserve(handle: int, max_M: int) -> None:
 
 def pifa_forward(handle: int, X, Y, M: int | None = None, stream=None) -> None:
     M = X.shape[0] if M is None else int(M)
+    _check_io(handle, X, Y, M)
     _check("pifa_forward", lib().pifa_forward(handle, _dev_ptr(X, "X"), _dev_ptr(Y, "Y"), M,
                                               _stream(stream)))
 
@@ -214,6 +260,13 @@ def pifa_layer_backward(handle: int, X, Y, dY, dX=None, dW_p=None, dC=None, M: i
     """Gradients of the layer: dX (bf16 M x d_in), dW_p (fp32 r x d_in), dC (fp32 (d_out-r) x r);
     each output may be None to skip it."""
     M = dY.shape[0] if M is None else int(M)
+    d = _recall(handle)
+    if d is not None and M > 0:  # bf16 activations and gradients, fp32 weight gradients
+        for t, n, name in ((X, M * d["d_in"], "X"), (Y, M * d["d_out"], "Y"), (dY, M * d["d_out"], "dY"),
+                           (dX, M * d["d_in"], "dX")):
+            _need(t, 2 * n, name)
+        _need(dW_p, 4 * d["r"] * d["d_in"], "dW_p")
+        _need(dC, 4 * (d["d_out"] - d["r"]) * d["r"], "dC")
     _check("pifa_layer_backward", lib().pifa_layer_backward(
         handle, _dev_ptr(X, "X"), _dev_ptr(Y, "Y"), _dev_ptr(dY, "dY"), M, _dev_ptr(dX, "dX"),
         _dev_ptr(dW_p, "dW_p"), _dev_ptr(dC, "dC"), _stream(stream)))
@@ -225,6 +278,10 @@ def dense_forward(W, X, Y, M: int | None = None, d_in: int | None = None, d_out:
     d_in = W.shape[1] if d_in is None else int(d_in)
     d_out = W.shape[0] if d_out is None else int(d_out)
     dt = _dtype_code(W) if dtype is None else int(dtype)
+    if M > 0:
+        _need(W, d_out * d_in * _esize(dt), "W")
+        _need(X, M * d_in * _esize(dt), "X")
+        _need(Y, M * d_out * _esize(dt), "Y")
     _check("dense_forward", lib().dense_forward(_dev_ptr(W, "W"), _dev_ptr(X, "X"), _dev_ptr(Y, "Y"),
                                                 M, d_in, d_out, dt, _stream(stream)))
 
@@ -234,14 +291,16 @@ def dense_layer_create(W, d_in: int | None = None, d_out: int | None = None,
     d_in = W.shape[1] if d_in is None else int(d_in)
     d_out = W.shape[0] if d_out is None else int(d_out)
     dt = _dtype_code(W) if dtype is None else int(dtype)
+    _need(W, d_out * d_in * _esize(dt), "W")
     out = _vp()
     _check("dense_layer_create", lib().dense_layer_create(_dev_ptr(W, "W"), d_in, d_out, dt,
                                                           ctypes.byref(out)))
-    return out.value
+    return _remember(out.value, d_in=d_in, d_out=d_out, dt=dt)
 
 
 def dense_layer_forward(handle: int, X, Y, M: int | None = None, stream=None) -> None:
     M = X.shape[0] if M is None else int(M)
+    _check_io(handle, X, Y, M)
     _check("dense_layer_forward", lib().dense_layer_forward(handle, _dev_ptr(X, "X"), _dev_ptr(Y, "Y"), M,
                                                             _stream(stream)))
 
@@ -251,6 +310,7 @@ def dense_layer_reserve(handle: int, max_M: int) -> None:
 
 
 def dense_layer_destroy(handle: int) -> None:
+    _forget(handle)
     _check("dense_layer_destroy", lib().dense_layer_destroy(handle))
 
 
@@ -259,6 +319,12 @@ def lowrank_uv_forward(U, V, X, Y, M: int | None = None, dims=None, dtype: int |
     M = X.shape[0] if M is None else int(M)
     dims = (V.shape[1], U.shape[0], U.shape[1]) if dims is None else dims
     dt = _dtype_code(U) if dtype is None else int(dtype)
+    d_in, d_out, r = (int(v) for v in dims)
+    if M > 0:
+        _need(U, d_out * r * _esize(dt), "U")
+        _need(V, r * d_in * _esize(dt), "V")
+        _need(X, M * d_in * _esize(dt), "X")
+        _need(Y, M * d_out * _esize(dt), "Y")
     _check("lowrank_uv_forward", lib().lowrank_uv_forward(
         _dev_ptr(U, "U"), _dev_ptr(V, "V"), _dev_ptr(X, "X"), _dev_ptr(Y, "Y"), M, pifa_dims(*dims),
         dt, _stream(stream)))
@@ -267,14 +333,18 @@ def lowrank_uv_forward(U, V, X, Y, M: int | None = None, dims=None, dtype: int |
 def lowrank_layer_create(U, V, dims=None, dtype: int | None = None) -> int:
     dims = (V.shape[1], U.shape[0], U.shape[1]) if dims is None else dims
     dt = _dtype_code(U) if dtype is None else int(dtype)
+    d_in, d_out, r = (int(v) for v in dims)
+    _need(U, d_out * r * _esize(dt), "U")
+    _need(V, r * d_in * _esize(dt), "V")
     out = _vp()
     _check("lowrank_layer_create", lib().lowrank_layer_create(
         _dev_ptr(U, "U"), _dev_ptr(V, "V"), pifa_dims(*dims), dt, ctypes.byref(out)))
-    return out.value
+    return _remember(out.value, d_in=d_in, d_out=d_out, dt=dt)
 
 
 def lowrank_layer_forward(handle: int, X, Y, M: int | None = None, stream=None) -> None:
     M = X.shape[0] if M is None else int(M)
+    _check_io(handle, X, Y, M)
     _check("lowrank_layer_forward", lib().lowrank_layer_forward(
         handle, _dev_ptr(X, "X"), _dev_ptr(Y, "Y"), M, _stream(stream)))
 
@@ -284,6 +354,7 @@ def lowrank_layer_reserve(handle: int, max_M: int) -> None:
 
 
 def lowrank_layer_destroy(handle: int) -> None:
+    _forget(handle)
     _check("lowrank_layer_destroy", lib().lowrank_layer_destroy(handle))
 
 
@@ -297,7 +368,11 @@ def pifa_group_create(layers, dtype: int | None = None) -> int:
     npp = (_i32p * max(n, 1))()
     dims = (pifa_dims * max(n, 1))()
     keep = []
+    dt = (_dtype_code(layers[0][0]) if n else PIFA_BF16) if dtype is None else int(dtype)
     for i, (W_p, C, piv, npiv, d) in enumerate(layers):
+        if dt == PIFA_BF16:  # the only group dtype; the library rejects the others
+            _need(W_p, int(d[2]) * int(d[0]) * 2, "W_p")
+            _need(C, max(int(d[1]) - int(d[2]), 0) * int(d[2]) * 2, "C")
         wp[i] = _dev_ptr(W_p, "W_p")
         cc[i] = _dev_ptr(C, "C")
         a, ap = _host_i32(piv)
@@ -306,13 +381,13 @@ def pifa_group_create(layers, dtype: int | None = None) -> int:
         pp[i] = ap
         npp[i] = bp
         dims[i] = pifa_dims(*d)
-    dt = (_dtype_code(layers[0][0]) if n else PIFA_BF16) if dtype is None else int(dtype)
     out = _vp()
     _check("pifa_group_create", lib().pifa_group_create(n, wp, cc, pp, npp, dims, dt, ctypes.byref(out)))
-    return out.value
+    return _remember(out.value, d_in=int(layers[0][4][0]), d_out=sum(int(l[4][1]) for l in layers), dt=dt)
 
 
 def pifa_group_destroy(handle: int) -> None:
+    _forget(handle)
     _check("pifa_group_destroy", lib().pifa_group_destroy(handle))
 
 
@@ -322,6 +397,7 @@ def pifa_group_reserve(handle: int, max_M: int) -> None:
 
 def pifa_group_forward(handle: int, X, Y, M: int | None = None, stream=None) -> None:
     M = X.shape[0] if M is None else int(M)
+    _check_io(handle, X, Y, M)
     _check("pifa_group_forward", lib().pifa_group_forward(handle, _dev_ptr(X, "X"), _dev_ptr(Y, "Y"), M,
                                                           _stream(stream)))
 
@@ -344,10 +420,11 @@ def pifa_group_overflow_count(handle: int) -> int:
 def pifa_calib_create(d_in: int) -> int:
     out = _vp()
     _check("pifa_calib_create", lib().pifa_calib_create(int(d_in), ctypes.byref(out)))
-    return out.value
+    return _remember(out.value, n=int(d_in))
 
 
 def pifa_calib_destroy(handle: int) -> None:
+    _forget(handle)
     _check("pifa_calib_destroy", lib().pifa_calib_destroy(handle))
 
 
@@ -357,11 +434,19 @@ def pifa_calib_reset(handle: int, stream=None) -> None:
 
 def pifa_calib_accumulate(handle: int, X_o, X_u, B: int | None = None, stream=None) -> None:
     B = X_u.shape[0] if B is None else int(B)
+    d = _recall(handle)
+    if d is not None and B > 0:
+        _need(X_o, 2 * B * d["n"], "X_o")
+        _need(X_u, 2 * B * d["n"], "X_u")
     _check("pifa_calib_accumulate", lib().pifa_calib_accumulate(handle, _dev_ptr(X_o, "X_o"), _dev_ptr(X_u, "X_u"),
                                                                 B, _stream(stream)))
 
 
 def pifa_calib_read(handle: int, S=None, P=None, stream=None) -> None:
+    d = _recall(handle)
+    if d is not None:
+        _need(S, 8 * d["n"] * d["n"], "S")
+        _need(P, 8 * d["n"] * d["n"], "P")
     _check("pifa_calib_read", lib().pifa_calib_read(handle, _dev_ptr(S, "S"), _dev_ptr(P, "P"), _stream(stream)))
 
 
@@ -374,6 +459,11 @@ def pifa_calib_reconstruct(handle: int, W, Vt, lam: float, alpha: float, U_r=Non
         U_r = torch.empty((d_out, r), dtype=torch.float64, device=W.device)
     if Vt_r is None:
         Vt_r = torch.empty((r, d_in), dtype=torch.float64, device=W.device)
+    d = _recall(handle)
+    if d is not None:
+        n = d["n"]
+        for t, nb, name in ((W, d_out * n, "W"), (Vt, r * n, "Vt"), (U_r, d_out * r, "U_r"), (Vt_r, r * n, "Vt_r")):
+            _need(t, 8 * nb, name)
     _check("pifa_calib_reconstruct", lib().pifa_calib_reconstruct(
         handle, _dev_ptr(W, "W"), int(d_out), _dev_ptr(Vt, "Vt"), int(r), float(lam), float(alpha),
         _dev_ptr(U_r, "U_r"), _dev_ptr(Vt_r, "Vt_r"), _stream(stream)))

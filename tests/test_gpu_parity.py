@@ -276,6 +276,32 @@ def test_non_finite_inputs_stay_in_their_rows(dtype):
         lay.close()
 
 
+def test_short_buffers_are_rejected_before_the_call():
+    """The binding checks buffer sizes against the handle's dimensions, so a
+    tensor that is too small never reaches the kernels (which would access it
+    past its end)."""
+    torch = torch_mod()
+    from paper_2501_19090_amd import pifa
+    piv, npiv = inputs.random_partition(96, 40, 3)
+    Wp, C = inputs.layout_probe_layer(64, 96, 40)
+    lay = DeviceLayer(piv, npiv, Wp, C, "bf16")
+    try:
+        x = torch.zeros((8, 64), dtype=torch.bfloat16, device="cuda:0")
+        y_short = torch.zeros((8, 95), dtype=torch.bfloat16, device="cuda:0")
+        with pytest.raises(ValueError):
+            pifa.pifa_forward(lay.handle, x, y_short)
+        with pytest.raises(ValueError):
+            pifa.pifa_forward(lay.handle, x[:4], torch.zeros((8, 96), dtype=torch.bfloat16, device="cuda:0"), 8)
+        y = torch.zeros((8, 96), dtype=torch.bfloat16, device="cuda:0")
+        pifa.pifa_forward(lay.handle, x, y)  # the right sizes still run
+        torch.cuda.synchronize()
+        w = torch.zeros((96, 64), dtype=torch.bfloat16, device="cuda:0")
+        with pytest.raises(ValueError):
+            pifa.dense_forward(w[:50], x, y, d_out=96)
+    finally:
+        lay.close()
+
+
 def _exchanged_pivot_set(W, piv, npiv, swaps: int):
     """A second valid pivot set: starting from QRCP's, repeatedly swap the
     pivot j and non-pivot k with the largest |C[k, j]| (a basis exchange that
