@@ -212,6 +212,10 @@ SplitPlan split_plan(int64_t tiles, int64_t M, int64_t N, int64_t K) {
 // Partial-product bytes a launch of this shape needs (0 if it does not split).
 TileCfg pick_tile(int64_t M, int64_t N);
 
+// No product with more rows than this splits K: its 128-row tiles alone
+// fill the chip.  Reserving for every M up to it covers every split.
+constexpr int64_t kSplitMaxM = 128 * kCus;
+
 size_t split_bytes(int64_t M, int64_t N, int64_t K) {
     if (M == 0 || N == 0 || pick_tile(M, N) != kTile128x128) return 0;
     const SplitPlan p = split_plan(ceil_div(M, 128) * ceil_div(N, 128), M, N, K);
@@ -867,8 +871,8 @@ pifa_status pifa_layer_reserve(pifa_handle h, int64_t max_M) {
     if (s != PIFA_OK) return s;
     // the split partials of every M up to max_M (they are not monotone in M)
     size_t part = 0;
-    for (int64_t m = kDecodeMaxM + 1; m <= max_M; m = m < 4096 ? m + 1 : m * 2)
-        part = std::max(part, pifa_part_bytes(h, std::min(m, max_M)));
+    for (int64_t m = kDecodeMaxM + 1; m <= std::min(max_M, kSplitMaxM); ++m)
+        part = std::max(part, pifa_part_bytes(h, m));
     s = h->part.ensure(part, 0);
     if (s != PIFA_OK) return s;
     return hipDeviceSynchronize() == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
@@ -1031,8 +1035,8 @@ pifa_status dense_layer_reserve(dense_handle h, int64_t max_M) {
     if (!h || max_M < 0) return PIFA_ERR_INVALID_ARG;
     PIFA_ON_DEVICE(h->device);
     size_t part = 0;
-    for (int64_t m = kDecodeMaxM + 1; m <= max_M; m = m < 4096 ? m + 1 : m * 2)
-        part = std::max(part, dense_part_bytes(h->dtype, std::min(m, max_M), h->d_in, h->d_out));
+    for (int64_t m = kDecodeMaxM + 1; m <= std::min(max_M, kSplitMaxM); ++m)
+        part = std::max(part, dense_part_bytes(h->dtype, m, h->d_in, h->d_out));
     pifa_status s = h->part.ensure(part, 0);
     if (s != PIFA_OK) return s;
     return hipDeviceSynchronize() == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
@@ -1120,8 +1124,8 @@ pifa_status lowrank_layer_reserve(lowrank_handle h, int64_t max_M) {
     pifa_status s = h->ws.ensure(need, 0);
     if (s != PIFA_OK) return s;
     size_t part = 0;
-    for (int64_t m = kDecodeMaxM + 1; m <= max_M; m = m < 4096 ? m + 1 : m * 2)
-        part = std::max(part, lowrank_part_bytes(h->dtype, std::min(m, max_M), h->d_in, h->d_out, h->r_pad));
+    for (int64_t m = kDecodeMaxM + 1; m <= std::min(max_M, kSplitMaxM); ++m)
+        part = std::max(part, lowrank_part_bytes(h->dtype, m, h->d_in, h->d_out, h->r_pad));
     s = h->part.ensure(part, 0);
     if (s != PIFA_OK) return s;
     return hipDeviceSynchronize() == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
@@ -1648,8 +1652,8 @@ pifa_status pifa_group_reserve(pifa_group_handle g, int64_t max_M) {
                                           group_ws_bytes(g, std::min<int64_t>(max_M, kDecodeMaxM))), 0);
     if (s != PIFA_OK) return s;
     size_t part = 0;
-    for (int64_t m = kDecodeMaxM + 1; m <= max_M; m = m < 4096 ? m + 1 : m * 2)
-        part = std::max(part, group_part_bytes(g, std::min(m, max_M)));
+    for (int64_t m = kDecodeMaxM + 1; m <= std::min(max_M, kSplitMaxM); ++m)
+        part = std::max(part, group_part_bytes(g, m));
     s = g->part.ensure(part, 0);
     if (s != PIFA_OK) return s;
     return hipDeviceSynchronize() == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
