@@ -457,7 +457,8 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--full", action="store_true", help="also sweep every configuration")
-    ap.add_argument("--out", default=os.path.join(ROOT, "gpurun_out", "bench_full.json"))
+    ap.add_argument("--out", default=os.path.join("results", "bench_full.json"),
+                    help="where --full writes its per-configuration report")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--profile-m", type=int, default=4096,
                     help="with --profile-run: activation rows of the profiled forward (1..4096)")
@@ -604,7 +605,7 @@ def main():
     if args.full:
         out["full_report"] = args.out
         full = run_full(args)
-        os.makedirs(os.path.dirname(args.out), exist_ok=True)
+        os.makedirs(os.path.dirname(os.path.abspath(args.out)), exist_ok=True)
         with open(args.out, "w") as f:
             json.dump(full, f, indent=1)
     print(json.dumps(out), flush=True)
