@@ -174,8 +174,9 @@ pifa_status pifa_layer_backward(pifa_handle h, const void* X, const void* Y, con
  * transformer MLP's gate and up projections, or attention's q, k and v), with
  * a rank of their own each (MPIFA_NS sets a density per module: appendix
  * "Experiment Details", MPIFA_NS).  Evaluated together: one product X [W_p,1; W_p,2; ...]^T reads
- * X once for every layer's pivot outputs, and one launch computes every
- * layer's Y_np,i = Y_p,i C_i^T.
+ * X once for every layer's pivot outputs; for M <= 16 one launch also
+ * streams every layer's C for Y_np,i = Y_p,i C_i^T, and for larger M each
+ * layer's Y_np,i is its own launch.
  *   n             number of layers, 1 <= n <= 8.
  *   W_p[i], C[i]  device pointers as for pifa_layer_create (C[i] may be NULL
  *                 when r_i = d_out,i).

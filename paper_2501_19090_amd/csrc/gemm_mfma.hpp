@@ -343,40 +343,6 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_nt_mfma(const T* __restric
     }
 }
 
-// Several products with the same M in one launch (grouped layers): problem
-// g owns workgroups [tile_start[g], tile_start[g + 1]) of the XCD-remapped
-// id space; B is in lane order.
-constexpr int kMaxGroup = 8;
-
-template <typename T, typename Epi>
-struct GemmProblem {
-    const T* A;
-    int64_t lda;
-    const T* B;
-    int64_t N, K;
-    Epi epi;
-};
-
-template <typename T, typename Epi>
-struct GemmGroup {
-    GemmProblem<T, Epi> p[kMaxGroup];
-    int64_t tile_start[kMaxGroup + 1];
-    int64_t M;
-    int n;
-};
-
-template <typename T, int BM, int BN, int BK, int WM, int WN, int PGR, typename Epi>
-__global__ __launch_bounds__(WM* WN* kWave) void gemm_nt_grouped(GemmGroup<T, Epi> grp) {
-    const int64_t t = xcd_remap(blockIdx.x, grp.tile_start[grp.n]);
-    int g = 0;
-    while (g + 1 < grp.n && t >= grp.tile_start[g + 1]) ++g;
-    const GemmProblem<T, Epi>& p = grp.p[g];
-    int64_t tm, tn;
-    band_coords(t - grp.tile_start[g], ceil_div(grp.M, BM), ceil_div(p.N, BN), tm, tn);
-    gemm_nt_tile<T, BM, BN, BK, WM, WN, true, PGR, Epi>(p.A, p.lda, grp.M, p.B, 0, p.N, p.K, 0, p.K, tm, tn,
-                                                       p.epi);
-}
-
 // Epilogue of a K-split launch: the fp32 partial tile of split s goes to
 // P[s][m][n] (row-major M x N per split).
 struct SplitEpi {

@@ -35,6 +35,7 @@ namespace {
 
 // ------------------------------------------------------------------ config
 constexpr int64_t kDecodeMaxM = 16;  // M at or below this takes the weight-streaming path
+constexpr int kMaxGroup = kMaxSkinnyGroup;  // layers per pifa_group
 constexpr int64_t kRowPad = 64;      // W_p rows / C columns padded to this multiple
 
 constexpr int kGemmBK = 64;
@@ -370,33 +371,6 @@ hipError_t launch_skinny_packed(int site, AL al, const TB* B, int64_t N, int64_t
     return hipGetLastError();
 }
 
-// Grouped prefill products (same M, B in lane order): one launch, the tile
-// shape picked for the group's total width.
-template <int BM, int BN, int WM, int WN, int PGR, typename T, typename Epi>
-hipError_t launch_grouped_cfg(GemmGroup<T, Epi> grp, hipStream_t st) {
-    grp.tile_start[0] = 0;
-    for (int g = 0; g < grp.n; ++g)
-        grp.tile_start[g + 1] = grp.tile_start[g] + ceil_div(grp.M, BM) * ceil_div(grp.p[g].N, BN);
-    if (grp.tile_start[grp.n] == 0) return hipSuccess;
-    hipLaunchKernelGGL((gemm_nt_grouped<T, BM, BN, kGemmBK, WM, WN, PGR, Epi>),
-                       dim3((unsigned)grp.tile_start[grp.n]), dim3(WM * WN * kWave), 0, st, grp);
-    return hipGetLastError();
-}
-
-template <typename T, typename Epi>
-hipError_t launch_gemm_grouped(int site, const GemmGroup<T, Epi>& grp, hipStream_t st) {
-    int64_t n_total = 0;
-    for (int g = 0; g < grp.n; ++g) n_total += grp.p[g].N;
-    if (grp.M == 0 || n_total == 0) return hipSuccess;
-    TimedLaunch timed(site, st);
-    switch (pick_tile(grp.M, n_total)) {
-        case kTile256x256: return launch_grouped_cfg<256, 256, 2, 4, 1>(grp, st);
-        case kTile256x192: return launch_grouped_cfg<256, 192, 4, 2, 2>(grp, st);
-        case kTile256x128: return launch_grouped_cfg<256, 128, 4, 2, 2>(grp, st);
-        default: return launch_grouped_cfg<128, 128, 4, 2, 2>(grp, st);
-    }
-}
-
 // Grouped weight streams for decode-sized M (at most 16 rows).
 template <typename TB, typename AL, typename Epi>
 hipError_t launch_skinny_grouped(int site, SkinnyGroup<TB, AL, Epi> grp, const int64_t* n_rows,
@@ -613,7 +587,10 @@ size_t group_ws_bytes(const pifa_group* g, int64_t M) {
 }
 
 size_t group_part_bytes(const pifa_group* g, int64_t M) {
-    return M <= kDecodeMaxM ? 0 : split_bytes(M, g->r_pad, g->d_in);
+    if (M <= kDecodeMaxM) return 0;
+    size_t b = split_bytes(M, g->r_pad, g->d_in);
+    for (const pifa_layer* h : g->layers) b = std::max(b, split_bytes(M, h->n_np, h->r_pad));
+    return b;
 }
 
 void free_dense(dense_layer* h) {
@@ -1733,19 +1710,22 @@ pifa_status pifa_group_forward(pifa_group_handle g, const void* X, void* Y, int6
                                                        y_scale, g->overflow, M),
                                 (float*)g->part.ptr, st);
     if (e != hipSuccess) return PIFA_ERR_HIP;
-    GemmGroup<f16, EpiNP> grp{};
-    grp.M = M;
+    // The non-pivot products: one launch per member, as its own pifa_forward
+    // runs it.  Both products are compute-bound at these sizes; one launch
+    // over all members measured slower (372 against 2 x 165 us for the
+    // LLaMA-7B gate and up projections at M = 4096).
     for (int i = 0; i < g->n; ++i) {
         const pifa_layer* h = g->layers[(size_t)i];
         if (h->n_np == 0) continue;
         const float out_scale = std::ldexp(1.0f, -(g->y_log2 + h->c_log2));
-        grp.p[grp.n++] = {yp + g->r_off[(size_t)i], g->r_pad, (const f16*)h->C, h->n_np, h->r_pad,
-                          make_epi<bf16, kWsNone>(y, g->d_out, h->npiv, h->n_np, out_scale, nullptr, 0, 0, 1.f,
-                                                  nullptr, M)};
+        e = launch_gemm<f16, true>(kSiteGroupGemm2, yp + g->r_off[(size_t)i], g->r_pad, M, (const f16*)h->C, 0,
+                                   h->n_np, h->r_pad,
+                                   make_epi<bf16, kWsNone>(y, g->d_out, h->npiv, h->n_np, out_scale, nullptr, 0, 0,
+                                                           1.f, nullptr, M),
+                                   (float*)g->part.ptr, st);
+        if (e != hipSuccess) return PIFA_ERR_HIP;
     }
-    if (grp.n == 0) return PIFA_OK;
-    e = launch_gemm_grouped(kSiteGroupGemm2, grp, st);
-    return e == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
+    return PIFA_OK;
 }
 
 pifa_status pifa_build_f64(const double* W, pifa_dims dims, double* W_p, double* C, int32_t* pivot_idx,
