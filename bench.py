@@ -251,7 +251,8 @@ def gpu_built_layer(d_in, d_out, r, seed):
 
 def measure_group(seed):
     """LLaMA-7B MLP gate and up projections (two 4096 -> 11008 layers, r = 2048)
-    as one group (shared X read once, one launch per product) against two
+    as one group (X read once for both pivot products; one launch for both
+    non-pivot products at M = 1, one per layer at M = 4096) against two
     separate pifa_forward calls, at M = 4096 and at M = 1."""
     import torch
     from paper_2501_19090_amd import inputs, pifa
