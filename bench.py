@@ -474,6 +474,10 @@ def main():
     ap.add_argument("--profile-run", action="store_true",
                     help="only the headline forward (warmup, then steps) plus one calibration copy of 512 MiB "
                          "(for rocprofv3 runs)")
+    ap.add_argument("--profile-path", choices=("forward", "backward", "reconstruct"), default="forward",
+                    help="with --profile-run: what to run -- the forward, the backward pass at M = 4096 "
+                         "(warmup, then steps), or the online reconstruction as the benchmark times it "
+                         "(calibration sums over 2048-token batches, then one solve)")
     args = ap.parse_args()
     if not 1 <= args.profile_m <= 4096:
         ap.error("--profile-m must be in 1..4096")
@@ -489,6 +493,11 @@ def main():
         sys.exit(1)
     pifa.lib()  # fail loudly if the HIP library is missing
     torch.cuda.set_device(0)
+
+    if args.profile_run and args.profile_path == "reconstruct":
+        t = measure_reconstruct()
+        log("profile run done: solve %.1f ms" % t["solve_ms"])
+        return
 
     d_in = d_out = 4096
     r, M = 2048, 4096
@@ -506,6 +515,18 @@ def main():
         dst = torch.empty_like(src)
         dst.copy_(src)
         torch.cuda.synchronize()
+        if args.profile_path == "backward":
+            g = torch.from_numpy(inputs.round_bf16(inputs.activations(M, d_out, 32))[0].view(np.int16)).cuda().view(
+                torch.bfloat16)
+            pifa.pifa_forward(h, x, y, M, stream)
+            dx = torch.empty((M, d_in), dtype=torch.bfloat16, device="cuda:0")
+            dwp = torch.empty((r, d_in), dtype=torch.float32, device="cuda:0")
+            dc = torch.empty((d_out - r, r), dtype=torch.float32, device="cuda:0")
+            for i in range(args.warmup + args.steps):
+                pifa.pifa_layer_backward(h, x, y, g, dx, dwp, dc, M, stream)
+            torch.cuda.synchronize()
+            log("profile run done")
+            return
         if args.profile_m != M:  # the same layer at another batch size
             M = args.profile_m
             x = x[:M].contiguous()
