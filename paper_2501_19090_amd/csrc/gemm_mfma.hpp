@@ -93,30 +93,44 @@ struct Mfma<f16> {
 //  1. The dispatcher sends consecutive workgroup ids round-robin to the 8
 //     XCDs; undo that so each XCD gets a contiguous range of tiles (tiles
 //     that share A rows then share that XCD's L2).
-//  2. Within the range, walk tiles in bands of `kGroupM` tile rows so that
-//     concurrently resident tiles reuse both A and B panels.
+//  2. Within the range, walk tiles in bands of `group` tile rows, column by
+//     column, so that one XCD's range is a block of about group x (range /
+//     group) tiles.  Its L2 then fills group A panels of BM rows and
+//     range / group B panels of BN rows; `band_rows` picks the power of two
+//     that makes the two byte counts about equal, which minimises their sum
+//     (256 x 128 tiles of a 4096 x 2048 product: 4 x 8 tiles, 16 MB of
+//     panels per XCD against 20 MB for 8 x 4).
 constexpr int kXcds = 8;
-constexpr int kGroupM = 8;
 
 // Step 1 on its own: consecutive ids of one XCD become a contiguous range.
 __device__ __forceinline__ int64_t xcd_remap(int64_t bid, int64_t ntiles) {
     return ntiles % kXcds == 0 ? (bid % kXcds) * (ntiles / kXcds) + bid / kXcds : bid;
 }
 
-// Step 2 on its own: tile t of a tiles_m x tiles_n grid, in bands of kGroupM tile rows.
-__device__ __forceinline__ void band_coords(int64_t t, int64_t tiles_m, int64_t tiles_n, int64_t& tm,
-                                            int64_t& tn) {
-    const int64_t band = (int64_t)kGroupM * tiles_n;
-    const int64_t first_m = (t / band) * kGroupM;
-    const int64_t rows = (tiles_m - first_m) < kGroupM ? (tiles_m - first_m) : kGroupM;
+template <int BM, int BN>
+__device__ __forceinline__ int64_t band_rows(int64_t tiles_m, int64_t ntiles) {
+    const int64_t per_xcd = ntiles % kXcds == 0 ? ntiles / kXcds : ntiles;
+    int64_t g = 1;
+    while (2 * g <= tiles_m && 4 * g * g * BM <= per_xcd * BN) g *= 2;
+    return g;
+}
+
+// Step 2 on its own: tile t of a tiles_m x tiles_n grid, in bands of `group` tile rows.
+__device__ __forceinline__ void band_coords(int64_t t, int64_t tiles_m, int64_t tiles_n, int64_t group,
+                                            int64_t& tm, int64_t& tn) {
+    const int64_t band = group * tiles_n;
+    const int64_t first_m = (t / band) * group;
+    const int64_t rows = (tiles_m - first_m) < group ? (tiles_m - first_m) : group;
     const int64_t in_band = t % band;
     tm = first_m + in_band % rows;
     tn = in_band / rows;
 }
 
-__device__ __forceinline__ void tile_coords(int64_t bid, int64_t tiles_m, int64_t tiles_n,
-                                            int64_t& tm, int64_t& tn) {
-    band_coords(xcd_remap(bid, tiles_m * tiles_n), tiles_m, tiles_n, tm, tn);
+template <int BM, int BN>
+__device__ __forceinline__ void tile_coords(int64_t bid, int64_t tiles_m, int64_t tiles_n, int64_t& tm,
+                                            int64_t& tn) {
+    const int64_t ntiles = tiles_m * tiles_n;
+    band_coords(xcd_remap(bid, ntiles), tiles_m, tiles_n, band_rows<BM, BN>(tiles_m, ntiles), tm, tn);
 }
 
 // Offset past every buffer range: the load returns 0 without a branch.
@@ -330,7 +344,7 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_nt_mfma(const T* __restric
                                                              int64_t ldb, int64_t N, int64_t K,
                                                              int64_t k_split, Epi epi) {
     int64_t tm, tn;
-    tile_coords(blockIdx.x, ceil_div(M, BM), ceil_div(N, BN), tm, tn);
+    tile_coords<BM, BN>(blockIdx.x, ceil_div(M, BM), ceil_div(N, BN), tm, tn);
     if constexpr (std::is_same<Epi, SplitEpi>::value) {
         const int64_t kbeg = (int64_t)blockIdx.y * k_split;
         const int64_t kend = (kbeg + k_split) < K ? (kbeg + k_split) : K;
