@@ -137,6 +137,27 @@ def test_integer_layers_bitexact_large_tiles(dims):
             lay.close()
 
 
+@pytest.mark.parametrize("M", [1, 2, 3, 4, 5])
+def test_integer_layers_bitexact_long_weight_streams(M):
+    """Decode rows against weight streams long enough for the streaming decode
+    kernel: W_p 1536 x 8192 (96 groups of 16 rows, each split over two
+    workgroups, x 64 blocks of 128 K) and C 12800 x 1536 (800 groups x 12
+    blocks, fewer than one per wave).  M = 5 takes the kernel with one
+    workgroup per group.  Integer data: bit-exact against the oracle."""
+    d_in, d_out, r = 8192, 14336, 1536
+    piv, npiv = inputs.random_partition(d_out, r, seed=11)
+    X, Wp, C = inputs.integer_layer(d_in, d_out, r, M, seed=M + 40)
+    lay = DeviceLayer(piv, npiv, Wp, C, "bf16")
+    try:
+        st, x64 = inputs.round_to(X, "bf16")
+        y = from_dev(lay.forward(to_dev(st)))
+        ref = lay.oracle(x64)
+        assert np.abs(ref).max() <= 256
+        assert np.array_equal(y, ref), (M, np.abs(y - ref).max())
+    finally:
+        lay.close()
+
+
 def test_layout_probe_large_m():
     """Probe weights at the attention shape with M = 4096 rows."""
     name = "B_attn_4096"
