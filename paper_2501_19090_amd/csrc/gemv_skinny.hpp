@@ -164,119 +164,6 @@ __global__ __launch_bounds__(WAVES* kWave) void skinny_packed(AL al, const TB* _
                                                                (int)(blockIdx.x % PARTS));
 }
 
-// Streaming variant for a long weight stream (many 16-row groups, or a deep
-// K) and at most kStreamRows activation rows.  A workgroup walks a list of
-// items, each one pass of its waves over STEP = WAVES * UNROLL blocks of 128 K
-// values of one unit (a 16-row group, or part of one as above), and issues the
-// weight loads of the next item before the MFMAs of the current one.  The
-// weight stream then stays in flight across passes, units and reductions
-// instead of restarting with every workgroup.  The activation rows are staged
-// in LDS first, as the MFMA operand chunks al.load produces, so the MFMA loop
-// issues no global loads of its own: global loads complete in issue order as
-// far as the wait counters go, and an activation load issued after the
-// prefetch would make the MFMAs wait for the prefetch as well.
-//
-// Grid: any number of workgroups; workgroup b takes units b, b + gridDim.x, ...
-// Dynamic LDS: skinny_stream_lds(M, K, OPS, WAVES) bytes.
-constexpr int kStreamRows = 4;
-
-__host__ __device__ inline int64_t skinny_stream_lds(int64_t M, int64_t K, int ops, int waves) {
-    return M * packed_kblocks(K) * (kSkinnyStepK / 8) * ops * 16 + 2 * (int64_t)waves * kWave * 16;
-}
-
-template <typename TB, int WAVES, int UNROLL, int PARTS, typename AL, typename Epi>
-__global__ __launch_bounds__(WAVES* kWave) void skinny_stream(AL al, const TB* __restrict__ B, int64_t units,
-                                                               int64_t K, Epi epi) {
-    static_assert(PARTS == 1 || PARTS == 2 || PARTS == 4, "parts of a 16-row group");
-    constexpr int OPS = AL::kOps;
-    constexpr int STEP = WAVES * UNROLL;
-    constexpr int PROWS = kSkinnyRows / PARTS;
-    extern __shared__ u32x4 xs[];  // [M][KC][OPS] operand chunks, then [2][WAVES][kWave] f32x4
-    const int lane = threadIdx.x & (kWave - 1);
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-    const int64_t KB = packed_kblocks(K);
-    const int64_t KC = KB * (kSkinnyStepK / 8);  // 8-value chunks per staged row
-    const int M = (int)al.M;
-    f32x4* red = reinterpret_cast<f32x4*>(xs + M * KC * OPS);
-
-    const int row = lane & 15;
-    const bool live = row < M;
-    // LDS chunk of (row, K values 32 * (lane / 16) + 8 * c of block b): lds_lane + (16 * b + c) * OPS
-    const int lds_lane = (row * (int)KC + (lane >> 4) * 4) * OPS;
-    const int64_t passes = ceil_div(KB, (int64_t)STEP);
-    const int64_t my_units = (int64_t)blockIdx.x < units ? ceil_div(units - (int64_t)blockIdx.x, (int64_t)gridDim.x) : 0;
-    const int64_t items = my_units * passes;
-
-    // weights of item j (zeros past the last item: a masked lane's offset is
-    // past the buffer range, so the load returns 0 without a memory access)
-    auto fetch = [&](int64_t j, u32x4(&bw)[UNROLL][4]) {
-        const int64_t unit = blockIdx.x + (j / passes) * gridDim.x;
-        const bool mine = j < items && (PARTS == 1 || row / PROWS == (int)(unit % PARTS));
-        const auto rs = make_rsrc31(B + (unit / PARTS) * KB * (kPackChunks * 8), KB * kPackChunks * 16);
-        const int64_t kb0 = (j % passes) * STEP + wave;
-#pragma unroll
-        for (int u = 0; u < UNROLL; ++u) {
-            const int64_t b = kb0 + (int64_t)u * WAVES;
-            const uint32_t off = (mine && b < KB) ? (uint32_t)((b * kPackChunks + lane) * 16) : kMaskedOffset;
-#pragma unroll
-            for (int c = 0; c < 4; ++c) bw[u][c] = load16(rs, off + c * kWave * 16);
-        }
-    };
-    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-    int par = 0;
-    auto step = [&](int64_t j, const u32x4(&bw)[UNROLL][4]) {
-        const int64_t kb0 = (j % passes) * STEP + wave;
-#pragma unroll
-        for (int u = 0; u < UNROLL; ++u) {
-            const int64_t b = kb0 + (int64_t)u * WAVES;
-#pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                u32x4 aw[OPS];
-#pragma unroll
-                for (int o = 0; o < OPS; ++o)
-                    aw[o] = (live && b < KB) ? xs[lds_lane + ((int)b * (kSkinnyStepK / 8) + c) * OPS + o] : zero16();
-#pragma unroll
-                for (int o = 0; o < OPS; ++o) acc = Mfma<TB>::mma16(aw[o], bw[u][c], acc);
-            }
-        }
-        if (j < items && j % passes == passes - 1) {
-            // the unit is complete: sum the waves and store (as skinny_finish)
-            red[(par * WAVES + wave) * kWave + lane] = acc;
-            __syncthreads();
-            if (wave == 0) {
-                f32x4 tot = red[par * WAVES * kWave + lane];
-#pragma unroll
-                for (int w = 1; w < WAVES; ++w) tot += red[(par * WAVES + w) * kWave + lane];
-                const int64_t unit = blockIdx.x + (j / passes) * gridDim.x;
-                const int part = (int)(unit % PARTS);
-                if ((unsigned)((lane & 15) - part * PROWS) < (unsigned)PROWS) {
-                    const auto c = epi.col((unit / PARTS) * kSkinnyRows + (lane & 15));
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) epi.store(4 * (lane >> 4) + v, c, tot[v]);
-                }
-            }
-            acc = f32x4{0.f, 0.f, 0.f, 0.f};
-            par ^= 1;
-        }
-    };
-    // the first weights are in flight while the rows are staged
-    u32x4 w0[UNROLL][4], w1[UNROLL][4];
-    fetch(0, w0);
-    for (int64_t i = threadIdx.x; i < M * KC; i += WAVES * kWave) {
-        u32x4 v[OPS];
-        al.load((int)(i / KC), (i % KC) * 8, K, v);
-#pragma unroll
-        for (int o = 0; o < OPS; ++o) xs[i * OPS + o] = v[o];
-    }
-    __syncthreads();  // staged rows visible
-    for (int64_t j = 0; j < items; j += 2) {
-        fetch(j + 1, w1);
-        step(j, w0);
-        fetch(j + 2, w0);
-        step(j + 1, w1);
-    }
-}
-
 // Several weight streams with the same activation rows in one launch
 // (grouped layers): problem p owns workgroups [start[p], start[p + 1]).
 constexpr int kMaxSkinnyGroup = 8;
@@ -303,6 +190,159 @@ __global__ __launch_bounds__(WAVES* kWave) void skinny_packed_grouped(SkinnyGrou
     while (q + 1 < grp.n && b >= grp.start[q + 1]) ++q;
     const SkinnyProblem<TB, AL, Epi>& p = grp.p[q];
     skinny_packed_group<TB, WAVES, UNROLL, MT, 1, AL, Epi>(p.al, p.B, p.K, p.epi, b - grp.start[q]);
+}
+
+// Streaming variant for long weight streams (many 16-row groups, or a deep
+// K) and at most kStreamRows activation rows.  The problems of a SkinnyGroup
+// (one, or the members of a grouped layer, each with its own K) are cut into
+// units: a 16-row group, or 1 / PARTS of one as above; problem q owns units
+// [start[q], start[q + 1]).  Workgroup b takes units b, b + gridDim.x, ... and
+// walks them in passes of its waves over STEP = WAVES * UNROLL blocks of 128 K
+// values, issuing the weight loads of the next pass before the MFMAs of the
+// current one, so the stream stays in flight across passes, units, problems
+// and reductions instead of restarting with every workgroup.
+//
+// Every problem's activation rows are staged in LDS first, as the MFMA
+// operand chunks al.load produces, so the MFMA loop issues no global loads of
+// its own: global loads complete in issue order as far as the wait counters
+// go, and an activation load issued after the prefetch would make the MFMAs
+// wait for the prefetch as well.  With 16 waves, UNROLL 1 and the same PARTS
+// the sums run in the order of skinny_packed_group (bit-identical results).
+//
+// Dynamic LDS: skinny_stream_lds(M, sum of the problems' K rounded up to 128,
+// OPS, WAVES) bytes.  Every problem has the same activation rows M.
+constexpr int kStreamRows = 4;
+
+__host__ __device__ inline int64_t skinny_stream_lds(int64_t M, int64_t k_blocks_total, int ops, int waves) {
+    return M * k_blocks_total * (kSkinnyStepK / 8) * ops * 16 + 2 * (int64_t)waves * kWave * 16;
+}
+
+template <typename TB, int WAVES, int UNROLL, int PARTS, typename AL, typename Epi>
+__global__ __launch_bounds__(WAVES* kWave) void skinny_stream(SkinnyGroup<TB, AL, Epi> grp) {
+    static_assert(PARTS == 1 || PARTS == 2 || PARTS == 4, "parts of a 16-row group");
+    constexpr int OPS = AL::kOps;
+    constexpr int STEP = WAVES * UNROLL;
+    constexpr int PROWS = kSkinnyRows / PARTS;
+    constexpr int CPB = kSkinnyStepK / 8;  // 8-value chunks per 128-wide K block
+    extern __shared__ u32x4 xs[];          // per problem [M][KB * CPB][OPS] chunks, then [2][WAVES][kWave] f32x4
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int M = (int)grp.p[0].al.M;
+    const int64_t units = grp.start[grp.n];
+    int64_t kb_total = 0;
+    for (int q = 0; q < grp.n; ++q) kb_total += packed_kblocks(grp.p[q].K);
+    f32x4* red = reinterpret_cast<f32x4*>(xs + M * kb_total * CPB * OPS);
+    const int row = lane & 15;
+    const bool live = row < M;
+
+    // iteration state (uniform): unit u of problem q, pass p; u >= units ends
+    struct It {
+        int64_t u;
+        int q;
+        int64_t p;
+    };
+    auto settle = [&](It s) {
+        while (s.q + 1 < grp.n && s.u >= grp.start[s.q + 1]) ++s.q;
+        return s;
+    };
+    auto next = [&](It s) {
+        if (s.p + 1 < ceil_div(packed_kblocks(grp.p[s.q].K), (int64_t)STEP)) {
+            ++s.p;
+            return s;
+        }
+        s.u += gridDim.x;
+        s.p = 0;
+        return settle(s);
+    };
+    // weights of one pass (zeros past the last unit: a masked lane's offset is
+    // past the buffer range, so the load returns 0 without a memory access)
+    auto fetch = [&](const It& s, u32x4(&bw)[UNROLL][4]) {
+        const SkinnyProblem<TB, AL, Epi>& P = grp.p[s.q];
+        const int64_t KB = packed_kblocks(P.K);
+        const int64_t lu = s.u - grp.start[s.q];
+        const bool mine = s.u < units && (PARTS == 1 || row / PROWS == (int)(lu % PARTS));
+        const auto rs = make_rsrc31(P.B + (lu / PARTS) * KB * (kPackChunks * 8), KB * kPackChunks * 16);
+        const int64_t kb0 = s.p * STEP + wave;
+#pragma unroll
+        for (int u = 0; u < UNROLL; ++u) {
+            const int64_t b = kb0 + (int64_t)u * WAVES;
+            const uint32_t off = (mine && b < KB) ? (uint32_t)((b * kPackChunks + lane) * 16) : kMaskedOffset;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) bw[u][c] = load16(rs, off + c * kWave * 16);
+        }
+    };
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+    int par = 0;
+    auto step = [&](const It& s, const u32x4(&bw)[UNROLL][4]) {
+        const SkinnyProblem<TB, AL, Epi>& P = grp.p[s.q];
+        const int64_t KB = packed_kblocks(P.K);
+        int64_t kb_before = 0;  // staged K blocks of the problems before q
+        for (int q = 0; q < s.q; ++q) kb_before += packed_kblocks(grp.p[q].K);
+        // chunk (row, K values 32 * (lane / 16) + 8 * c of block b): lds_lane + (CPB * b + c) * OPS
+        const int lds_lane = (int)((M * kb_before * CPB + row * KB * CPB + (lane >> 4) * 4) * OPS);
+        const int64_t kb0 = s.p * STEP + wave;
+#pragma unroll
+        for (int u = 0; u < UNROLL; ++u) {
+            const int64_t b = kb0 + (int64_t)u * WAVES;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                u32x4 aw[OPS];
+#pragma unroll
+                for (int o = 0; o < OPS; ++o)
+                    aw[o] = (live && b < KB) ? xs[lds_lane + ((int)b * CPB + c) * OPS + o] : zero16();
+#pragma unroll
+                for (int o = 0; o < OPS; ++o) acc = Mfma<TB>::mma16(aw[o], bw[u][c], acc);
+            }
+        }
+        if (s.u < units && s.p + 1 == ceil_div(KB, (int64_t)STEP)) {
+            // the unit is complete: sum the waves and store (as skinny_finish)
+            red[(par * WAVES + wave) * kWave + lane] = acc;
+            __syncthreads();
+            if (wave == 0) {
+                f32x4 tot = red[par * WAVES * kWave + lane];
+#pragma unroll
+                for (int w = 1; w < WAVES; ++w) tot += red[(par * WAVES + w) * kWave + lane];
+                const int64_t lu = s.u - grp.start[s.q];
+                const int part = (int)(lu % PARTS);
+                if ((unsigned)((lane & 15) - part * PROWS) < (unsigned)PROWS) {
+                    const auto c = P.epi.col((lu / PARTS) * kSkinnyRows + (lane & 15));
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) P.epi.store(4 * (lane >> 4) + v, c, tot[v]);
+                }
+            }
+            acc = f32x4{0.f, 0.f, 0.f, 0.f};
+            par ^= 1;
+        }
+    };
+
+    // the first weights are in flight while the rows are staged
+    It cur = settle(It{(int64_t)blockIdx.x, 0, 0});
+    It nxt = next(cur);
+    u32x4 w0[UNROLL][4], w1[UNROLL][4];
+    fetch(cur, w0);
+    for (int q = 0, off = 0; q < grp.n; ++q) {
+        const SkinnyProblem<TB, AL, Epi>& P = grp.p[q];
+        const int64_t KC = packed_kblocks(P.K) * CPB;
+        for (int64_t i = threadIdx.x; i < M * KC; i += WAVES * kWave) {
+            u32x4 v[OPS];
+            P.al.load((int)(i / KC), (i % KC) * 8, P.K, v);
+#pragma unroll
+            for (int o = 0; o < OPS; ++o) xs[off + i * OPS + o] = v[o];
+        }
+        off += (int)(M * KC * OPS);
+    }
+    __syncthreads();  // staged rows visible
+    while (cur.u < units) {
+        fetch(nxt, w1);
+        step(cur, w0);
+        cur = nxt;
+        nxt = next(nxt);
+        if (cur.u >= units) break;
+        fetch(nxt, w0);
+        step(cur, w1);
+        cur = nxt;
+        nxt = next(nxt);
+    }
 }
 
 // Row-major weights (row stride ldb), for caller-owned matrices.

@@ -344,23 +344,38 @@ void skinny_launch(const AL& al, const TB* B, int64_t N, int64_t K, const Epi& e
 constexpr int64_t kStreamMinBlocks = 6144;
 constexpr int64_t kStreamMaxLds = 65536;
 
+// grp.start[] counts 16-row groups per problem; the kernel's units are
+// PARTS per group
 template <typename TB, int PARTS, typename AL, typename Epi>
-void skinny_stream_launch(const AL& al, const TB* B, int64_t N, int64_t K, const Epi& epi, hipStream_t st) {
-    const int64_t units = PARTS * packed_groups(N);
+void skinny_stream_launch(SkinnyGroup<TB, AL, Epi> grp, int64_t k_blocks_total, hipStream_t st) {
+    for (int q = 0; q <= grp.n; ++q) grp.start[q] *= PARTS;
+    const int64_t units = grp.start[grp.n];
     const int64_t per_wg = ceil_div(units, (int64_t)kCus);
     hipLaunchKernelGGL((skinny_stream<TB, 16, 1, PARTS, AL, Epi>), dim3((unsigned)ceil_div(units, per_wg)),
-                       dim3(16 * kWave), (size_t)skinny_stream_lds(al.M, K, AL::kOps, 16), st, al, B, units, K,
-                       epi);
+                       dim3(16 * kWave), (size_t)skinny_stream_lds(grp.p[0].al.M, k_blocks_total, AL::kOps, 16), st,
+                       grp);
+}
+
+// Whether a weight stream of `blocks` 16 x 128 blocks over k_blocks_total
+// staged K blocks takes the streaming kernel.
+inline bool use_stream(int64_t M, int64_t blocks, int64_t k_blocks_total, int ops) {
+    return M <= kStreamRows && blocks >= kStreamMinBlocks &&
+           skinny_stream_lds(M, k_blocks_total, ops, 16) <= kStreamMaxLds;
 }
 
 template <typename TB, int MT, typename AL, typename Epi>
 void skinny_packed_mt(const AL& al, const TB* B, int64_t N, int64_t K, const Epi& epi, hipStream_t st) {
     const int64_t groups = packed_groups(N);
     if constexpr (MT == 1) {
-        if (al.M <= kStreamRows && groups * packed_kblocks(K) >= kStreamMinBlocks &&
-            skinny_stream_lds(al.M, K, AL::kOps, 16) <= kStreamMaxLds) {
-            if (groups <= 128) return skinny_stream_launch<TB, 2>(al, B, N, K, epi, st);
-            return skinny_stream_launch<TB, 1>(al, B, N, K, epi, st);
+        const int64_t KB = packed_kblocks(K);
+        if (use_stream(al.M, groups * KB, KB, AL::kOps)) {
+            SkinnyGroup<TB, AL, Epi> one;
+            one.p[0] = SkinnyProblem<TB, AL, Epi>{al, B, K, epi};
+            one.n = 1;
+            one.start[0] = 0;
+            one.start[1] = groups;
+            if (groups <= 128) return skinny_stream_launch<TB, 2>(one, KB, st);
+            return skinny_stream_launch<TB, 1>(one, KB, st);
         }
         const SkinnyShape c = skinny_shape(al.M, groups, packed_kblocks(K));
         const int key = c.waves * 100 + c.unroll * 10 + c.parts;
@@ -402,11 +417,19 @@ hipError_t launch_skinny_grouped(int site, SkinnyGroup<TB, AL, Epi> grp, const i
     grp.start[0] = 0;
     for (int q = 0; q < grp.n; ++q) grp.start[q + 1] = grp.start[q] + packed_groups(n_rows[q]);
     if (grp.start[grp.n] == 0) return hipSuccess;
-    int64_t KB = 0;
-    for (int q = 0; q < grp.n; ++q) KB = std::max(KB, packed_kblocks(grp.p[q].K));
+    int64_t KB = 0, kb_total = 0, blocks = 0;
+    for (int q = 0; q < grp.n; ++q) {
+        KB = std::max(KB, packed_kblocks(grp.p[q].K));
+        kb_total += packed_kblocks(grp.p[q].K);
+        blocks += (grp.start[q + 1] - grp.start[q]) * packed_kblocks(grp.p[q].K);
+    }
+    TimedLaunch timed(site, st);
+    if (use_stream(grp.p[0].al.M, blocks, kb_total, AL::kOps)) {
+        skinny_stream_launch<TB, 1>(grp, kb_total, st);
+        return hipGetLastError();
+    }
     const SkinnyShape c = skinny_shape(grp.p[0].al.M, grp.start[grp.n], KB);  // one workgroup per group
     const dim3 grid((unsigned)grp.start[grp.n]);
-    TimedLaunch timed(site, st);
     if (c.waves == 16 && c.unroll == 2)
         hipLaunchKernelGGL((skinny_packed_grouped<TB, 16, 2, 1, AL, Epi>), grid, dim3(16 * kWave), 0, st, grp);
     else if (c.waves == 16)
