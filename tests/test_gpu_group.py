@@ -136,6 +136,29 @@ def test_group_parity_vs_oracle_mlp_shape():
         grp.close()
 
 
+def test_group_long_streams_equal_member_forwards_bitexact():
+    """Decode rows where the grouped weight streams are long enough for the
+    streaming kernel (MLP up shape, C 8960 x 2048, plus a rank-1229 member
+    with a different K): each block equals its member's own forward bit for
+    bit; M = 5 takes the one-workgroup-per-group kernels."""
+    d_in = 4096
+    members = []
+    for name in ("C_mlp_up_4096x11008", "E_sweep_r30"):
+        piv, npiv, Wp, C, *_ = config_layer(name)
+        members.append(DeviceLayer(piv, npiv, Wp, C, "bf16"))
+    grp = DeviceGroup(members)
+    try:
+        for M in (1, 3, 4, 5):
+            x_dev, _ = activations(M, d_in, 300 + M, "bf16")
+            y = grp.forward(x_dev).cpu()
+            for i, m in enumerate(members):
+                ref = m.forward(x_dev).cpu()
+                blk = y[:, grp.offsets[i]:grp.offsets[i + 1]]
+                assert torch_mod().equal(blk.view(torch_mod().int16), ref.view(torch_mod().int16)), (M, i)
+    finally:
+        grp.close()
+
+
 def test_group_overflow_counted_and_scale_applies():
     from paper_2501_19090_amd import pifa
     d_in = 256
