@@ -190,9 +190,14 @@ enum TileCfg : int { kTile256x256 = 0, kTile256x192 = 1, kTile256x128 = 2, kTile
 // bytes, written and read back once) at most the operand bytes ((M + N) K 2)
 // and capped at kMaxPartialBytes.  Measured on the LLaMA-7B attention
 // products at M = 17..256: more splits than this fill more CUs but lose more
-// to the partials and the short K loops than they gain.
+// to the partials and the short K loops than they gain.  No split when one
+// split's partials (M N 4 bytes) exceed kMaxSplitSliceBytes: the tall, narrow
+// products of the rank sweep at M = 4096 (N = 410..832 wide, 128..224 tiles
+// of 128 x 128) ran 17-34% faster unsplit with CUs left idle than split in
+// two (the r = 80% non-pivot product 38 against 57 us).
 constexpr int64_t kMaxSplit = 16;
 constexpr int64_t kMaxPartialBytes = 256ll << 20;
+constexpr int64_t kMaxSplitSliceBytes = 6ll << 20;
 
 struct SplitPlan {
     int64_t splits, k_split;
@@ -200,7 +205,7 @@ struct SplitPlan {
 
 SplitPlan split_plan(int64_t tiles, int64_t M, int64_t N, int64_t K) {
     SplitPlan p{1, K};
-    if (tiles >= kCus) return p;
+    if (tiles >= kCus || M * N * 4 > kMaxSplitSliceBytes) return p;
     int64_t s = std::min<int64_t>({ceil_div(kCus, tiles), K / (4 * kGemmBK), kMaxSplit,
                                    std::max<int64_t>(1, K * (M + N) / (2 * std::max<int64_t>(1, M * N))),
                                    kMaxPartialBytes / std::max<int64_t>(1, M * N * 4)});
