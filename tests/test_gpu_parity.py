@@ -137,14 +137,17 @@ def test_integer_layers_bitexact_large_tiles(dims):
             lay.close()
 
 
+@pytest.mark.parametrize("dims", [(8192, 14336, 1536), (8200, 14336, 1500)])
 @pytest.mark.parametrize("M", [1, 2, 3, 4, 5])
-def test_integer_layers_bitexact_long_weight_streams(M):
+def test_integer_layers_bitexact_long_weight_streams(dims, M):
     """Decode rows against weight streams long enough for the streaming decode
     kernel: W_p 1536 x 8192 (96 groups of 16 rows, each split over two
     workgroups, x 64 blocks of 128 K) and C 12800 x 1536 (800 groups x 12
-    blocks, fewer than one per wave).  M = 5 takes the kernel with one
-    workgroup per group.  Integer data: bit-exact against the oracle."""
-    d_in, d_out, r = 8192, 14336, 1536
+    blocks, fewer than one per wave); the second layer has a ragged last K
+    block in W_p (d_in = 8200) and 1500 pivots padded to 1536.  M = 5 takes
+    the kernel with one workgroup per group.  Integer data: bit-exact against
+    the oracle."""
+    d_in, d_out, r = dims
     piv, npiv = inputs.random_partition(d_out, r, seed=11)
     X, Wp, C = inputs.integer_layer(d_in, d_out, r, M, seed=M + 40)
     lay = DeviceLayer(piv, npiv, Wp, C, "bf16")
