@@ -478,9 +478,16 @@ def main():
                     help="with --profile-run: what to run -- the forward, the backward pass at M = 4096 "
                          "(warmup, then steps), or the online reconstruction as the benchmark times it "
                          "(calibration sums over 2048-token batches, then one solve)")
+    ap.add_argument("--profile-config", default="B_attn_4096",
+                    help="with --profile-run and the forward path: the layer of the named configuration "
+                         "(e.g. D_70b_up_8192x28672), its weights rotated over copies larger than the "
+                         "Infinity Cache")
     args = ap.parse_args()
     if not 1 <= args.profile_m <= 4096:
         ap.error("--profile-m must be in 1..4096")
+    from paper_2501_19090_amd import inputs as _inputs
+    if args.profile_config not in _inputs.CONFIGS:
+        ap.error("--profile-config must be one of: " + ", ".join(sorted(_inputs.CONFIGS)))
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only (run with --gpus 1): sharding the PIFA layer over "
               "several GPUs is not implemented.", file=sys.stderr)
@@ -497,6 +504,22 @@ def main():
     if args.profile_run and args.profile_path == "reconstruct":
         t = measure_reconstruct()
         log("profile run done: solve %.1f ms" % t["solve_ms"])
+        return
+
+    if args.profile_run and args.profile_path == "forward" and args.profile_config != "B_attn_4096":
+        cfg, lay, d_in, d_out, r, _, _, _ = inputs.CONFIGS[args.profile_config]
+        wl = Workload(d_in, d_out, r, inputs.config_seed(cfg, lay))
+        M = args.profile_m
+        wl.ensure_copies()
+        wl.reserve(M)
+        stream = torch.cuda.current_stream().cuda_stream
+        x = torch.from_numpy(inputs.round_bf16(inputs.activations(M, d_in, 99))[0].view(np.int16)).cuda().view(
+            torch.bfloat16)
+        y = torch.empty((M, d_out), dtype=torch.bfloat16, device="cuda:0")
+        for i in range(args.warmup + args.steps):
+            pifa.pifa_forward(wl.pifa_h[i % len(wl.pifa_h)], x, y, M, stream)
+        torch.cuda.synchronize()
+        log("profile run done: %s, M = %d, %d weight copies" % (args.profile_config, M, len(wl.pifa_h)))
         return
 
     d_in = d_out = 4096
