@@ -282,8 +282,15 @@ hipError_t launch_gemm(int site, const T* A, int64_t lda, int64_t M, const T* B,
     } else {
         // too few tiles for the chip even at 128 x 128: split K
         const int64_t t128x128 = ceil_div(M, 128) * ceil_div(N, 128);
+        const int64_t t128x64 = ceil_div(M, 128) * ceil_div(N, 64);
         const SplitPlan p = partials ? split_plan(t128x128, M, N, K) : SplitPlan{1, K};
-        if (p.splits == 1) {
+        if (p.splits == 1 && 2 * t128x128 <= kCus && t128x64 <= kCus) {
+            // unsplit and at most half the chip busy with 128 x 128 tiles:
+            // 128 x 64 tiles fill it in one round (the rank sweep's 410-wide
+            // products at M = 4096: 224 tiles, 35 against 45 us)
+            hipLaunchKernelGGL((gemm_nt_mfma<T, 128, 64, kGemmBK, 4, 2, BPACK, 2, Epi>), dim3((unsigned)t128x64),
+                               dim3(8 * kWave), 0, st, A, lda, M, B, ldb, N, K, K, epi);
+        } else if (p.splits == 1) {
             hipLaunchKernelGGL((gemm_nt_mfma<T, 128, 128, kGemmBK, 4, 2, BPACK, 2, Epi>), dim3((unsigned)t128x128),
                                dim3(8 * kWave), 0, st, A, lda, M, B, ldb, N, K, K, epi);
         } else {

@@ -116,11 +116,13 @@ def test_integer_layers_bitexact(dims, dtype):
             lay.close()
 
 
-@pytest.mark.parametrize("dims", [(2048, 4096, 2048), (1536, 2752, 1536), (2560, 4096, 2458), (1280, 4096, 1229)])
+@pytest.mark.parametrize("dims", [(2048, 4096, 2048), (1536, 2752, 1536), (2560, 4096, 2458), (1280, 4096, 1229),
+                                  (1024, 1024, 410)])
 def test_integer_layers_bitexact_large_tiles(dims):
     """M = 4096 selects the large prefill tiles (256 x 128; 256 x 192 for the
     2496-wide pivot product of r = 2458 and the 2867-wide non-pivot product
-    of r = 1229); integer data keeps every element exact, checked on sampled
+    of r = 1229; 128 x 64 for the 448-wide pivot product of r = 410, which
+    is not split); integer data keeps every element exact, checked on sampled
     rows against the oracle."""
     d_in, d_out, r = dims
     M = 4096
