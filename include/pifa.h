@@ -88,6 +88,20 @@ pifa_status pifa_validate_partition(const int32_t* pivot_idx, const int32_t* non
                                     pifa_dims dims);
 
 /*
+ * Host-only diagnostic: the output tile (tile_m x tile_n rows x columns of
+ * Y) and the number of K splits (1 = none; otherwise fp32 partial products
+ * summed by a second kernel) that a prefill product Y = A B^T of M x N
+ * outputs over K runs with (more than 16 activation rows; the products of
+ * pifa_forward, the baselines, the backward pass and the calibration sums
+ * all take this plan).  wide_epilogue = 0 for epilogues that keep per-output
+ * state (fp32 or fp64 outputs, starting values), which never take the 256 x
+ * 256 and 256 x 192 tiles.  Needs no GPU.  Returns PIFA_OK or
+ * PIFA_ERR_INVALID_ARG (a size below 1 or a null pointer).
+ */
+pifa_status pifa_gemm_plan(int64_t M, int64_t N, int64_t K, int wide_epilogue, int64_t* tile_m,
+                           int64_t* tile_n, int64_t* k_splits);
+
+/*
  * Create a PIFA layer from the output of Algorithm "Pivoting Factorization".
  *   W_p           device, r x d_in, dtype.  Row j is the weight row that
  *                 produces output column pivot_idx[j].

@@ -253,55 +253,67 @@ TileCfg pick_tile(int64_t M, int64_t N) {
     return (TileCfg)best;
 }
 
+// The tile and K split of a prefill product.  wide_ok: the epilogue fits the
+// registers the 256 x 256 and 256 x 192 tiles leave; can_split: a partials
+// buffer is available.
+struct GemmPlan {
+    int64_t bm, bn;
+    SplitPlan split;
+};
+
+GemmPlan gemm_plan(int64_t M, int64_t N, int64_t K, bool wide_ok, bool can_split) {
+    TileCfg cfg = pick_tile(M, N);
+    if (!wide_ok && (cfg == kTile256x256 || cfg == kTile256x192)) cfg = kTile256x128;
+    if (cfg == kTile256x256) return {256, 256, {1, K}};
+    if (cfg == kTile256x192) return {256, 192, {1, K}};
+    if (cfg == kTile256x128) return {256, 128, {1, K}};
+    // too few tiles for the chip even at 128 x 128: split K, or, when that
+    // does not pay and 128 x 128 tiles keep at most half the chip busy, take
+    // 128 x 64 tiles if they fill it in one round (the rank sweep's 410-wide
+    // products at M = 4096: 224 tiles, 35 against 45 us)
+    const int64_t t128x128 = ceil_div(M, 128) * ceil_div(N, 128);
+    const SplitPlan p = can_split ? split_plan(t128x128, M, N, K) : SplitPlan{1, K};
+    if (p.splits == 1 && 2 * t128x128 <= kCus && ceil_div(M, 128) * ceil_div(N, 64) <= kCus) return {128, 64, p};
+    return {128, 128, p};
+}
+
 template <typename T, bool BPACK, typename Epi>
 hipError_t launch_gemm(int site, const T* A, int64_t lda, int64_t M, const T* B, int64_t ldb,
                        int64_t N, int64_t K, Epi epi, float* partials, hipStream_t st) {
     if (M == 0 || N == 0) return hipSuccess;
     TimedLaunch timed(site, st);
-    TileCfg cfg = pick_tile(M, N);
     // epilogues that load the accumulators' starting values, or add into
     // fp64 / store fp32 outputs, need more registers than the 256 x 256 and
     // 256 x 192 tiles have left (they spill there)
     constexpr bool kWideOk = !InitEpi<Epi>::value && !std::is_same<Epi, AccF64Epi>::value &&
                              !std::is_same<Epi, ScatterEpi<float, kWsNone>>::value;
-    if (!kWideOk && (cfg == kTile256x256 || cfg == kTile256x192)) cfg = kTile256x128;
-    if (cfg == kTile256x256) {
+    const GemmPlan g = gemm_plan(M, N, K, kWideOk, partials != nullptr);
+    const dim3 grid((unsigned)(ceil_div(M, g.bm) * ceil_div(N, g.bn)));
+    if (g.bm == 256 && g.bn == 256) {
         if constexpr (kWideOk)
-            hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 256, kGemmBK, 2, 4, BPACK, 1, Epi>),
-                               dim3((unsigned)(ceil_div(M, 256) * ceil_div(N, 256))), dim3(8 * kWave), 0, st, A,
-                               lda, M, B, ldb, N, K, K, epi);
-    } else if (cfg == kTile256x192) {
+            hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 256, kGemmBK, 2, 4, BPACK, 1, Epi>), grid, dim3(8 * kWave), 0,
+                               st, A, lda, M, B, ldb, N, K, K, epi);
+    } else if (g.bm == 256 && g.bn == 192) {
         if constexpr (kWideOk)
-            hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 192, kGemmBK, 4, 2, BPACK, 2, Epi>),
-                               dim3((unsigned)(ceil_div(M, 256) * ceil_div(N, 192))), dim3(8 * kWave), 0, st, A,
-                               lda, M, B, ldb, N, K, K, epi);
-    } else if (cfg == kTile256x128) {
-        hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 128, kGemmBK, 4, 2, BPACK, 2, Epi>),
-                           dim3((unsigned)(ceil_div(M, 256) * ceil_div(N, 128))), dim3(8 * kWave), 0, st, A, lda,
-                           M, B, ldb, N, K, K, epi);
+            hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 192, kGemmBK, 4, 2, BPACK, 2, Epi>), grid, dim3(8 * kWave), 0,
+                               st, A, lda, M, B, ldb, N, K, K, epi);
+    } else if (g.bm == 256) {
+        hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 128, kGemmBK, 4, 2, BPACK, 2, Epi>), grid, dim3(8 * kWave), 0, st,
+                           A, lda, M, B, ldb, N, K, K, epi);
+    } else if (g.bn == 64) {
+        hipLaunchKernelGGL((gemm_nt_mfma<T, 128, 64, kGemmBK, 4, 2, BPACK, 2, Epi>), grid, dim3(8 * kWave), 0, st,
+                           A, lda, M, B, ldb, N, K, K, epi);
+    } else if (g.split.splits == 1) {
+        hipLaunchKernelGGL((gemm_nt_mfma<T, 128, 128, kGemmBK, 4, 2, BPACK, 2, Epi>), grid, dim3(8 * kWave), 0, st,
+                           A, lda, M, B, ldb, N, K, K, epi);
     } else {
-        // too few tiles for the chip even at 128 x 128: split K
-        const int64_t t128x128 = ceil_div(M, 128) * ceil_div(N, 128);
-        const int64_t t128x64 = ceil_div(M, 128) * ceil_div(N, 64);
-        const SplitPlan p = partials ? split_plan(t128x128, M, N, K) : SplitPlan{1, K};
-        if (p.splits == 1 && 2 * t128x128 <= kCus && t128x64 <= kCus) {
-            // unsplit and at most half the chip busy with 128 x 128 tiles:
-            // 128 x 64 tiles fill it in one round (the rank sweep's 410-wide
-            // products at M = 4096: 224 tiles, 35 against 45 us)
-            hipLaunchKernelGGL((gemm_nt_mfma<T, 128, 64, kGemmBK, 4, 2, BPACK, 2, Epi>), dim3((unsigned)t128x64),
-                               dim3(8 * kWave), 0, st, A, lda, M, B, ldb, N, K, K, epi);
-        } else if (p.splits == 1) {
-            hipLaunchKernelGGL((gemm_nt_mfma<T, 128, 128, kGemmBK, 4, 2, BPACK, 2, Epi>), dim3((unsigned)t128x128),
-                               dim3(8 * kWave), 0, st, A, lda, M, B, ldb, N, K, K, epi);
-        } else {
-            SplitEpi se{partials, M, N};
-            hipLaunchKernelGGL((gemm_nt_mfma<T, 128, 128, kGemmBK, 4, 2, BPACK, 2, SplitEpi>),
-                               dim3((unsigned)t128x128, (unsigned)p.splits), dim3(8 * kWave), 0, st, A, lda, M,
-                               B, ldb, N, K, p.k_split, se);
-            const int64_t work = M * ceil_div(N, 4);
-            hipLaunchKernelGGL((split_reduce<Epi>), dim3((unsigned)std::min<int64_t>(ceil_div(work, 256), 65536)),
-                               dim3(256), 0, st, (const float*)partials, (int)p.splits, M, N, epi);
-        }
+        SplitEpi se{partials, M, N};
+        hipLaunchKernelGGL((gemm_nt_mfma<T, 128, 128, kGemmBK, 4, 2, BPACK, 2, SplitEpi>),
+                           dim3(grid.x, (unsigned)g.split.splits), dim3(8 * kWave), 0, st, A, lda, M, B, ldb, N, K,
+                           g.split.k_split, se);
+        const int64_t work = M * ceil_div(N, 4);
+        hipLaunchKernelGGL((split_reduce<Epi>), dim3((unsigned)std::min<int64_t>(ceil_div(work, 256), 65536)),
+                           dim3(256), 0, st, (const float*)partials, (int)g.split.splits, M, N, epi);
     }
     return hipGetLastError();
 }
@@ -784,6 +796,16 @@ const char* pifa_status_string(pifa_status s) {
         case PIFA_ERR_WRONG_DEVICE: return "PIFA_ERR_WRONG_DEVICE";
     }
     return "PIFA_ERR_UNKNOWN";
+}
+
+pifa_status pifa_gemm_plan(int64_t M, int64_t N, int64_t K, int wide_epilogue, int64_t* tile_m,
+                           int64_t* tile_n, int64_t* k_splits) {
+    if (M < 1 || N < 1 || K < 1 || !tile_m || !tile_n || !k_splits) return PIFA_ERR_INVALID_ARG;
+    const GemmPlan g = gemm_plan(M, N, K, wide_epilogue != 0, true);
+    *tile_m = g.bm;
+    *tile_n = g.bn;
+    *k_splits = g.split.splits;
+    return PIFA_OK;
 }
 
 pifa_status pifa_validate_partition(const int32_t* pivot_idx, const int32_t* nonpivot_idx,

@@ -53,6 +53,8 @@ _st = ctypes.c_int
 _SIGNATURES = {
     "pifa_status_string": (ctypes.c_char_p, [_st]),
     "pifa_validate_partition": (_st, [_i32p, _i32p, pifa_dims]),
+    "pifa_gemm_plan": (_st, [_i64, _i64, _i64, ctypes.c_int, ctypes.POINTER(_i64), ctypes.POINTER(_i64),
+                             ctypes.POINTER(_i64)]),
     "pifa_layer_create": (_st, [_vp, _vp, _i32p, _i32p, pifa_dims, ctypes.c_int, ctypes.POINTER(_vp)]),
     "pifa_layer_destroy": (_st, [_vp]),
     "pifa_layer_reserve": (_st, [_vp, _i64]),
@@ -201,6 +203,15 @@ def _check(fn: str, status: int):
 # ---------------------------------------------------------------- entry points
 def pifa_status_string(status: int) -> str:
     return lib().pifa_status_string(int(status)).decode()
+
+
+def pifa_gemm_plan(M: int, N: int, K: int, wide_epilogue: bool = True):
+    """(tile_m, tile_n, k_splits) of a prefill product of M x N outputs over K
+    (host only).  Raises on an invalid size."""
+    tm, tn, ks = _i64(), _i64(), _i64()
+    _check("pifa_gemm_plan", lib().pifa_gemm_plan(int(M), int(N), int(K), int(bool(wide_epilogue)), ctypes.byref(tm),
+                                                  ctypes.byref(tn), ctypes.byref(ks)))
+    return tm.value, tn.value, ks.value
 
 
 def pifa_validate_partition(pivot_idx, nonpivot_idx, dims) -> int:

@@ -161,3 +161,29 @@ def test_group_backward_and_calibration_reject_bad_args_on_host():
     assert lib.pifa_calib_reconstruct(None, FAKE, 8, FAKE, 4, 0.25, 1e-3, FAKE, FAKE, None) == inval
     assert lib.pifa_calib_read(None, None, None, None) == inval
     assert lib.pifa_calib_destroy(None) == pifa.PIFA_OK
+
+
+@pytest.mark.parametrize("shape,wide,plan", [
+    ((4096, 2048, 4096), True, (256, 128, 1)),    # attention layer, both products
+    ((4096, 2496, 4096), True, (256, 192, 1)),    # r = 60% pivot product: one round of 256 x 192
+    ((4096, 8960, 2048), True, (256, 192, 1)),    # MLP up projection's non-pivot product
+    ((4096, 4096, 8192), True, (256, 256, 1)),    # 70B square layer's pivot product
+    ((4096, 4096, 8192), False, (256, 128, 1)),   # epilogue with per-output state: no wide tile
+    ((4096, 448, 4096), True, (128, 64, 1)),      # r = 10% pivot product: 224 tiles of 128 x 64, no split
+    ((4096, 832, 4096), True, (128, 128, 1)),     # 13.6 MB per split: no split, 224 tiles
+    ((2048, 2048, 4096), True, (128, 128, 1)),    # 256 tiles fill the chip
+])
+def test_gemm_plan_of_measured_shapes(shape, wide, plan):
+    """The prefill tile and K split chosen for shapes whose choice was measured."""
+    assert pifa.pifa_gemm_plan(*shape, wide_epilogue=wide) == plan
+
+
+def test_gemm_plan_splits_small_batches():
+    """Few rows: K is split, with at most 16 splits, and partials no larger
+    than the operands."""
+    for M in (17, 64, 128, 256):
+        tm, tn, s = pifa.pifa_gemm_plan(M, 2048, 4096)
+        assert (tm, tn) == (128, 128) and 1 < s <= 16
+        assert s * M * 2048 * 4 <= (M + 2048) * 4096 * 2
+    with pytest.raises(pifa.PifaError):
+        pifa.pifa_gemm_plan(0, 2048, 4096)
