@@ -179,11 +179,15 @@ def test_gemm_plan_of_measured_shapes(shape, wide, plan):
 
 
 def test_gemm_plan_splits_small_batches():
-    """Few rows: K is split, with at most 16 splits, and partials no larger
-    than the operands."""
+    """Few rows: K is split over 128 x 64 tiles (half the splits 128 x 128
+    tiles would need for as many workgroups), with at most 16 splits and
+    partials no larger than the operands."""
     for M in (17, 64, 128, 256):
         tm, tn, s = pifa.pifa_gemm_plan(M, 2048, 4096)
-        assert (tm, tn) == (128, 128) and 1 < s <= 16
+        assert (tm, tn) == (128, 64) and 1 < s <= 16
         assert s * M * 2048 * 4 <= (M + 2048) * 4096 * 2
+        assert ((M + 127) // 128) * (2048 // 64) * s <= 512
+    assert pifa.pifa_gemm_plan(128, 2048, 4096) == (128, 64, 8)
+    assert pifa.pifa_gemm_plan(256, 2048, 4096) == (128, 64, 4)
     with pytest.raises(pifa.PifaError):
         pifa.pifa_gemm_plan(0, 2048, 4096)
