@@ -38,8 +38,11 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "PIFA layer TFLOP/s + HBM GB/s, speedup vs same-GPU U·V at r=d/2, bf16"
-PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16/fp16 MFMA
-PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E
+# MI355X published peaks: dense bf16/fp16 MFMA 2.5 PFLOP/s (256 CUs x 4 SIMDs
+# x 1024 FLOP/clk at 2.4 GHz = 2516.6 TFLOP/s) and HBM3E 8 TB/s
+PEAK_BF16_TFLOPS = 256 * 4 * 1024 * 2.4e9 / 1e12
+PEAK_SCLK_MHZ = 2400.0
+PEAK_HBM_GBPS = 8000.0
 CACHE_DEFEAT_BYTES = 600 << 20  # > 256 MB Infinity Cache
 
 
@@ -59,30 +62,44 @@ def dense_flops(M, d_in, d_out):
     return 2.0 * M * d_in * d_out
 
 
+def upload_bf16(a):
+    """fp64 host array -> bf16 device tensor (rounded once on the host, fp64 ->
+    fp32 -> bf16 as the tests round; torch only moves the bits)."""
+    import torch
+    from paper_2501_19090_amd import inputs
+    return torch.from_numpy(inputs.round_bf16(a)[0].view(np.int16)).to("cuda:0").view(torch.bfloat16)
+
+
+def host_f64(t):
+    return t.cpu().numpy()
+
+
 class Workload:
-    """Device-resident PIFA, low-rank and dense layers of one synthetic W' = U V."""
+    """Device-resident PIFA, low-rank and dense layers of one synthetic W' = U V.
+    W' = U V is formed on the host (fp64, numpy); the PIFA form is built on the
+    GPU by pifa_build_f64; every rounding to bf16 happens on the host."""
 
     def __init__(self, d_in, d_out, r, seed):
         import torch
         from paper_2501_19090_amd import inputs, pifa
         self.torch, self.pifa = torch, pifa
         self.d_in, self.d_out, self.r, self.seed = d_in, d_out, r, seed
-        dev = torch.device("cuda:0")
         U, V = inputs.lowrank_factors(d_out, d_in, r, seed)
-        U64 = torch.from_numpy(U).to(dev)
-        V64 = torch.from_numpy(V).to(dev)
-        del U, V
-        W64 = U64 @ V64
+        W = U @ V
+        W64 = torch.from_numpy(W).to("cuda:0")
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         piv, npiv, Wp, C, report = pifa.pifa_build_f64(W64, r)
         torch.cuda.synchronize()
         self.build_ms = 1e3 * (time.perf_counter() - t0)
         self.build_report = report.tolist()
-        self.wp, self.c = Wp.to(torch.bfloat16), (C.to(torch.bfloat16) if C.numel() else None)
-        self.u, self.v = U64.to(torch.bfloat16), V64.to(torch.bfloat16)
-        self.w = W64.to(torch.bfloat16)  # dense baseline weight
-        del W64, Wp, C, U64, V64
+        del W64
+        self.wp = upload_bf16(host_f64(Wp))
+        self.c = upload_bf16(host_f64(C)) if C.numel() else None
+        del Wp, C
+        self.u, self.v = upload_bf16(U), upload_bf16(V)
+        self.w = upload_bf16(W)  # dense baseline weight
+        del U, V, W
         torch.cuda.empty_cache()
         self.piv, self.npiv = piv, npiv
         self.pifa_bytes = 2 * (r * d_in + (d_out - r) * r) + 4 * d_out
@@ -238,15 +255,16 @@ def measure(wl: Workload, M: int, iters: int, warmup: int, rotate: bool):
 
 
 def gpu_built_layer(d_in, d_out, r, seed):
-    """(pivot_idx, nonpivot_idx, W_p bf16, C bf16) of a Gaussian rank-r W' = U V,
-    built on the GPU."""
+    """(pivot_idx, nonpivot_idx, W_p bf16, C bf16) of a Gaussian rank-r W' = U V
+    (formed on the host), built on the GPU."""
     import torch
     from paper_2501_19090_amd import inputs, pifa
     U, V = inputs.lowrank_factors(d_out, d_in, r, seed)
-    W = torch.from_numpy(U).cuda() @ torch.from_numpy(V).cuda()
+    W = torch.from_numpy(U @ V).cuda()
     del U, V
     piv, npiv, Wp, C, _ = pifa.pifa_build_f64(W, r)
-    return piv, npiv, Wp.to(torch.bfloat16), C.to(torch.bfloat16)
+    del W
+    return piv, npiv, upload_bf16(host_f64(Wp)), upload_bf16(host_f64(C))
 
 
 def measure_group(seed):
@@ -351,10 +369,9 @@ def measure_reconstruct(n=4096, m=4096, r=2048, batch=2048, batches=8):
     dev = lambda a: torch.from_numpy(inputs.round_bf16(a)[0].view(np.int16)).cuda().view(torch.bfloat16)
     xus = [dev(inputs.activations(batch, n, 41 + 2 * i)) for i in range(batches)]
     xos = [dev(inputs.activations(batch, n, 42 + 2 * i)) for i in range(batches)]
-    g = torch.Generator(device="cuda:0")
-    g.manual_seed(43)
-    W = torch.randn((m, n), dtype=torch.float64, device="cuda:0", generator=g) / math.sqrt(n)
-    Vt = torch.randn((r, n), dtype=torch.float64, device="cuda:0", generator=g) / math.sqrt(n)
+    rng = np.random.default_rng(43)
+    W = torch.from_numpy(rng.standard_normal((m, n)) / math.sqrt(n)).cuda()
+    Vt = torch.from_numpy(rng.standard_normal((r, n)) / math.sqrt(n)).cuda()
     h = pifa.pifa_calib_create(n)
     try:
         pifa.pifa_calib_accumulate(h, xos[0], xus[0])  # workspace
@@ -390,9 +407,38 @@ def measure_reconstruct(n=4096, m=4096, r=2048, batch=2048, batches=8):
             "kernels": {k: {"launches": c, "avg_us": 1e3 * v / c} for k, (c, v) in kern.items()}}
 
 
-def cpu_baseline(wl, M_full, budget_s=10.0):
-    """The fp64 oracle's PIFA forward on a bounded row sample of the workload
-    (the same bf16 layer the GPU runs)."""
+def cpu_model_name() -> str:
+    """The host CPU's model string (lscpu, else /proc/cpuinfo)."""
+    import subprocess
+    try:
+        out = subprocess.run(["lscpu"], stdout=subprocess.PIPE, stderr=subprocess.DEVNULL, text=True,
+                             timeout=10).stdout
+        for ln in out.splitlines():
+            if ln.strip().startswith("Model name"):
+                return ln.split(":", 1)[1].strip()
+    except Exception:
+        pass
+    try:
+        with open("/proc/cpuinfo") as f:
+            return next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
+    except OSError:
+        return ""
+
+
+def median_time(fn, runs=3):
+    ts = []
+    for _ in range(runs):
+        t0 = time.perf_counter()
+        fn()
+        ts.append(time.perf_counter() - t0)
+    return float(np.median(ts)), ts
+
+
+def cpu_baseline(wl, M_full, budget_s=4.0):
+    """The fp64 oracle's PIFA forward on the same bf16 layer the GPU runs,
+    wall-clock median of 3 runs, with all host threads and with one; the
+    threaded sample is sized to about `budget_s` per run (all 4096 rows on
+    the usual 16-thread host)."""
     import oracle
     from paper_2501_19090_amd import inputs
     d_in, d_out, r = wl.d_in, wl.d_out, wl.r
@@ -406,14 +452,10 @@ def cpu_baseline(wl, M_full, budget_s=10.0):
     oracle.pifa_forward(X[:rows], piv, npiv, Wp, C, d_out=d_out, threads=threads)
     t1 = time.perf_counter() - t0
     rows = int(min(M_full, max(rows, rows * budget_s / max(t1, 1e-6))))
-    t0 = time.perf_counter()
-    oracle.pifa_forward(X[:rows], piv, npiv, Wp, C, d_out=d_out, threads=threads)
-    dt = time.perf_counter() - t0
-    # one thread, on a sample sized from the threaded rate (about 3 s)
-    rows1 = int(min(M_full, max(4, rows * 3.0 / (dt * threads))))
-    t0 = time.perf_counter()
-    oracle.pifa_forward(X[:rows1], piv, npiv, Wp, C, d_out=d_out, threads=1)
-    dt1 = time.perf_counter() - t0
+    dt, runs = median_time(lambda: oracle.pifa_forward(X[:rows], piv, npiv, Wp, C, d_out=d_out, threads=threads))
+    # one thread, on a sample sized from the threaded rate (about 2 s per run)
+    rows1 = int(min(M_full, max(4, rows * 2.0 / (dt * threads))))
+    dt1, runs1 = median_time(lambda: oracle.pifa_forward(X[:rows1], piv, npiv, Wp, C, d_out=d_out, threads=1))
     # the oracle's build (QRCP + coefficient solve) of the same W' = U V
     U, V = inputs.lowrank_factors(d_out, d_in, r, wl.seed)
     W = U @ V
@@ -423,23 +465,18 @@ def cpu_baseline(wl, M_full, budget_s=10.0):
     build_s = time.perf_counter() - t0
     same_pivots = bool(np.array_equal(np.asarray(b["pivot_idx"]), np.asarray(piv)))
     del W, b
-    model = ""
-    try:
-        with open("/proc/cpuinfo") as f:
-            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
-    except OSError:
-        pass
     return {"value": pifa_flops(rows, d_in, d_out, r) / dt / 1e12, "unit": "TFLOP/s", "cores": threads,
             "kind": "oracle",
-            "sample": "fp64 PIFA forward of the same 4096x4096 r=2048 layer on %d of %d activation rows "
-                      "(%.1f s, %d OpenMP threads; rows are independent, so throughput scales to the batch)"
-                      % (rows, M_full, dt, threads),
+            "sample": "fp64 PIFA forward of the same 4096x4096 r=2048 layer on %d of %d activation rows, "
+                      "median of 3 runs (%s s), %d OpenMP threads; rows are independent, so throughput "
+                      "scales to the batch" % (rows, M_full, ", ".join("%.2f" % t for t in runs), threads),
             "single_thread": {"value": pifa_flops(rows1, d_in, d_out, r) / dt1 / 1e12, "unit": "TFLOP/s",
-                              "sample": "%d rows, %.1f s" % (rows1, dt1)},
+                              "sample": "%d rows, median of 3 runs (%s s)"
+                                        % (rows1, ", ".join("%.2f" % t for t in runs1))},
             "build_s": build_s,
             "build": "oracle QRCP + coefficient solve of the 4096x4096 rank-2048 W' (fp64, %d threads); "
                      "pivot set identical to the GPU build: %s" % (threads, same_pivots),
-            "cpu_model": model, "nproc": os.cpu_count(),
+            "cpu_model": cpu_model_name(), "nproc": os.cpu_count(),
             "affinity": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else None}
 
 
@@ -567,8 +604,14 @@ def main():
         log("profile run done")
         return
 
-    # ---- headline: K timed steps of the M = 4096 forward (no per-launch
-    # events inside: they add about 10% to a step)
+    # ---- the same-engine baselines at the headline M first: their ~400
+    # forwards also bring the clocks to the level they hold under this load
+    # (about 150 forwards), so the timed steps below run on settled clocks
+    pre = measure(wl, M, args.steps, 100, rotate=False)
+    log("prefill baselines:", json.dumps(pre))
+
+    # ---- headline: W untimed warm-up steps, then K timed steps of the
+    # M = 4096 forward (no per-launch events inside: they add about 10%)
     for _ in range(args.warmup):
         pifa.pifa_forward(h, x, y, M, stream)
     torch.cuda.synchronize()
@@ -581,7 +624,7 @@ def main():
     ms_step = ev0.elapsed_time(ev1) / args.steps
     value = pifa_flops(M, d_in, d_out, r) / (ms_step * 1e9)
     # ---- the same K steps again with each launch bracketed by HIP events on
-    # its stream: per-kernel durations for the roofline
+    # its stream: per-kernel durations for the roofline (same settled clocks)
     pifa.pifa_profile_reset()
     pifa.pifa_profile_enable(True)
     ev0.record()
@@ -593,24 +636,40 @@ def main():
     ms_step_instrumented = ev0.elapsed_time(ev1) / args.steps
     kern = pifa.pifa_profile_read()
     pifa.pifa_profile_reset()
-    log("prefill M=%d: %.1f us/step (%.1f with per-launch events), %.1f TFLOP/s; kernels %s"
-        % (M, 1e3 * ms_step, 1e3 * ms_step_instrumented, value, kern))
+    # ---- the clock the matrix cores hold right after that load, and the
+    # sustained MFMA-only rate at it (no memory traffic)
+    probe_tflops, sclk_mhz = pifa.pifa_probe_mfma(20000)
+    log("prefill M=%d: %.1f us/step (%.1f with per-launch events), %.1f TFLOP/s; kernels %s; "
+        "MFMA-only %.0f TFLOP/s at %.0f MHz"
+        % (M, 1e3 * ms_step, 1e3 * ms_step_instrumented, value, kern, probe_tflops, sclk_mhz))
 
-    g1_n, g1_ms = kern["pifa_gemm1_xwp"]
-    g1_us = 1e3 * g1_ms / g1_n
-    g1_flops = 2.0 * M * r * d_in
-    achieved = g1_flops / (g1_us * 1e6)
+    def kernel_roof(site, flops):
+        n, ms = kern[site]
+        us = 1e3 * ms / n
+        ach = flops / (us * 1e6)
+        return {"avg_us": us, "achieved": ach, "frac": ach / PEAK_BF16_TFLOPS,
+                "algorithmic_flops_per_launch": flops}
+
+    g1 = kernel_roof("pifa_gemm1_xwp", 2.0 * M * r * d_in)
+    g2 = kernel_roof("pifa_gemm2_ypc", 2.0 * M * r * (d_out - r))
+    peak_at_clock = PEAK_BF16_TFLOPS * sclk_mhz / PEAK_SCLK_MHZ
     traffic = traffic_from_profiles("pifa_gemm1_xwp")
-    roofline = {"bound": "mfma", "kernel": "pifa_gemm1_xwp (X W_p^T, bf16 MFMA)", "achieved": achieved,
-                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
-                "traffic": traffic, "avg_us": g1_us, "algorithmic_flops_per_launch": g1_flops,
+    roofline = {"bound": "mfma", "kernel": "pifa_gemm1_xwp (X W_p^T, bf16 MFMA, pivot-column epilogue)",
+                "achieved": g1["achieved"], "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": g1["frac"],
+                "traffic": traffic, "avg_us": g1["avg_us"],
+                "algorithmic_flops_per_launch": g1["algorithmic_flops_per_launch"],
+                "gemm2": dict(g2, kernel="pifa_gemm2_ypc (Y_p C^T, fp16 MFMA, non-pivot epilogue)"),
+                "layer": {"us": 1e3 * ms_step, "achieved": value, "frac": value / PEAK_BF16_TFLOPS},
+                "sclk_mhz": sclk_mhz,
+                "frac_at_measured_clock": g1["achieved"] / peak_at_clock,
+                "mfma_only_tflops": probe_tflops,
                 "timing": "HIP events around every launch on its stream, over K instrumented steps run "
-                          "right after the K timed steps (%.1f us/step with the events)" % (1e3 * ms_step_instrumented)}
+                          "right after the K timed steps on settled clocks (%.1f us/step with the events); "
+                          "sclk from shader-clock / real-time counters of an MFMA-only kernel run right "
+                          "after them" % (1e3 * ms_step_instrumented)}
     kernels = {k: {"launches": n, "avg_us": 1e3 * v / n} for k, (n, v) in kern.items()}
 
-    # ---- baselines at the headline M, and the decode case
-    pre = measure(wl, M, args.steps, 100, rotate=False)
-    log("prefill baselines:", json.dumps(pre))
+    # ---- the decode case
     dec = measure(wl, 1, 200, 20, rotate=True)
     log("decode:", json.dumps(dec))
     dec_bytes = wl.pifa_bytes + 2 * (d_in + d_out)
@@ -619,6 +678,17 @@ def main():
               "uv_us": dec["uv_us"], "dense_us": dec["dense_us"],
               "speedup_vs_uv": dec["speedup_vs_uv"], "speedup_vs_dense": dec["speedup_vs_dense"],
               "weights_rotated": dec["weights_rotated"], "kernels": dec["kernels"]}
+    # ---- HBM read rate of the chip at hand (1 GiB, four times the Infinity Cache)
+    buf = torch.empty(1 << 30, dtype=torch.uint8, device="cuda:0")
+    buf.zero_()
+    hbm_read = pifa.pifa_probe_hbm_read(buf, 5)
+    del buf
+    torch.cuda.empty_cache()
+    peak_check = {"mfma_only_tflops": probe_tflops, "sclk_mhz_under_mfma": sclk_mhz,
+                  "peak_bf16_tflops_at_that_clock": peak_at_clock, "hbm_read_gbps": hbm_read,
+                  "what": "MFMA-only kernel (2048 x 4 waves of independent 32x32x16 bf16 MFMAs) and 5 "
+                          "streaming reads of a 1 GiB buffer, on this GPU in this run"}
+    log("peak check:", json.dumps(peak_check))
     cpu = None
     if not args.no_cpu:
         cpu = cpu_baseline(wl, M)
@@ -642,6 +712,7 @@ def main():
                                "(r=d/2), M=4096 rows, bf16 in/out, fp32 accumulation",
                    "d_in": d_in, "d_out": d_out, "r": r, "M": M},
         "roofline": roofline,
+        "peak_check": peak_check,
         "cpu_baseline": cpu,
         "hbm_gbps_decode": decode["pifa_gbps"],
         "speedup_vs_uv": pre["speedup_vs_uv"],

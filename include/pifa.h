@@ -363,6 +363,26 @@ pifa_status pifa_profile_reset(void);
 pifa_status pifa_profile_read(const char** names, int64_t* launches, double* total_ms, int max_sites,
                               int* n_sites);
 
+/*
+ * Peak probes (diagnostics; they allocate and free a few KB and synchronise).
+ *
+ * pifa_probe_mfma: the sustained bf16 matrix-core rate of the current device.
+ * 2048 workgroups of 4 waves each issue `iters` rounds of four independent
+ * v_mfma_f32_32x32x16_bf16 on register operands (no memory traffic); the
+ * second of two launches is timed with HIP events.  *tflops is its dense
+ * FLOP rate; *sclk_mhz is the shader clock the loop ran at, averaged over
+ * the workgroups (shader-clock cycles over real-time-clock ticks).
+ *
+ * pifa_probe_hbm_read: `reps` back-to-back reads of the device buffer `buf`
+ * (`bytes` a multiple of 16, 16-byte aligned; larger than the 256 MB
+ * Infinity Cache to measure HBM) with 16-byte loads; *gbps = bytes * reps /
+ * the elapsed time of the `reps` launches (one untimed launch first).
+ * Both return PIFA_ERR_INVALID_ARG for a bad argument and PIFA_ERR_HIP if
+ * a launch or event fails.
+ */
+pifa_status pifa_probe_mfma(int64_t iters, double* tflops, double* sclk_mhz, void* stream);
+pifa_status pifa_probe_hbm_read(const void* buf, int64_t bytes, int reps, double* gbps, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -68,6 +68,8 @@ def _load():
         lib.oracle_reconstruction_error.restype = ctypes.c_double
         lib.oracle_reconstruction_error.argtypes = [f64p, i64, i64, i64, i32p, i32p, f64p, f64p,
                                                     ctypes.c_int]
+        lib.oracle_set_progress.restype = None
+        lib.oracle_set_progress.argtypes = [i64]
         lib.oracle_max_threads.restype = ctypes.c_int
         lib.oracle_max_threads.argtypes = []
         _lib = lib
@@ -95,7 +97,7 @@ class OracleRankError(ValueError):
     """The input W' does not have numerical rank exactly r."""
 
 
-def build_pifa(W, r: int, threads: int | None = None) -> dict:
+def build_pifa(W, r: int, threads: int | None = None, progress: int = 0) -> dict:
     """Pivoting Factorization of a rank-r matrix W' (d_out x d_in).
 
     Returns a dict with ``pivot_idx`` (sorted I), ``nonpivot_idx`` (sorted
@@ -103,6 +105,8 @@ def build_pifa(W, r: int, threads: int | None = None) -> dict:
     (pivots in QRCP selection order) and ``report`` (|R_00|, |R_{r-1,r-1}|,
     largest residual norm after r steps, certification flag).
     Raises OracleRankError if W' is not numerically of rank r.
+    progress > 0 prints a line to stderr every `progress` pivoting steps
+    (long builds); it does not change the result.
     """
     lib = _load()
     W = _f64(W)
@@ -118,10 +122,15 @@ def build_pifa(W, r: int, threads: int | None = None) -> dict:
     # a 1-element dummy keeps the pointer valid when C is empty
     Cbuf = C if C.size else np.zeros(1, np.float64)
     npbuf = npiv if npiv.size else np.zeros(1, np.int32)
-    st = lib.oracle_pifa_build(_p(W, ctypes.c_double), d_out, d_in, r, int(nt),
-                               _p(piv, ctypes.c_int32), _p(npbuf, ctypes.c_int32),
-                               _p(Wp, ctypes.c_double), _p(Cbuf, ctypes.c_double),
-                               _p(order, ctypes.c_int32), _p(report, ctypes.c_double))
+    with _lock:
+        lib.oracle_set_progress(int(progress))
+        try:
+            st = lib.oracle_pifa_build(_p(W, ctypes.c_double), d_out, d_in, r, int(nt),
+                                       _p(piv, ctypes.c_int32), _p(npbuf, ctypes.c_int32),
+                                       _p(Wp, ctypes.c_double), _p(Cbuf, ctypes.c_double),
+                                       _p(order, ctypes.c_int32), _p(report, ctypes.c_double))
+        finally:
+            lib.oracle_set_progress(0)
     if st == ORACLE_NOT_RANK_R:
         raise OracleRankError("input is not numerically of rank %d (report=%s)" % (r, report))
     if st != ORACLE_OK:

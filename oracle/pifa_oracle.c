@@ -45,6 +45,7 @@
  */
 #include <math.h>
 #include <stdint.h>
+#include <stdio.h>
 #include <stdlib.h>
 #include <string.h>
 
@@ -64,6 +65,12 @@ enum {
 };
 
 static int clamp_threads(int nthreads) { return nthreads < 1 ? 1 : nthreads; }
+
+/* Progress lines of long builds: every `oracle_progress_every` QRCP steps a
+ * line goes to stderr (0 = silent).  Reporting only; no effect on results. */
+static int64_t oracle_progress_every = 0;
+
+void oracle_set_progress(int64_t every) { oracle_progress_every = every < 0 ? 0 : every; }
 
 typedef struct {
     int32_t key;  /* original row index of W' */
@@ -128,6 +135,11 @@ int oracle_pifa_build(const double* W, int64_t d_out, int64_t d_in, int64_t r,
 
     int status = ORACLE_OK;
     for (int64_t k = 0; k < r; ++k) {
+        if (oracle_progress_every > 0 && k % oracle_progress_every == 0) {
+            fprintf(stderr, "oracle build %lld x %lld, r = %lld: QRCP step %lld\n", (long long)d_out,
+                    (long long)d_in, (long long)r, (long long)k);
+            fflush(stderr);
+        }
         /* pivot: largest residual norm, ties to the lowest original index */
         int64_t p = k;
         for (int64_t j = k + 1; j < d_out; ++j) {
@@ -220,6 +232,11 @@ int oracle_pifa_build(const double* W, int64_t d_out, int64_t d_in, int64_t r,
                 for (int64_t t = 0; t < r; ++t)
                     R11[s * r + t] = (t >= s) ? A[t * d_in + s] : 0.0;
 
+            if (oracle_progress_every > 0) {
+                fprintf(stderr, "oracle build %lld x %lld, r = %lld: QRCP done, solving for C\n",
+                        (long long)d_out, (long long)d_in, (long long)r);
+                fflush(stderr);
+            }
             /* C^T = R11^{-1} R12 by back substitution, one non-pivot row of
              * W' (one column of R12) at a time, scattered to sorted order */
 #pragma omp parallel num_threads(nt)

@@ -28,6 +28,7 @@
 #include "layout.hpp"
 #include "linalg64.hpp"
 #include "prepack.hpp"
+#include "probe.hpp"
 
 using namespace pifa;
 
@@ -846,6 +847,69 @@ pifa_status pifa_validate_partition(const int32_t* pivot_idx, const int32_t* non
 
 namespace {
 
+// The forward of Algorithm "PIFA Layer" with caller-chosen workspace: ws
+// holds pifa_ws_bytes(h, M) bytes (the Y_p hand-off), part
+// pifa_part_bytes(h, M) bytes (K-split partial products; may be null when
+// that is 0).  Arguments are already validated.
+pifa_status forward_with(pifa_layer* h, const void* X, void* Y, int64_t M, void* ws, float* part,
+                         hipStream_t st) {
+    hipError_t e;
+    if (h->dtype == PIFA_F32) {
+        float* yp = (float*)ws;
+        e = launch_gemm_f32(kSitePifaF32Gemm1, (const float*)X, h->d_in, M, (const float*)h->Wp, h->d_in,
+                            h->r, h->d_in,
+                            make_epi<float, kWsF32>((float*)Y, h->d_out, h->piv, h->r, 1.f, yp, h->r,
+                                                    h->r, 1.f, nullptr, M),
+                            st);
+        if (e != hipSuccess) return PIFA_ERR_HIP;
+        if (h->n_np > 0) {
+            e = launch_gemm_f32(kSitePifaF32Gemm2, yp, h->r, M, (const float*)h->C, h->r, h->n_np, h->r,
+                                make_epi<float, kWsNone>((float*)Y, h->d_out, h->npiv, h->n_np, 1.f,
+                                                         nullptr, 0, 0, 1.f, nullptr, M),
+                                st);
+            if (e != hipSuccess) return PIFA_ERR_HIP;
+        }
+        return PIFA_OK;
+    }
+
+    const float y_scale = std::ldexp(1.0f, h->y_log2);
+    const float out_scale = std::ldexp(1.0f, -(h->y_log2 + h->c_log2));
+    if (M <= kDecodeMaxM) {
+        f16* yp = (f16*)ws;  // hi plane, then lo plane, M x r_pad each
+        e = launch_skinny_packed<bf16>(kSitePifaGemv1, ALoad16<bf16>{(const bf16*)X, h->d_in, M},
+                                       (const bf16*)h->Wp, h->r_pad, h->d_in,
+                                       make_epi<bf16, kWsF16Pair>((bf16*)Y, h->d_out, h->piv, h->r, 1.f, yp,
+                                                                  h->r_pad, h->r_pad, y_scale, h->overflow, M),
+                                       st);
+        if (e != hipSuccess) return PIFA_ERR_HIP;
+        if (h->n_np > 0) {
+            e = launch_skinny_packed<f16>(kSitePifaGemv2, ALoadPair16{yp, h->r_pad, M}, (const f16*)h->C, h->n_np,
+                                          h->r_pad,
+                                          make_epi<bf16, kWsNone>((bf16*)Y, h->d_out, h->npiv, h->n_np,
+                                                                  out_scale, nullptr, 0, 0, 1.f, nullptr, M),
+                                          st);
+            if (e != hipSuccess) return PIFA_ERR_HIP;
+        }
+        return PIFA_OK;
+    }
+
+    f16* yp = (f16*)ws;
+    e = launch_gemm<bf16, true>(kSitePifaGemm1, (const bf16*)X, h->d_in, M, (const bf16*)h->Wp, 0, h->r_pad,
+                                h->d_in,
+                                make_epi<bf16, kWsF16>((bf16*)Y, h->d_out, h->piv, h->r, 1.f, yp, h->r_pad,
+                                                       h->r_pad, y_scale, h->overflow, M),
+                                part, st);
+    if (e != hipSuccess) return PIFA_ERR_HIP;
+    if (h->n_np > 0) {
+        e = launch_gemm<f16, true>(kSitePifaGemm2, yp, h->r_pad, M, (const f16*)h->C, 0, h->n_np, h->r_pad,
+                                   make_epi<bf16, kWsNone>((bf16*)Y, h->d_out, h->npiv, h->n_np, out_scale,
+                                                           nullptr, 0, 0, 1.f, nullptr, M),
+                                   part, st);
+        if (e != hipSuccess) return PIFA_ERR_HIP;
+    }
+    return PIFA_OK;
+}
+
 // Copy n host indices to a new device array, adding `offset` to each.
 pifa_status upload_indices(const int32_t* src, int64_t n, int64_t offset, int32_t** dst) {
     std::vector<int32_t> tmp((size_t)n);
@@ -989,65 +1053,9 @@ pifa_status pifa_forward(pifa_handle h, const void* X, void* Y, int64_t M, void*
     hipStream_t st = as_stream(stream);
     pifa_status s = h->ws.ensure(pifa_ws_bytes(h, M), st);
     if (s != PIFA_OK) return s;
-    hipError_t e;
-
-    if (h->dtype == PIFA_F32) {
-        float* yp = (float*)h->ws.ptr;
-        e = launch_gemm_f32(kSitePifaF32Gemm1, (const float*)X, h->d_in, M, (const float*)h->Wp, h->d_in,
-                            h->r, h->d_in,
-                            make_epi<float, kWsF32>((float*)Y, h->d_out, h->piv, h->r, 1.f, yp, h->r,
-                                                    h->r, 1.f, nullptr, M),
-                            st);
-        if (e != hipSuccess) return PIFA_ERR_HIP;
-        if (h->n_np > 0) {
-            e = launch_gemm_f32(kSitePifaF32Gemm2, yp, h->r, M, (const float*)h->C, h->r, h->n_np, h->r,
-                                make_epi<float, kWsNone>((float*)Y, h->d_out, h->npiv, h->n_np, 1.f,
-                                                         nullptr, 0, 0, 1.f, nullptr, M),
-                                st);
-            if (e != hipSuccess) return PIFA_ERR_HIP;
-        }
-        return PIFA_OK;
-    }
-
-    const float y_scale = std::ldexp(1.0f, h->y_log2);
-    const float out_scale = std::ldexp(1.0f, -(h->y_log2 + h->c_log2));
-    if (M <= kDecodeMaxM) {
-        f16* yp = (f16*)h->ws.ptr;  // hi plane, then lo plane, M x r_pad each
-        e = launch_skinny_packed<bf16>(kSitePifaGemv1, ALoad16<bf16>{(const bf16*)X, h->d_in, M},
-                                       (const bf16*)h->Wp, h->r_pad, h->d_in,
-                                       make_epi<bf16, kWsF16Pair>((bf16*)Y, h->d_out, h->piv, h->r, 1.f, yp,
-                                                                  h->r_pad, h->r_pad, y_scale, h->overflow, M),
-                                       st);
-        if (e != hipSuccess) return PIFA_ERR_HIP;
-        if (h->n_np > 0) {
-            e = launch_skinny_packed<f16>(kSitePifaGemv2, ALoadPair16{yp, h->r_pad, M}, (const f16*)h->C, h->n_np,
-                                          h->r_pad,
-                                          make_epi<bf16, kWsNone>((bf16*)Y, h->d_out, h->npiv, h->n_np,
-                                                                  out_scale, nullptr, 0, 0, 1.f, nullptr, M),
-                                          st);
-            if (e != hipSuccess) return PIFA_ERR_HIP;
-        }
-        return PIFA_OK;
-    }
-
     s = h->part.ensure(pifa_part_bytes(h, M), st);
     if (s != PIFA_OK) return s;
-    float* part = (float*)h->part.ptr;
-    f16* yp = (f16*)h->ws.ptr;
-    e = launch_gemm<bf16, true>(kSitePifaGemm1, (const bf16*)X, h->d_in, M, (const bf16*)h->Wp, 0, h->r_pad,
-                                h->d_in,
-                                make_epi<bf16, kWsF16>((bf16*)Y, h->d_out, h->piv, h->r, 1.f, yp, h->r_pad,
-                                                       h->r_pad, y_scale, h->overflow, M),
-                                part, st);
-    if (e != hipSuccess) return PIFA_ERR_HIP;
-    if (h->n_np > 0) {
-        e = launch_gemm<f16, true>(kSitePifaGemm2, yp, h->r_pad, M, (const f16*)h->C, 0, h->n_np, h->r_pad,
-                                   make_epi<bf16, kWsNone>((bf16*)Y, h->d_out, h->npiv, h->n_np, out_scale,
-                                                           nullptr, 0, 0, 1.f, nullptr, M),
-                                   part, st);
-        if (e != hipSuccess) return PIFA_ERR_HIP;
-    }
-    return PIFA_OK;
+    return forward_with(h, X, Y, M, h->ws.ptr, (float*)h->part.ptr, st);
 }
 
 pifa_status dense_forward(const void* W, const void* X, void* Y, int64_t M, int64_t d_in,
@@ -1968,6 +1976,91 @@ pifa_status pifa_profile_read(const char** names, int64_t* launches, double* tot
     }
     *n_sites = n;
     return status;
+}
+
+// ------------------------------------------------------------------ peak probes
+namespace {
+
+struct DevBuf {
+    void* p = nullptr;
+    ~DevBuf() {
+        if (p) (void)hipFree(p);
+    }
+};
+
+}  // namespace
+
+pifa_status pifa_probe_mfma(int64_t iters, double* tflops, double* sclk_mhz, void* stream) {
+    if (iters < 1 || !tflops || !sclk_mhz) return PIFA_ERR_INVALID_ARG;
+    hipStream_t st = as_stream(stream);
+    constexpr unsigned kGrid = 2048, kThreads = 256;
+    DevBuf clocks, sink;
+    if (hipMalloc(&clocks.p, (size_t)kGrid * 16) != hipSuccess) return PIFA_ERR_OOM;
+    if (hipMalloc(&sink.p, (size_t)kGrid * 4) != hipSuccess) return PIFA_ERR_OOM;
+    int dev = 0, wall_khz = 0;
+    PIFA_HIP(hipGetDevice(&dev));
+    PIFA_HIP(hipDeviceGetAttribute(&wall_khz, hipDeviceAttributeWallClockRate, dev));
+    if (wall_khz <= 0) return PIFA_ERR_UNSUPPORTED;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    PIFA_HIP(hipEventCreate(&e0));
+    if (hipEventCreate(&e1) != hipSuccess) {
+        (void)hipEventDestroy(e0);
+        return PIFA_ERR_HIP;
+    }
+    auto run = [&]() {
+        hipLaunchKernelGGL(mfma_probe, dim3(kGrid), dim3(kThreads), 0, st, iters, 0.0f, (float*)sink.p,
+                           (uint64_t*)clocks.p);
+        return hipGetLastError();
+    };
+    float ms = 0.f;
+    bool ok = run() == hipSuccess && hipEventRecord(e0, st) == hipSuccess && run() == hipSuccess &&
+              hipEventRecord(e1, st) == hipSuccess && hipEventSynchronize(e1) == hipSuccess &&
+              hipEventElapsedTime(&ms, e0, e1) == hipSuccess;
+    std::vector<uint64_t> h((size_t)kGrid * 2);
+    ok = ok && hipMemcpy(h.data(), clocks.p, h.size() * 8, hipMemcpyDeviceToHost) == hipSuccess;
+    (void)hipEventDestroy(e0);
+    (void)hipEventDestroy(e1);
+    if (!ok || ms <= 0.f) return PIFA_ERR_HIP;
+    // 4 waves x 4 MFMAs of 32 x 32 x 16 (2 * 16384 FLOPs each) per iteration
+    *tflops = (double)kGrid * 4 * 4 * 32768.0 * (double)iters / (ms * 1e9);
+    double mhz = 0.0;
+    int64_t n = 0;
+    for (unsigned b = 0; b < kGrid; ++b) {
+        if (h[2 * b + 1] == 0) continue;
+        mhz += (double)h[2 * b] / (double)h[2 * b + 1] * (wall_khz / 1000.0);
+        ++n;
+    }
+    *sclk_mhz = n ? mhz / n : 0.0;
+    return PIFA_OK;
+}
+
+pifa_status pifa_probe_hbm_read(const void* buf, int64_t bytes, int reps, double* gbps, void* stream) {
+    if (!buf || bytes < 16 || bytes % 16 != 0 || reps < 1 || !gbps || !aligned16(buf)) return PIFA_ERR_INVALID_ARG;
+    hipStream_t st = as_stream(stream);
+    constexpr unsigned kGrid = 4096, kThreads = 256;
+    DevBuf sink;
+    if (hipMalloc(&sink.p, (size_t)kGrid * 4) != hipSuccess) return PIFA_ERR_OOM;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    PIFA_HIP(hipEventCreate(&e0));
+    if (hipEventCreate(&e1) != hipSuccess) {
+        (void)hipEventDestroy(e0);
+        return PIFA_ERR_HIP;
+    }
+    auto run = [&]() {
+        hipLaunchKernelGGL(hbm_read_probe, dim3(kGrid), dim3(kThreads), 0, st, (const u32x4*)buf, bytes / 16,
+                           (uint32_t*)sink.p);
+        return hipGetLastError();
+    };
+    bool ok = run() == hipSuccess && hipEventRecord(e0, st) == hipSuccess;
+    for (int i = 0; ok && i < reps; ++i) ok = run() == hipSuccess;
+    float ms = 0.f;
+    ok = ok && hipEventRecord(e1, st) == hipSuccess && hipEventSynchronize(e1) == hipSuccess &&
+         hipEventElapsedTime(&ms, e0, e1) == hipSuccess;
+    (void)hipEventDestroy(e0);
+    (void)hipEventDestroy(e1);
+    if (!ok || ms <= 0.f) return PIFA_ERR_HIP;
+    *gbps = (double)bytes * reps / (ms * 1e6);
+    return PIFA_OK;
 }
 
 }  // extern "C"

@@ -90,22 +90,6 @@ def random_partition(d_out: int, r: int, seed: int):
     return piv, npiv
 
 
-def direct_layer(d_in: int, d_out: int, r: int, seed: int, c_std: float = 0.25):
-    """A synthetic PIFA layer drawn directly, for shapes whose build is too slow
-    to repeat on every run (timing does not depend on the values).
-
-    Any (I, W_p, C) is the PIFA layer of the rank-r matrix whose pivot rows are
-    W_p and whose non-pivot rows are C W_p, so this is a valid layer.  Values:
-    W_p ~ N(0, 1/r) (the entry law of U V above), C ~ N(0, c_std^2) (the rms of
-    built coefficient matrices on the Gaussian layers is about 0.2-0.3).
-    """
-    rng = np.random.default_rng([int(seed), 11])
-    Wp = rng.standard_normal((r, d_in)) * float(r) ** -0.5
-    C = rng.standard_normal((d_out - r, r)) * c_std
-    piv, npiv = random_partition(d_out, r, seed)
-    return piv, npiv, Wp, C
-
-
 # --------------------------------------------------------------------------
 # exactness probes
 # --------------------------------------------------------------------------
@@ -163,8 +147,8 @@ def integer_layer(d_in: int, d_out: int, r: int, M: int, seed: int, density: flo
 # the workloads: LLaMA layer shapes with synthetic values
 # --------------------------------------------------------------------------
 # name -> (config index, layer index, d_in, d_out, r, dtype, M values, layer kind)
-# layer kind "built": (I, W_p, C) come from the PIFA build of U V;
-#            "direct": drawn by direct_layer (shapes whose build takes minutes).
+# layer kind "built": (I, W_p, C) come from the PIFA build of W' = U V
+# (every configuration, the LLaMA-70B shapes included).
 RANK_SWEEP = (0.1, 0.2, 0.3, 0.4, 0.5, 0.6, 0.7, 0.8, 0.9)
 
 CONFIGS = {
@@ -172,8 +156,8 @@ CONFIGS = {
     "B_attn_4096": (1, 0, 4096, 4096, 2048, "bf16", (1, 16, 128, 2048, 4096), "built"),
     "C_mlp_up_4096x11008": (2, 0, 4096, 11008, 2048, "bf16", (1, 4096), "built"),
     "C_mlp_down_11008x4096": (2, 1, 11008, 4096, 2048, "bf16", (1, 4096), "built"),
-    "D_70b_sq_8192": (3, 0, 8192, 8192, 4096, "bf16", (1, 4096), "direct"),
-    "D_70b_up_8192x28672": (3, 1, 8192, 28672, 4096, "bf16", (1, 4096), "direct"),
+    "D_70b_sq_8192": (3, 0, 8192, 8192, 4096, "bf16", (1, 4096), "built"),
+    "D_70b_up_8192x28672": (3, 1, 8192, 28672, 4096, "bf16", (1, 4096), "built"),
 }
 for _i, _rho in enumerate(RANK_SWEEP):
     CONFIGS["E_sweep_r%02d" % round(100 * _rho)] = (4, _i, 4096, 4096, int(round(_rho * 4096)), "bf16",

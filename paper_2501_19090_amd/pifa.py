@@ -89,6 +89,8 @@ _SIGNATURES = {
     "pifa_calib_read": (_st, [_vp, _vp, _vp, _vp]),
     "pifa_calib_reconstruct": (_st, [_vp, _vp, _i64, _vp, _i64, ctypes.c_double, ctypes.c_double, _vp, _vp, _vp]),
     "pifa_build_f64": (_st, [_vp, pifa_dims, _vp, _vp, _i32p, _i32p, ctypes.POINTER(ctypes.c_double), _vp]),
+    "pifa_probe_mfma": (_st, [_i64, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double), _vp]),
+    "pifa_probe_hbm_read": (_st, [_vp, _i64, ctypes.c_int, ctypes.POINTER(ctypes.c_double), _vp]),
     "pifa_profile_enable": (_st, [ctypes.c_int]),
     "pifa_profile_reset": (_st, []),
     "pifa_profile_read": (_st, [ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(_i64),
@@ -158,6 +160,28 @@ def _need(t, nbytes: int, name: str) -> None:
         raise ValueError("%s holds %d bytes, the call needs %d" % (name, t.numel() * t.element_size(), nbytes))
 
 
+def _torch_dtype(dt: int):
+    import torch
+    return {PIFA_BF16: torch.bfloat16, PIFA_F32: torch.float32}.get(dt, torch.float64 if dt == "f64" else None)
+
+
+def _same(t, name: str, dt, device=None) -> None:
+    """t (if given) has element type dt (PIFA_BF16, PIFA_F32 or "f64") and lives
+    on the given device index: the library reads raw bytes, so a tensor of
+    another type or on another GPU would be misread, not rejected."""
+    if t is None:
+        return
+    want = _torch_dtype(dt)
+    if want is not None and t.dtype != want:
+        raise TypeError("%s is %s, the call expects %s" % (name, t.dtype, want))
+    if device is not None and t.is_cuda and t.device.index != device:
+        raise ValueError("%s is on cuda:%d, the handle on cuda:%d" % (name, t.device.index, device))
+
+
+def _device_of(t):
+    return t.device.index if (t is not None and t.is_cuda) else None
+
+
 def _remember(handle: int, **dims) -> int:
     with _dims_lock:
         _dims[handle] = dims
@@ -176,6 +200,9 @@ def _forget(handle: int) -> None:
 
 def _check_io(handle: int, X, Y, M: int) -> None:
     d = _recall(handle)
+    if d is not None:
+        _same(X, "X", d["dt"], d.get("dev"))
+        _same(Y, "Y", d["dt"], d.get("dev"))
     if d is not None and M > 0:
         _need(X, M * d["d_in"] * _esize(d["dt"]), "X")
         _need(Y, M * d["d_out"] * _esize(d["dt"]), "Y")
@@ -227,12 +254,15 @@ def pifa_layer_create(W_p, C, pivot_idx, nonpivot_idx, dims, dtype: int | None =
     piv, pp = _host_i32(pivot_idx)
     npv, npp = _host_i32(nonpivot_idx)
     d_in, d_out, r = (int(v) for v in dims)
+    dev = _device_of(W_p)
+    _same(W_p, "W_p", dt, dev)
+    _same(C, "C", dt, dev)
     _need(W_p, r * d_in * _esize(dt), "W_p")
     _need(C, max(d_out - r, 0) * r * _esize(dt), "C")
     out = _vp()
     _check("pifa_layer_create", lib().pifa_layer_create(
         _dev_ptr(W_p, "W_p"), _dev_ptr(C, "C"), pp, npp, pifa_dims(*dims), dt, ctypes.byref(out)))
-    return _remember(out.value, d_in=d_in, d_out=d_out, r=r, dt=dt)
+    return _remember(out.value, d_in=d_in, d_out=d_out, r=r, dt=dt, dev=dev)
 
 
 def pifa_layer_destroy(handle: int) -> None:
@@ -272,6 +302,11 @@ def pifa_layer_backward(handle: int, X, Y, dY, dX=None, dW_p=None, dC=None, M: i
     each output may be None to skip it."""
     M = dY.shape[0] if M is None else int(M)
     d = _recall(handle)
+    if d is not None:
+        for t, name in ((X, "X"), (Y, "Y"), (dY, "dY"), (dX, "dX")):
+            _same(t, name, PIFA_BF16, d.get("dev"))
+        _same(dW_p, "dW_p", PIFA_F32, d.get("dev"))
+        _same(dC, "dC", PIFA_F32, d.get("dev"))
     if d is not None and M > 0:  # bf16 activations and gradients, fp32 weight gradients
         for t, n, name in ((X, M * d["d_in"], "X"), (Y, M * d["d_out"], "Y"), (dY, M * d["d_out"], "dY"),
                            (dX, M * d["d_in"], "dX")):
@@ -289,6 +324,8 @@ def dense_forward(W, X, Y, M: int | None = None, d_in: int | None = None, d_out:
     d_in = W.shape[1] if d_in is None else int(d_in)
     d_out = W.shape[0] if d_out is None else int(d_out)
     dt = _dtype_code(W) if dtype is None else int(dtype)
+    for t, name in ((W, "W"), (X, "X"), (Y, "Y")):
+        _same(t, name, dt, _device_of(W))
     if M > 0:
         _need(W, d_out * d_in * _esize(dt), "W")
         _need(X, M * d_in * _esize(dt), "X")
@@ -302,11 +339,12 @@ def dense_layer_create(W, d_in: int | None = None, d_out: int | None = None,
     d_in = W.shape[1] if d_in is None else int(d_in)
     d_out = W.shape[0] if d_out is None else int(d_out)
     dt = _dtype_code(W) if dtype is None else int(dtype)
+    _same(W, "W", dt)
     _need(W, d_out * d_in * _esize(dt), "W")
     out = _vp()
     _check("dense_layer_create", lib().dense_layer_create(_dev_ptr(W, "W"), d_in, d_out, dt,
                                                           ctypes.byref(out)))
-    return _remember(out.value, d_in=d_in, d_out=d_out, dt=dt)
+    return _remember(out.value, d_in=d_in, d_out=d_out, dt=dt, dev=_device_of(W))
 
 
 def dense_layer_forward(handle: int, X, Y, M: int | None = None, stream=None) -> None:
@@ -331,6 +369,8 @@ def lowrank_uv_forward(U, V, X, Y, M: int | None = None, dims=None, dtype: int |
     dims = (V.shape[1], U.shape[0], U.shape[1]) if dims is None else dims
     dt = _dtype_code(U) if dtype is None else int(dtype)
     d_in, d_out, r = (int(v) for v in dims)
+    for t, name in ((U, "U"), (V, "V"), (X, "X"), (Y, "Y")):
+        _same(t, name, dt, _device_of(U))
     if M > 0:
         _need(U, d_out * r * _esize(dt), "U")
         _need(V, r * d_in * _esize(dt), "V")
@@ -345,12 +385,14 @@ def lowrank_layer_create(U, V, dims=None, dtype: int | None = None) -> int:
     dims = (V.shape[1], U.shape[0], U.shape[1]) if dims is None else dims
     dt = _dtype_code(U) if dtype is None else int(dtype)
     d_in, d_out, r = (int(v) for v in dims)
+    _same(U, "U", dt, _device_of(U))
+    _same(V, "V", dt, _device_of(U))
     _need(U, d_out * r * _esize(dt), "U")
     _need(V, r * d_in * _esize(dt), "V")
     out = _vp()
     _check("lowrank_layer_create", lib().lowrank_layer_create(
         _dev_ptr(U, "U"), _dev_ptr(V, "V"), pifa_dims(*dims), dt, ctypes.byref(out)))
-    return _remember(out.value, d_in=d_in, d_out=d_out, dt=dt)
+    return _remember(out.value, d_in=d_in, d_out=d_out, dt=dt, dev=_device_of(U))
 
 
 def lowrank_layer_forward(handle: int, X, Y, M: int | None = None, stream=None) -> None:
@@ -380,7 +422,10 @@ def pifa_group_create(layers, dtype: int | None = None) -> int:
     dims = (pifa_dims * max(n, 1))()
     keep = []
     dt = (_dtype_code(layers[0][0]) if n else PIFA_BF16) if dtype is None else int(dtype)
+    dev = _device_of(layers[0][0]) if n else None
     for i, (W_p, C, piv, npiv, d) in enumerate(layers):
+        _same(W_p, "W_p", dt, dev)
+        _same(C, "C", dt, dev)
         if dt == PIFA_BF16:  # the only group dtype; the library rejects the others
             _need(W_p, int(d[2]) * int(d[0]) * 2, "W_p")
             _need(C, max(int(d[1]) - int(d[2]), 0) * int(d[2]) * 2, "C")
@@ -394,7 +439,8 @@ def pifa_group_create(layers, dtype: int | None = None) -> int:
         dims[i] = pifa_dims(*d)
     out = _vp()
     _check("pifa_group_create", lib().pifa_group_create(n, wp, cc, pp, npp, dims, dt, ctypes.byref(out)))
-    return _remember(out.value, d_in=int(layers[0][4][0]), d_out=sum(int(l[4][1]) for l in layers), dt=dt)
+    return _remember(out.value, d_in=int(layers[0][4][0]), d_out=sum(int(l[4][1]) for l in layers), dt=dt,
+                     dev=dev)
 
 
 def pifa_group_destroy(handle: int) -> None:
@@ -446,6 +492,9 @@ def pifa_calib_reset(handle: int, stream=None) -> None:
 def pifa_calib_accumulate(handle: int, X_o, X_u, B: int | None = None, stream=None) -> None:
     B = X_u.shape[0] if B is None else int(B)
     d = _recall(handle)
+    if d is not None:
+        _same(X_o, "X_o", PIFA_BF16)
+        _same(X_u, "X_u", PIFA_BF16)
     if d is not None and B > 0:
         _need(X_o, 2 * B * d["n"], "X_o")
         _need(X_u, 2 * B * d["n"], "X_u")
@@ -455,6 +504,8 @@ def pifa_calib_accumulate(handle: int, X_o, X_u, B: int | None = None, stream=No
 
 def pifa_calib_read(handle: int, S=None, P=None, stream=None) -> None:
     d = _recall(handle)
+    _same(S, "S", "f64")
+    _same(P, "P", "f64")
     if d is not None:
         _need(S, 8 * d["n"] * d["n"], "S")
         _need(P, 8 * d["n"] * d["n"], "P")
@@ -470,6 +521,8 @@ def pifa_calib_reconstruct(handle: int, W, Vt, lam: float, alpha: float, U_r=Non
         U_r = torch.empty((d_out, r), dtype=torch.float64, device=W.device)
     if Vt_r is None:
         Vt_r = torch.empty((r, d_in), dtype=torch.float64, device=W.device)
+    for t, name in ((W, "W"), (Vt, "Vt"), (U_r, "U_r"), (Vt_r, "Vt_r")):
+        _same(t, name, "f64", _device_of(W))
     d = _recall(handle)
     if d is not None:
         n = d["n"]
@@ -500,6 +553,23 @@ def pifa_build_f64(W, r: int, stream=None):
         _dev_ptr(W, "W"), pifa_dims(d_in, d_out, r), _dev_ptr(Wp, "W_p"), C.data_ptr() if C.numel() else None,
         piv.ctypes.data_as(_i32p), npp, report, _stream(stream)))
     return piv, npiv, Wp, C, np.array(list(report))
+
+
+def pifa_probe_mfma(iters: int = 20000, stream=None):
+    """(dense bf16 MFMA TFLOP/s, shader clock in MHz) of an MFMA-only kernel."""
+    tf, mhz = ctypes.c_double(), ctypes.c_double()
+    _check("pifa_probe_mfma", lib().pifa_probe_mfma(int(iters), ctypes.byref(tf), ctypes.byref(mhz),
+                                                    _stream(stream)))
+    return tf.value, mhz.value
+
+
+def pifa_probe_hbm_read(buf, reps: int = 5, stream=None) -> float:
+    """GB/s of `reps` streaming reads of the device tensor `buf`."""
+    nbytes = (buf.numel() * buf.element_size()) // 16 * 16
+    out = ctypes.c_double()
+    _check("pifa_probe_hbm_read", lib().pifa_probe_hbm_read(_dev_ptr(buf, "buf"), nbytes, int(reps),
+                                                            ctypes.byref(out), _stream(stream)))
+    return out.value
 
 
 def pifa_profile_enable(on: bool) -> None:

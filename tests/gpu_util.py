@@ -1,8 +1,11 @@
-"""Helpers for the GPU parity tests: seeded layers (built by the oracle or
-drawn directly), upload of the rounded bits, and comparison metrics."""
+"""Helpers for the GPU parity tests: seeded layers built by the oracle,
+upload of the rounded bits, and comparison metrics."""
 from __future__ import annotations
 
+import contextlib
 import functools
+import sys
+import time
 
 import numpy as np
 
@@ -32,20 +35,41 @@ def rel_fro(got, ref) -> float:
     return float(np.linalg.norm(got - ref) / (n if n > 0 else 1.0))
 
 
+# pytest's capture manager (set by conftest): long oracle builds print their
+# progress past the capture, so a run shows it while the build is under way
+CAPTURE_MANAGER = None
+# builds of a W' with at least this many elements report progress
+LARGE_BUILD_ELEMS = 1 << 26
+
+
+def _uncaptured():
+    if CAPTURE_MANAGER is None:
+        return contextlib.nullcontext()
+    return CAPTURE_MANAGER.global_and_fixture_disabled()
+
+
 @functools.lru_cache(maxsize=None)
-def gaussian_layer(d_in: int, d_out: int, r: int, seed: int, kind: str = "built"):
-    """(pivot_idx, nonpivot_idx, W_p, C) in fp64, plus U, V when built."""
-    if kind == "built":
-        U, V = inputs.lowrank_factors(d_out, d_in, r, seed)
+def gaussian_layer(d_in: int, d_out: int, r: int, seed: int):
+    """(pivot_idx, nonpivot_idx, W_p, C, U, V) in fp64: the oracle's PIFA build
+    of the Gaussian rank-r W' = U V.  Built once per process."""
+    U, V = inputs.lowrank_factors(d_out, d_in, r, seed)
+    if d_out * d_in < LARGE_BUILD_ELEMS:
         b = oracle.build_pifa(U @ V, r)
         return b["pivot_idx"], b["nonpivot_idx"], b["Wp"], b["C"], U, V
-    piv, npiv, Wp, C = inputs.direct_layer(d_in, d_out, r, seed)
-    return piv, npiv, Wp, C, None, None
+    with _uncaptured():
+        t0 = time.perf_counter()
+        print("oracle build of the %d x %d rank-%d layer (seed %d) ..." % (d_out, d_in, r, seed),
+              file=sys.stderr, flush=True)
+        b = oracle.build_pifa(U @ V, r, progress=512)
+        print("oracle build of the %d x %d layer done in %.1f s" % (d_out, d_in, time.perf_counter() - t0),
+              file=sys.stderr, flush=True)
+    return b["pivot_idx"], b["nonpivot_idx"], b["Wp"], b["C"], U, V
 
 
 def config_layer(name: str):
     cfg, lay, d_in, d_out, r, dt, Ms, kind = inputs.CONFIGS[name]
-    return gaussian_layer(d_in, d_out, r, inputs.config_seed(cfg, lay), kind)
+    assert kind == "built"
+    return gaussian_layer(d_in, d_out, r, inputs.config_seed(cfg, lay))
 
 
 class DeviceLayer:
@@ -83,13 +107,23 @@ class DeviceLayer:
             self.handle = 0
 
 
-def sample_rows(M: int, k: int = 24, seed: int = 0) -> np.ndarray:
-    """Rows to check against the oracle: all rows when few, else the first,
-    the last and a seeded random subset."""
-    if M <= 64:
+# Rows of Y are independent, so a check may cover a subset of them; up to
+# this many rows every row is compared with the oracle.
+ALL_ROWS_MAX_M = 4096
+
+
+def sample_rows(M: int, k: int | None = None, seed: int = 0) -> np.ndarray:
+    """Rows to compare with the oracle.  By default every row up to
+    ALL_ROWS_MAX_M rows; with k (or above that size) the first row, the last
+    row and a seeded random subset, k + 2 >= 256 rows in all."""
+    if k is None and M <= ALL_ROWS_MAX_M:
+        return np.arange(M)
+    k = 510 if k is None else k
+    if M <= k + 2:
         return np.arange(M)
     rng = np.random.default_rng([seed, M])
-    return np.unique(np.concatenate([[0, M - 1], rng.choice(M, size=k, replace=False)]))
+    inner = rng.choice(np.arange(1, M - 1), size=k, replace=False)
+    return np.unique(np.concatenate([[0, M - 1], inner]))
 
 
 def activations(M: int, d_in: int, seed: int, dtype: str):

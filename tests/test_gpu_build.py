@@ -14,7 +14,7 @@ import pytest
 import oracle
 from paper_2501_19090_amd import inputs
 
-from gpu_util import DeviceLayer, activations, from_dev, rel_fro, sample_rows, torch_mod
+from gpu_util import DeviceLayer, activations, config_layer, from_dev, rel_fro, sample_rows, torch_mod
 
 pytestmark = pytest.mark.gpu
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -48,6 +48,25 @@ def test_build_matches_oracle(d_out, d_in, r):
         assert rel_fro(C, ref["C"]) <= 1e-10
     assert report[3] == 1.0
     assert oracle.reconstruction_error(W, piv, npiv, Wp, C) <= 1e-10
+
+
+@pytest.mark.timeout(900)  # the oracle build of a LLaMA-70B shape takes minutes (then cached)
+@pytest.mark.parametrize("name", ["D_70b_sq_8192", "D_70b_up_8192x28672"])
+def test_build_matches_oracle_llama70b_shapes(name):
+    """The GPU build of the LLaMA-70B layers (8192 x 8192 and 8192 -> 28672,
+    r = 4096) selects exactly the oracle's pivots, and its C agrees."""
+    cfg, lay_i, d_in, d_out, r, *_ = inputs.CONFIGS[name]
+    piv_o, npiv_o, Wp_o, C_o, U, V = config_layer(name)
+    W = U @ V
+    piv, npiv, Wp, C, report = _gpu_build(W, r)
+    assert np.array_equal(piv, piv_o) and np.array_equal(npiv, npiv_o)
+    assert np.array_equal(Wp, Wp_o)
+    err_c = rel_fro(C, C_o)
+    rec = oracle.reconstruction_error(W, piv, npiv, Wp, C)
+    print("%s: identical pivots, C rel_F %.2e, reconstruction %.2e" % (name, err_c, rec), flush=True)
+    assert err_c <= 1e-10
+    assert report[3] == 1.0
+    assert rec <= 1e-10
 
 
 def test_build_worked_examples():
