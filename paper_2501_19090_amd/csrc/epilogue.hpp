@@ -86,6 +86,84 @@ struct ScatterEpi {
     }
 };
 
+// Contiguous-output epilogue with 16-byte stores: out[m * ldo + n] =
+// TOut(acc(m, n) * scale) for m < M, n < N.  The tile is staged in LDS as
+// whole row pieces and written 8 values per store (rows 16-byte aligned:
+// ldo a multiple of 8, out 16-byte aligned).  TOut is bf16 (an output) or
+// f16 (the Y_p hand-off, whose overflows are counted in *overflow when it
+// is not null).
+template <typename TOut>
+struct StagedEpi {
+    static constexpr bool kStaged = true;
+    uint16_t* out;
+    int64_t ldo;
+    int64_t N;
+    float scale;
+    int* overflow;
+    int64_t M;
+
+    // element-wise form, for the K-split reduction
+    struct Col {
+        int64_t n;
+        bool ok;
+    };
+    __device__ __forceinline__ Col col(int64_t n) const { return Col{n, n < N}; }
+    __device__ __forceinline__ uint16_t bits(float v, int& over) const {
+        const float s = v * scale;
+        if constexpr (__is_same(TOut, f16)) {
+            const f16 h = (f16)s;
+            over += !__builtin_isfinite((float)h) && __builtin_isfinite(s);
+            return __builtin_bit_cast(uint16_t, h);
+        } else {
+            return f32_to_bf16_bits(s);
+        }
+    }
+    __device__ __forceinline__ void store(int64_t m, const Col& c, float v) const {
+        if (m >= M || !c.ok) return;
+        int over = 0;
+        out[m * ldo + c.n] = bits(v, over);
+        if (over && overflow) atomicAdd(overflow, over);
+    }
+};
+
+// The pivot product's epilogue of a bf16 prefill: the pivot outputs go to
+// their columns of Y element by element (scatter), and the fp16 hand-off,
+// a contiguous M x ldws matrix, is staged in LDS and written with 16-byte
+// stores.  col / store serve the K-split reduction, element by element.
+struct PivotHandoffEpi {
+    static constexpr bool kDual = true;
+    ScatterEpi<bf16, kWsNone> y;
+    StagedEpi<f16> ws;
+
+    struct Col {
+        typename ScatterEpi<bf16, kWsNone>::Col y;
+        typename StagedEpi<f16>::Col ws;
+    };
+    __device__ __forceinline__ Col col(int64_t n) const { return Col{y.col(n), ws.col(n)}; }
+    __device__ __forceinline__ void store(int64_t m, const Col& c, float v) const {
+        y.store(m, c.y, v);
+        ws.store(m, c.ws, v);
+    }
+    // the same outputs with the hand-off written element by element (for
+    // tiles whose registers cannot hold the staging on top of 128
+    // accumulators per lane)
+    __host__ ScatterEpi<bf16, kWsF16> elementwise() const {
+        ScatterEpi<bf16, kWsF16> e;
+        e.out = y.out;
+        e.ldo = y.ldo;
+        e.idx = y.idx;
+        e.n_out = y.n_out;
+        e.out_scale = y.out_scale;
+        e.ws = ws.out;
+        e.ldws = ws.ldo;
+        e.n_ws = ws.N;
+        e.ws_scale = ws.scale;
+        e.overflow = ws.overflow;
+        e.M = y.M;
+        return e;
+    }
+};
+
 template <typename TOut, int WS>
 __host__ inline ScatterEpi<TOut, WS> make_epi(TOut* out, int64_t ldo, const int32_t* idx,
                                               int64_t n_out, float out_scale, void* ws,

@@ -62,6 +62,34 @@ struct SkipEpi<E, std::void_t<decltype(&E::skip_tile)>> {
     static constexpr bool value = true;
 };
 
+// An epilogue with kStaged writes a contiguous output through LDS with
+// 16-byte stores (StagedEpi).
+template <typename E, typename = void>
+struct StagedEpiT {
+    static constexpr bool value = false;
+};
+template <typename E>
+struct StagedEpiT<E, std::void_t<decltype(E::kStaged)>> {
+    static constexpr bool value = true;
+};
+
+// An epilogue with kDual has a per-element part (y) and a staged part (ws).
+template <typename E, typename = void>
+struct DualEpiT {
+    static constexpr bool value = false;
+};
+template <typename E>
+struct DualEpiT<E, std::void_t<decltype(E::kDual)>> {
+    static constexpr bool value = true;
+};
+
+// LDS bytes of a BM x BN tile of T with K step BK: the double-buffered
+// operand tiles (the staged epilogues reuse them after the K loop).
+template <typename T, int BM, int BN, int BK>
+constexpr int gemm_lds_bytes() {
+    return 2 * (BM + BN) * (BK + 8) * (int)sizeof(T);
+}
+
 template <typename T>
 struct Mfma;
 
@@ -142,6 +170,57 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc31(const void* base, 
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, 0x00020000);
 }
 
+// Store tile (m0, n0) of a contiguous output (StagedEpi): each chunk of R
+// rows is written to LDS as TOut rows of BN values (pitch BN + 8, which
+// spreads the column-wise writes over the banks), then read back and stored 8
+// values per 16-byte store; columns at or past N are not stored.
+template <int BM, int BN, int WM, int WN, int TM, int TN, typename TOut>
+__device__ __forceinline__ void staged_store(const f32x16 (&acc)[TM][TN], int64_t m0, int64_t n0,
+                                             const StagedEpi<TOut>& e, char* smem, int lds_bytes) {
+    constexpr int NT = WM * WN * kWave;
+    constexpr int WTM = BM / WM, WTN = BN / WN;
+    constexpr int P = BN + 8;       // LDS row pitch in elements
+    constexpr int G = BN / 8;       // 16-byte groups per row
+    constexpr int R0 = (BM * P * 2 <= 163840) ? BM : 163840 / (2 * P);
+    const int R = (lds_bytes / (2 * P)) < R0 ? (lds_bytes / (2 * P)) : R0;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const int wm = wave / WN, wn = wave % WN;
+    uint16_t* tile = reinterpret_cast<uint16_t*>(smem);
+    int over = 0;
+    for (int r0 = 0; r0 < BM && m0 + r0 < e.M; r0 += R) {
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int nl = wn * WTN + j * 32 + (lane & 31);
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int ml = wm * WTM + i * 32 + 4 * (lane >> 5) + 8 * (v >> 2) + (v & 3) - r0;
+                    if ((unsigned)ml < (unsigned)R && m0 + r0 + ml < e.M && n0 + nl < e.N)
+                        tile[ml * P + nl] = e.bits(acc[i][j][v], over);
+                }
+            }
+        }
+        __syncthreads();
+        for (int q = threadIdx.x; q < R * G; q += NT) {
+            const int rr = q / G, g = q % G;
+            const int64_t m = m0 + r0 + rr, n = n0 + 8 * g;
+            if (m >= e.M || n >= e.N) continue;
+            const u32x4 v = *reinterpret_cast<const u32x4*>(tile + rr * P + 8 * g);
+            uint16_t* dst = e.out + m * e.ldo + n;
+            if (n + 8 <= e.N) {
+                *reinterpret_cast<u32x4*>(dst) = v;
+            } else {
+                const uint16_t* hv = reinterpret_cast<const uint16_t*>(&v);
+                for (int x = 0; x < 8 && n + x < e.N; ++x) dst[x] = hv[x];
+            }
+        }
+    }
+    if (over && e.overflow) atomicAdd(e.overflow, over);
+}
+
 // One output tile (tm, tn) over the K range [kbeg, kend); both operands are
 // masked outside that range.
 template <typename T, int BM, int BN, int BK, int WM, int WN, bool BPACK, int PGR, typename Epi>
@@ -164,8 +243,10 @@ __device__ __forceinline__ void gemm_nt_tile(const T* __restrict__ A, int64_t ld
     static_assert(!BPACK || ((BK == 64 || BK == 128) && BN % kPackRows == 0), "bad packed tile");
     static_assert(PGR >= 1 && PGR <= 4, "prefetch depth");
 
-    __shared__ __attribute__((aligned(16))) T As[2][BM * LDK];
-    __shared__ __attribute__((aligned(16))) T Bs[2][BN * LDK];
+    constexpr int LDS_BYTES = gemm_lds_bytes<T, BM, BN, BK>();
+    __shared__ __attribute__((aligned(16))) char smem[LDS_BYTES];
+    T(*As)[BM * LDK] = reinterpret_cast<T(*)[BM * LDK]>(smem);
+    T(*Bs)[BN * LDK] = reinterpret_cast<T(*)[BN * LDK]>(smem + 2 * BM * LDK * sizeof(T));
 
     const int64_t m0 = tm * BM, n0 = tn * BN;
     if constexpr (SkipEpi<Epi>::value) {
@@ -310,6 +391,23 @@ __device__ __forceinline__ void gemm_nt_tile(const T* __restrict__ A, int64_t ld
     for (int u = 0; u < PGR - 1; ++u)
         if (kt + u < nk) body(kt + u, S[(u + 1) % PGR]);
 
+    if constexpr (StagedEpiT<Epi>::value) {
+        staged_store<BM, BN, WM, WN, TM, TN>(acc, m0, n0, epi, smem, LDS_BYTES);
+        return;
+    } else if constexpr (DualEpiT<Epi>::value) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const auto c = epi.y.col(n0 + wn * WTN + j * 32 + (lane & 31));
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                const int64_t mb = m0 + wm * WTM + i * 32 + 4 * (lane >> 5);
+#pragma unroll
+                for (int v = 0; v < 16; ++v) epi.y.store(mb + 8 * (v >> 2) + (v & 3), c, acc[i][j][v]);
+            }
+        }
+        staged_store<BM, BN, WM, WN, TM, TN>(acc, m0, n0, epi.ws, smem, LDS_BYTES);
+        return;
+    } else {
     // 32x32 accumulator layout: lane holds column (lane % 32) and rows
     // 8*(v/4) + 4*(lane/32) + (v%4) for v = 0..15.
 #pragma unroll
@@ -330,6 +428,7 @@ __device__ __forceinline__ void gemm_nt_tile(const T* __restrict__ A, int64_t ld
                 for (int v = 0; v < 16; ++v) epi.store(mb + 8 * (v >> 2) + (v & 3), c, acc[i][j][v]);
             }
         }
+    }
     }
 }
 

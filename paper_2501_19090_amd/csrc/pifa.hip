@@ -300,7 +300,10 @@ hipError_t launch_gemm(int site, const T* A, int64_t lda, int64_t M, const T* B,
     const GemmPlan g = gemm_plan(M, N, K, kWideOk, partials != nullptr);
     const dim3 grid((unsigned)(ceil_div(M, g.bm) * ceil_div(N, g.bn)));
     if (g.bm == 256 && g.bn == 256) {
-        if constexpr (kWideOk)
+        if constexpr (DualEpiT<Epi>::value)
+            hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 256, kGemmBK, 2, 4, BPACK, 1, ScatterEpi<bf16, kWsF16>>), grid,
+                               dim3(8 * kWave), 0, st, A, lda, M, B, ldb, N, K, K, epi.elementwise());
+        else if constexpr (kWideOk)
             hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 256, kGemmBK, 2, 4, BPACK, 1, Epi>), grid, dim3(8 * kWave), 0,
                                st, A, lda, M, B, ldb, N, K, K, epi);
     } else if (g.bm == 256 && g.bn == 192) {
@@ -712,6 +715,10 @@ size_t lowrank_ws_bytes(pifa_dtype dt, int64_t M, int64_t r_cols) {
     return (size_t)M * (size_t)r_cols * 2;
 }
 
+// A contiguous output with rows of ld elements at p can take the staged
+// 16-byte-store epilogue.
+inline bool staged_ok(const void* p, int64_t ld) { return aligned16(p) && ld % 8 == 0; }
+
 // Y = (X V^T) U^T.  V: r_cols x d_in, U: d_out x r_cols, both in lane order
 // when PACKED (bf16 handle), else row-major (stateless call, fp32).
 template <bool PACKED>
@@ -753,16 +760,26 @@ pifa_status lowrank_run(pifa_dtype dt, const void* U, const void* V, const void*
         return e == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
     }
     bf16* t = (bf16*)T;
-    e = launch_gemm<bf16, PACKED>(kSiteLowrankGemm1, (const bf16*)X, d_in, M, (const bf16*)V, d_in,
-                                  r_cols, d_in,
-                                  make_epi<bf16, kWsNone>(t, r_cols, nullptr, r_cols, 1.f, nullptr, 0,
-                                                          0, 1.f, nullptr, M),
-                                  partials, st);
+    // contiguous outputs with 16-byte rows take the staged 16-byte-store
+    // epilogue, as the PIFA hand-off does
+    if (staged_ok(t, r_cols))
+        e = launch_gemm<bf16, PACKED>(kSiteLowrankGemm1, (const bf16*)X, d_in, M, (const bf16*)V, d_in, r_cols, d_in,
+                                      StagedEpi<bf16>{(uint16_t*)t, r_cols, r_cols, 1.f, nullptr, M}, partials, st);
+    else
+        e = launch_gemm<bf16, PACKED>(kSiteLowrankGemm1, (const bf16*)X, d_in, M, (const bf16*)V, d_in,
+                                      r_cols, d_in,
+                                      make_epi<bf16, kWsNone>(t, r_cols, nullptr, r_cols, 1.f, nullptr, 0,
+                                                              0, 1.f, nullptr, M),
+                                      partials, st);
     if (e != hipSuccess) return PIFA_ERR_HIP;
-    e = launch_gemm<bf16, PACKED>(kSiteLowrankGemm2, t, r_cols, M, (const bf16*)U, r_cols, d_out, r_cols,
-                                  make_epi<bf16, kWsNone>((bf16*)Y, d_out, nullptr, d_out, 1.f, nullptr,
-                                                          0, 0, 1.f, nullptr, M),
-                                  partials, st);
+    if (staged_ok(Y, d_out))
+        e = launch_gemm<bf16, PACKED>(kSiteLowrankGemm2, t, r_cols, M, (const bf16*)U, r_cols, d_out, r_cols,
+                                      StagedEpi<bf16>{(uint16_t*)Y, d_out, d_out, 1.f, nullptr, M}, partials, st);
+    else
+        e = launch_gemm<bf16, PACKED>(kSiteLowrankGemm2, t, r_cols, M, (const bf16*)U, r_cols, d_out, r_cols,
+                                      make_epi<bf16, kWsNone>((bf16*)Y, d_out, nullptr, d_out, 1.f, nullptr,
+                                                              0, 0, 1.f, nullptr, M),
+                                      partials, st);
     return e == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
 }
 
@@ -788,8 +805,12 @@ pifa_status dense_run(pifa_dtype dt, const void* W, const void* X, void* Y, int6
             e = launch_skinny_rowmajor<bf16>(kSiteDenseGemv, a, (const bf16*)W, d_in, d_out, d_in, epi, st);
         return e == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
     }
-    e = launch_gemm<bf16, PACKED>(kSiteDenseGemm, (const bf16*)X, d_in, M, (const bf16*)W, d_in, d_out,
-                                  d_in, epi, partials, st);
+    if (staged_ok(Y, d_out))
+        e = launch_gemm<bf16, PACKED>(kSiteDenseGemm, (const bf16*)X, d_in, M, (const bf16*)W, d_in, d_out, d_in,
+                                      StagedEpi<bf16>{(uint16_t*)Y, d_out, d_out, 1.f, nullptr, M}, partials, st);
+    else
+        e = launch_gemm<bf16, PACKED>(kSiteDenseGemm, (const bf16*)X, d_in, M, (const bf16*)W, d_in, d_out,
+                                      d_in, epi, partials, st);
     return e == hipSuccess ? PIFA_OK : PIFA_ERR_HIP;
 }
 
@@ -894,11 +915,13 @@ pifa_status forward_with(pifa_layer* h, const void* X, void* Y, int64_t M, void*
     }
 
     f16* yp = (f16*)ws;
+    // pivot outputs scattered to their columns; the hand-off (contiguous,
+    // 16-byte rows) staged and written 16 bytes at a time
+    PivotHandoffEpi pe;
+    pe.y = make_epi<bf16, kWsNone>((bf16*)Y, h->d_out, h->piv, h->r, 1.f, nullptr, 0, 0, 1.f, nullptr, M);
+    pe.ws = StagedEpi<f16>{(uint16_t*)yp, h->r_pad, h->r_pad, y_scale, h->overflow, M};
     e = launch_gemm<bf16, true>(kSitePifaGemm1, (const bf16*)X, h->d_in, M, (const bf16*)h->Wp, 0, h->r_pad,
-                                h->d_in,
-                                make_epi<bf16, kWsF16>((bf16*)Y, h->d_out, h->piv, h->r, 1.f, yp, h->r_pad,
-                                                       h->r_pad, y_scale, h->overflow, M),
-                                part, st);
+                                h->d_in, pe, part, st);
     if (e != hipSuccess) return PIFA_ERR_HIP;
     if (h->n_np > 0) {
         e = launch_gemm<f16, true>(kSitePifaGemm2, yp, h->r_pad, M, (const f16*)h->C, 0, h->n_np, h->r_pad,

@@ -424,9 +424,9 @@ def pifa_group_create(layers, dtype: int | None = None) -> int:
     dt = (_dtype_code(layers[0][0]) if n else PIFA_BF16) if dtype is None else int(dtype)
     dev = _device_of(layers[0][0]) if n else None
     for i, (W_p, C, piv, npiv, d) in enumerate(layers):
-        _same(W_p, "W_p", dt, dev)
-        _same(C, "C", dt, dev)
         if dt == PIFA_BF16:  # the only group dtype; the library rejects the others
+            _same(W_p, "W_p", dt, dev)
+            _same(C, "C", dt, dev)
             _need(W_p, int(d[2]) * int(d[0]) * 2, "W_p")
             _need(C, max(int(d[1]) - int(d[2]), 0) * int(d[2]) * 2, "C")
         wp[i] = _dev_ptr(W_p, "W_p")

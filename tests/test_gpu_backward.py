@@ -71,8 +71,10 @@ def test_backward_full_size_sampled():
         x_dev, x64 = activations(M, lay.d_in, 21, "bf16")
         g_dev, g64 = activations(M, lay.d_out, 22, "bf16")
         dX, dWp, dC = _grads(lay, x_dev, g_dev, M)
-        # dX rows depend only on their own rows of X and G
-        rows = sample_rows(M)
+        # dX rows depend only on their own rows of X and G: the first, the
+        # last and 510 seeded rows (the oracle's backward of all 4096 rows
+        # takes minutes)
+        rows = sample_rows(M, k=510)
         rX, _, _ = oracle.pifa_backward(x64[rows], g64[rows], lay.piv, lay.npiv, lay.Wp, lay.C)
         assert rel_fro(from_dev(dX)[rows], rX) <= TOL
         # dW_p[S, :] and dC[:, S] for a few pivot slots S: the same gradients
@@ -122,8 +124,12 @@ def test_backward_rejects_f32_layer():
     lay = DeviceLayer(piv, npiv, Wp, C, "f32")
     try:
         x_dev, _ = activations(4, 64, 1, "f32")
-        with pytest.raises(pifa.PifaError) as e:
+        # the binding refuses fp32 activations for the (bf16-only) backward ...
+        with pytest.raises(TypeError):
             pifa.pifa_layer_backward(lay.handle, x_dev, x_dev, x_dev, None, None, None, 4)
-        assert e.value.status == pifa.PIFA_ERR_UNSUPPORTED
+        # ... and the library itself refuses the fp32 layer
+        st = pifa.lib().pifa_layer_backward(lay.handle, x_dev.data_ptr(), x_dev.data_ptr(), x_dev.data_ptr(), 4,
+                                            None, None, None, None)
+        assert st == pifa.PIFA_ERR_UNSUPPORTED
     finally:
         lay.close()
