@@ -55,8 +55,10 @@ typedef enum {
     PIFA_ERR_NOT_SPD = -7,     /* pifa_calib_reconstruct: a normal-      */
                                /* equation matrix is not positive        */
                                /* definite (too few calibration rows)    */
-    PIFA_ERR_WRONG_DEVICE = -8 /* a handle used while another device is  */
-                               /* current than the one it was created on */
+    PIFA_ERR_WRONG_DEVICE = -8, /* a handle used while another device is */
+                                /* current than the one it was created on*/
+    PIFA_ERR_TOO_LARGE = -9     /* pifa_forward_noalloc: the call needs   */
+                                /* more workspace than its fixed scratch */
 } pifa_status;
 
 /* Layer shape: W is d_out x d_in with rank r, 1 <= r <= min(d_in, d_out)
@@ -144,6 +146,25 @@ pifa_status pifa_layer_reserve(pifa_handle h, int64_t max_M);
  * and produces non-finite outputs in that row.
  */
 pifa_status pifa_forward(pifa_handle h, const void* X, void* Y, int64_t M, void* stream);
+
+/*
+ * pifa_forward for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).
+ * Same arguments, results and stream semantics as pifa_forward, bit for bit,
+ * but the workspace is a fixed 32 MiB array in the library's device memory
+ * (one per GPU, held until the process ends) instead of the handle's: the
+ * call allocates nothing, on the device or the host, and never synchronises.
+ * The Y_p hand-off (M * r_pad * 4 bytes for M <= 16, M * r_pad * 2 above;
+ * fp32 layers M * r * 4; r_pad = r rounded up to 64) rounded up to 256
+ * bytes, plus the K-split partial products of small batches, must fit in
+ * those 32 MiB, else PIFA_ERR_TOO_LARGE and nothing is launched (for the
+ * 4096 x 4096, r = 2048 layer every M up to 8192 fits).  Every call on a GPU
+ * shares that GPU's array: calls that overlap on one GPU, on any stream or
+ * handle, race and give undefined results.  Nothing in the array needs to
+ * start at zero (every call writes what it reads).  Launches are never
+ * timed by pifa_profile_*.
+ */
+pifa_status pifa_forward_noalloc(pifa_handle h, const void* X, void* Y, int64_t M, void* stream);
 
 /* Bytes of weights and indices a forward must read: r*d_in + (d_out-r)*r
  * elements of the dtype plus d_out int32 indices (Sec. 3.3 memory cost). */

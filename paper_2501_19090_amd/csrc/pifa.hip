@@ -161,6 +161,10 @@ Profiler& profiler() {
     return p;
 }
 
+// Set while a call runs that must create nothing (pifa_forward_noalloc):
+// its launches are never bracketed by profiling events.
+thread_local bool t_untimed = false;
+
 // Brackets one launch with events when profiling is on.
 struct TimedLaunch {
     int site;
@@ -168,7 +172,7 @@ struct TimedLaunch {
     hipEvent_t start = nullptr, stop = nullptr;
     TimedLaunch(int s, hipStream_t stream) : site(s), st(stream) {
         Profiler& p = profiler();
-        if (!p.on) return;
+        if (!p.on || t_untimed) return;
         std::lock_guard<std::mutex> g(p.mu);
         start = p.get();
         stop = p.get();
@@ -830,6 +834,7 @@ const char* pifa_status_string(pifa_status s) {
         case PIFA_ERR_NOT_RANK_R: return "PIFA_ERR_NOT_RANK_R";
         case PIFA_ERR_NOT_SPD: return "PIFA_ERR_NOT_SPD";
         case PIFA_ERR_WRONG_DEVICE: return "PIFA_ERR_WRONG_DEVICE";
+        case PIFA_ERR_TOO_LARGE: return "PIFA_ERR_TOO_LARGE";
     }
     return "PIFA_ERR_UNKNOWN";
 }
@@ -1999,6 +2004,53 @@ pifa_status pifa_profile_read(const char** names, int64_t* launches, double* tot
     }
     *n_sites = n;
     return status;
+}
+
+// ------------------------------------------------------------------ allocation-free forward
+namespace {
+
+// The workspace of pifa_forward_noalloc: one fixed array per GPU, held until
+// the process ends.  In host code `scratch` names a host-side stand-in, not
+// the device memory; its device address on each GPU comes from
+// hipGetSymbolAddress, called once per device with that device current.
+constexpr size_t kNoAllocScratchBytes = 32ull << 20;
+static __device__ __align__(256) uint8_t scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+pifa_status scratch_address(int dev, void** out) {
+    if (dev < 0 || dev >= kMaxDevices) return PIFA_ERR_UNSUPPORTED;
+    std::lock_guard<std::mutex> g(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return PIFA_ERR_HIP;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return PIFA_OK;
+}
+
+}  // namespace
+
+pifa_status pifa_forward_noalloc(pifa_handle h, const void* X, void* Y, int64_t M, void* stream) {
+    if (!h || M < 0) return PIFA_ERR_INVALID_ARG;
+    if (M == 0) return PIFA_OK;
+    if (!X || !Y) return PIFA_ERR_INVALID_ARG;
+    PIFA_ON_DEVICE(h->device);
+    if (h->dtype == PIFA_BF16 && !aligned16(X)) return PIFA_ERR_UNSUPPORTED;
+    const size_t ws = (size_t)round_up((int64_t)pifa_ws_bytes(h, M), 256);
+    const size_t part = pifa_part_bytes(h, M);
+    if (ws + part > kNoAllocScratchBytes) return PIFA_ERR_TOO_LARGE;
+    void* base = nullptr;
+    const pifa_status s = scratch_address(h->device, &base);
+    if (s != PIFA_OK) return s;
+    t_untimed = true;
+    const pifa_status r = forward_with(h, X, Y, M, base, part ? (float*)((char*)base + ws) : nullptr,
+                                       as_stream(stream));
+    t_untimed = false;
+    return r;
 }
 
 // ------------------------------------------------------------------ peak probes

@@ -30,6 +30,7 @@ PIFA_ERR_OOM = -5
 PIFA_ERR_NOT_RANK_R = -6
 PIFA_ERR_NOT_SPD = -7
 PIFA_ERR_WRONG_DEVICE = -8
+PIFA_ERR_TOO_LARGE = -9
 
 
 class pifa_dims(ctypes.Structure):
@@ -59,6 +60,7 @@ _SIGNATURES = {
     "pifa_layer_destroy": (_st, [_vp]),
     "pifa_layer_reserve": (_st, [_vp, _i64]),
     "pifa_forward": (_st, [_vp, _vp, _vp, _i64, _vp]),
+    "pifa_forward_noalloc": (_st, [_vp, _vp, _vp, _i64, _vp]),
     "pifa_layer_weight_bytes": (ctypes.c_size_t, [_vp]),
     "pifa_layer_set_intermediate_scale": (_st, [_vp, ctypes.c_int]),
     "pifa_layer_overflow_count": (_st, [_vp, ctypes.POINTER(_i64)]),
@@ -279,6 +281,15 @@ def pifa_forward(handle: int, X, Y, M: int | None = None, stream=None) -> None:
     _check_io(handle, X, Y, M)
     _check("pifa_forward", lib().pifa_forward(handle, _dev_ptr(X, "X"), _dev_ptr(Y, "Y"), M,
                                               _stream(stream)))
+
+
+def pifa_forward_noalloc(handle: int, X, Y, M: int | None = None, stream=None) -> None:
+    """pifa_forward with the library's fixed per-GPU scratch as workspace (no
+    allocation; calls on one GPU must not overlap)."""
+    M = X.shape[0] if M is None else int(M)
+    _check_io(handle, X, Y, M)
+    _check("pifa_forward_noalloc", lib().pifa_forward_noalloc(handle, _dev_ptr(X, "X"), _dev_ptr(Y, "Y"), M,
+                                                              _stream(stream)))
 
 
 def pifa_layer_weight_bytes(handle: int) -> int:
