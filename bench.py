@@ -481,8 +481,8 @@ def cpu_baseline(wl, M_full, budget_s=4.0):
 
 
 def traffic_from_profiles(kernel: str):
-    """HBM bytes per launch from a committed counter summary, if it matches
-    the current kernel sources; else None."""
+    """HBM bytes per launch from a committed counter summary, if it was taken
+    on the current version of the forward kernels; else None."""
     path = os.path.join(ROOT, "profiles", "%s_attn4096_M4096_traffic.txt" % kernel)
     if not os.path.exists(path):
         return None
@@ -490,7 +490,7 @@ def traffic_from_profiles(kernel: str):
         with open(path) as f:
             rec = json.load(f)
         from paper_2501_19090_amd import build
-        if rec.get("source_digest") != build.source_digest():
+        if rec.get("forward_kernel_digest") != build.forward_kernel_digest():
             return None
         return rec.get("hbm_bytes_per_launch")
     except Exception:
@@ -531,6 +531,7 @@ def main():
         sys.exit(2)
 
     import torch
+    from paper_2501_19090_amd import build as build_mod
     from paper_2501_19090_amd import inputs, pifa
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -686,8 +687,9 @@ def main():
     torch.cuda.empty_cache()
     peak_check = {"mfma_only_tflops": probe_tflops, "sclk_mhz_under_mfma": sclk_mhz,
                   "peak_bf16_tflops_at_that_clock": peak_at_clock, "hbm_read_gbps": hbm_read,
-                  "what": "MFMA-only kernel (2048 x 4 waves of independent 32x32x16 bf16 MFMAs) and 5 "
-                          "streaming reads of a 1 GiB buffer, on this GPU in this run"}
+                  "what": "MFMA-only kernel (2048 x 4 waves of independent 32x32x16 bf16 MFMAs) and "
+                          "grid-stride streaming reads of a zero-filled 1 GiB buffer (best of 3 grid sizes, "
+                          "5 reads each), on this GPU in this run"}
     log("peak check:", json.dumps(peak_check))
     cpu = None
     if not args.no_cpu:
@@ -713,6 +715,7 @@ def main():
                    "d_in": d_in, "d_out": d_out, "r": r, "M": M},
         "roofline": roofline,
         "peak_check": peak_check,
+        "forward_kernel_digest": build_mod.forward_kernel_digest(),
         "cpu_baseline": cpu,
         "hbm_gbps_decode": decode["pifa_gbps"],
         "speedup_vs_uv": pre["speedup_vs_uv"],
@@ -740,7 +743,8 @@ def main():
 
 def run_full(args):
     """Every configuration at its M values: PIFA vs U V vs dense."""
-    from paper_2501_19090_amd import inputs
+    from paper_2501_19090_amd import build, inputs
+    digest = build.source_digest()
     rows = []
     for name, (cfg, lay, d_in, d_out, r, dt, Ms, kind) in inputs.CONFIGS.items():
         if dt != "bf16":
@@ -752,6 +756,7 @@ def run_full(args):
             # settled under the load being timed (about 150 launches at 4096 rows)
             res = measure(wl, M, 100 if rotate else 50, 10 if rotate else 200, rotate)
             res.update({"config": name, "d_in": d_in, "d_out": d_out, "r": r, "build_ms": wl.build_ms,
+                        "source_digest": digest,
                         "pifa_weight_bytes": wl.pifa_bytes, "uv_weight_bytes": wl.uv_bytes,
                         "dense_weight_bytes": wl.dense_bytes,
                         "pifa_frac_mfma": res["pifa_tflops"] / PEAK_BF16_TFLOPS,
@@ -769,7 +774,7 @@ def run_full(args):
     wl = Workload(d_in, d_out, r, inputs.config_seed(cfg, lay))
     for M in (17, 32, 64, 256, 512):
         res = measure(wl, M, 100, 200, False)
-        res.update({"config": name + "_small_batch", "d_in": d_in, "d_out": d_out, "r": r,
+        res.update({"config": name + "_small_batch", "d_in": d_in, "d_out": d_out, "r": r, "source_digest": digest,
                     "pifa_frac_mfma": res["pifa_tflops"] / PEAK_BF16_TFLOPS,
                     "pifa_frac_hbm": res["pifa_gbps"] / PEAK_HBM_GBPS})
         log(json.dumps({k: (round(v, 4) if isinstance(v, float) else v) for k, v in res.items() if k != "kernels"}))

@@ -396,8 +396,10 @@ pifa_status pifa_profile_read(const char** names, int64_t* launches, double* tot
  *
  * pifa_probe_hbm_read: `reps` back-to-back reads of the device buffer `buf`
  * (`bytes` a multiple of 16, 16-byte aligned; larger than the 256 MB
- * Infinity Cache to measure HBM) with 16-byte loads; *gbps = bytes * reps /
- * the elapsed time of the `reps` launches (one untimed launch first).
+ * Infinity Cache to measure HBM) with 16-byte loads in a grid-stride loop;
+ * *gbps = bytes * reps / the elapsed time of the `reps` launches (one
+ * untimed launch first), the best of grids of 2048, 4096 and 8192
+ * workgroups of 256 threads.
  * Both return PIFA_ERR_INVALID_ARG for a bad argument and PIFA_ERR_HIP if
  * a launch or event fails.
  */

@@ -38,6 +38,24 @@ def source_digest() -> str:
     return h.hexdigest()[:16]
 
 
+# The headers that hold the forward pass's kernels (the prefill GEMM with its
+# epilogues and the decode weight streams); counters taken on one version of
+# them stay valid while these files are unchanged.
+FORWARD_KERNEL_SOURCES = ("common.hpp", "layout.hpp", "epilogue.hpp", "gemm_mfma.hpp", "gemv_skinny.hpp",
+                          "prepack.hpp")
+
+
+def forward_kernel_digest() -> str:
+    """sha256 over the forward kernels' headers (identifies their version)."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in FORWARD_KERNEL_SOURCES:
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(f.encode())
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
 def build(verbose: bool = False) -> str:
     """Always recompile (this is the build check); returns the library path."""
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

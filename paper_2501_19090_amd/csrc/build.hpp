@@ -2,13 +2,11 @@
 //
 // QR with column pivoting (Businger & Golub) on A = W'^T: column j of A is
 // row j of W', so A is held as d_out contiguous columns of length d_in -- the
-// bytes of W' in row-major order.  Step k:
-//   qr_pivot_reflect (one workgroup): pick the column of largest residual
-//     norm (ties to the lowest original row index), swap it into position k,
-//     and turn A[k:, k] into a Householder reflector H = I - tau v v^T
-//     (v[0] = 1 implicit, v[1:] stored below the diagonal, R[k][k] on it);
-//   qr_apply (one wave per trailing column): a_j -= tau (v^T a_j) v and the
-//     residual norm ||a_j[k+1:]||^2 recomputed exactly in the same pass.
+// bytes of W' in row-major order.  Step k picks the column of largest
+// residual norm (ties to the lowest original row index), swaps it into
+// position k and turns A[k:, k] into a Householder reflector H = I - tau v v^T
+// (v[0] = 1 implicit, v[1:] stored below the diagonal, R[k][k] on it); the
+// steps run in panels whose trailing update is one GEMM (qr_panel_* below).
 // After r steps R11 (r x r, upper triangular) and R12 (r x (d_out - r)) sit in
 // the first r entries of the columns.  The coefficient matrix solves
 // W_p^T C^T = W_np^T in the least-squares sense through those factors:
@@ -49,30 +47,54 @@ __global__ __launch_bounds__(256) void qr_init(const double* __restrict__ W, dou
     }
 }
 
-// Step k, part 1 (a single workgroup of kBuildThreads threads).
-// scal[0] = tau_k; status[0] is set to 1 if the pivot column is zero.
-__global__ __launch_bounds__(kBuildThreads) void qr_pivot_reflect(double* __restrict__ A,
-                                                                  double* __restrict__ norm2,
-                                                                  int32_t* __restrict__ perm,
-                                                                  double* __restrict__ tau,
-                                                                  int* __restrict__ status, int64_t k,
-                                                                  int64_t d_out, int64_t d_in) {
+// The pivoting runs in panels of at most kPanel steps (the blocked form of
+// LAPACK's xGEQP3 / xLAQPS): inside a panel the trailing columns are not
+// updated; each step k = k0 + j instead adds a column to
+//   F (d_out x kPanel, row c at F + c * kPanel):  F[c, j] = tau_k a_c^(k)T v_k,
+// where a_c^(k) = a_c - V[:, 0:j] F[c, 0:j]^T is column c after the panel's
+// earlier reflections and V holds their Householder vectors (stored in
+// A's columns k0 .. k-1 below the diagonal, with an implicit 1 on it).  Row k
+// of every trailing column is brought up to date at its step (it becomes
+// row k of R), and the residual norms are downdated by that row's squares.
+// At the end of a panel one GEMM, A[rows >= k0+nb, cols >= k0+nb] -= V F^T,
+// applies the panel's reflections to the rest of the trailing matrix, and
+// the residual norms of the trailing columns are recomputed exactly, so every
+// panel starts from exact norms.  The trailing matrix is read once per step
+// and written once per panel, instead of read twice and written once per
+// step.
+constexpr int kPanel = 16;
+
+// Step k = k0 + j, part 1 (a single workgroup of kBuildThreads threads):
+//   * pivot: the column of largest (downdated) residual norm, ties to the
+//     lowest original index; swap it into position k (A columns, F rows,
+//     norms, perm);
+//   * bring column k's rows [k, d_in) up to date: a_k -= V[:, 0:j] F[k, 0:j]^T;
+//   * turn a_k[k:] into a Householder reflector (R[k][k] on the diagonal,
+//     v[1:] below it, tau[k]);
+//   * aux[t] = -tau_k V[k:, t]^T v_k for t < j (for F's recurrence).
+// status[0] is set to 1 if the pivot column is zero.
+__global__ __launch_bounds__(kBuildThreads) void qr_panel_pivot(double* __restrict__ A, double* __restrict__ norm2,
+                                                                int32_t* __restrict__ perm, double* __restrict__ F,
+                                                                double* __restrict__ tau, double* __restrict__ aux,
+                                                                int* __restrict__ status, int64_t k, int64_t k0,
+                                                                int64_t d_out, int64_t d_in) {
     __shared__ double s_val[kBuildThreads / kWave];
     __shared__ int64_t s_idx[kBuildThreads / kWave];
     __shared__ int32_t s_key[kBuildThreads / kWave];
-    __shared__ int64_t s_p;
+    __shared__ double fk[kPanel];
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    const int j = (int)(k - k0);
 
     // argmax of norm2[k..d_out), ties to the lowest original index perm[]
     double bv = -1.0;
     int64_t bi = -1;
     int32_t bk = INT32_MAX;
-    for (int64_t j = k + tid; j < d_out; j += kBuildThreads) {
-        const double v = norm2[j];
-        const int32_t key = perm[j];
+    for (int64_t c = k + tid; c < d_out; c += kBuildThreads) {
+        const double v = norm2[c];
+        const int32_t key = perm[c];
         if (v > bv || (v == bv && key < bk)) {
             bv = v;
-            bi = j;
+            bi = c;
             bk = key;
         }
     }
@@ -99,14 +121,12 @@ __global__ __launch_bounds__(kBuildThreads) void qr_pivot_reflect(double* __rest
                 bi = s_idx[w];
                 bk = s_key[w];
             }
-        s_val[0] = bv;
         s_idx[0] = bi;
-        s_key[0] = bk;
     }
     __syncthreads();
     const int64_t p = s_idx[0];
 
-    // swap columns k and p
+    // swap columns k and p, with their F rows, norms and original indices
     if (p != k) {
         double* ak = A + k * d_in;
         double* ap = A + p * d_in;
@@ -114,6 +134,11 @@ __global__ __launch_bounds__(kBuildThreads) void qr_pivot_reflect(double* __rest
             const double t = ak[i];
             ak[i] = ap[i];
             ap[i] = t;
+        }
+        if (tid < j) {
+            const double t = F[k * kPanel + tid];
+            F[k * kPanel + tid] = F[p * kPanel + tid];
+            F[p * kPanel + tid] = t;
         }
         if (tid == 0) {
             const int32_t tp = perm[k];
@@ -125,19 +150,50 @@ __global__ __launch_bounds__(kBuildThreads) void qr_pivot_reflect(double* __rest
         }
     }
     __syncthreads();
+    if (tid < kPanel) fk[tid] = tid < j ? F[k * kPanel + tid] : 0.0;
+    __syncthreads();
 
-    // Householder reflector for x = A[k:, k]
+    // One pass over rows [k, d_in) of column k and of the panel's earlier
+    // reflectors V[:, 0:j] (a row's j values loaded together): the column
+    // after those reflections, x[i] = a_k[i] - V[i, 0:j] fk, its squared
+    // norm, and dot[t] = sum_{i > k} V[i, t] x[i] for the aux vector.
     double* x = A + k * d_in;
     double s = 0.0;
-    for (int64_t i = k + tid; i < d_in; i += kBuildThreads) s += x[i] * x[i];
+    double dot[kPanel];
+#pragma unroll
+    for (int t = 0; t < kPanel; ++t) dot[t] = 0.0;
+    for (int64_t i = k + tid; i < d_in; i += kBuildThreads) {
+        double vrow[kPanel];
+#pragma unroll
+        for (int t = 0; t < kPanel; ++t) vrow[t] = t < j ? A[(k0 + t) * d_in + i] : 0.0;
+        double v = x[i];
+#pragma unroll
+        for (int t = 0; t < kPanel; ++t) v -= vrow[t] * fk[t];  // zero past j
+        x[i] = v;
+        s += v * v;
+        if (i > k) {
+#pragma unroll
+            for (int t = 0; t < kPanel; ++t) dot[t] += vrow[t] * v;
+        }
+    }
+    __shared__ double s_dot[kBuildThreads / kWave][kPanel + 1];
     s = wave_sum(s);
-    __syncthreads();
+#pragma unroll
+    for (int t = 0; t < kPanel; ++t) {
+        const double d = wave_sum(dot[t]);
+        if (lane == 0) s_dot[wave][t] = d;
+    }
     if (lane == 0) s_val[wave] = s;
     __syncthreads();
     if (tid == 0) {
         double t = 0.0;
         for (int w = 0; w < kBuildThreads / kWave; ++w) t += s_val[w];
         s_val[0] = t;
+    }
+    if (tid < j) {
+        double d = 0.0;
+        for (int w = 0; w < kBuildThreads / kWave; ++w) d += s_dot[w][tid];
+        s_dot[0][tid] = d;
     }
     __syncthreads();
     const double xnorm = sqrt(s_val[0]);
@@ -147,40 +203,81 @@ __global__ __launch_bounds__(kBuildThreads) void qr_pivot_reflect(double* __rest
             status[0] = 1;
             tau[k] = 0.0;
         }
+        if (tid < j) aux[tid] = 0.0;
         return;
     }
     const double beta = -copysign(xnorm, alpha);
+    const double tk = (beta - alpha) / beta;
     const double inv = 1.0 / (alpha - beta);
-    __syncthreads();
     for (int64_t i = k + 1 + tid; i < d_in; i += kBuildThreads) x[i] *= inv;
+    // aux[t] = -tau_k V[k:, t]^T v_k = -tau_k (V[k, t] + inv * dot[t]), v_k[k] = 1
+    if (tid < j) aux[tid] = -tk * (A[(k0 + tid) * d_in + k] + inv * s_dot[0][tid]);
+    __syncthreads();  // every thread read alpha = x[k] above
     if (tid == 0) {
         x[k] = beta;
-        tau[k] = (beta - alpha) / beta;
+        tau[k] = tk;
     }
 }
 
-// Step k, part 2: one wave per trailing column j > k.
-__global__ __launch_bounds__(256) void qr_apply(double* __restrict__ A, double* __restrict__ norm2,
-                                                const double* __restrict__ tau, int64_t k, int64_t d_out,
-                                                int64_t d_in) {
+// Step k = k0 + j, part 2: one wave per trailing column c > k, read only
+// except for three values per column:
+//   F[c, j]  = tau_k a_c^T v_k + F[c, 0:j] aux[0:j]  (a_c as of the panel start)
+//   R[k][c]  = a_c[k] - V[k, 0:j] F[c, 0:j]^T - F[c, j]   (written to a_c[k])
+//   norm2[c] -= R[k][c]^2
+__global__ __launch_bounds__(256) void qr_panel_gemv(double* __restrict__ A, double* __restrict__ norm2,
+                                                     double* __restrict__ F, const double* __restrict__ tau,
+                                                     const double* __restrict__ aux, int64_t k, int64_t k0,
+                                                     int64_t d_out, int64_t d_in) {
     const int lane = threadIdx.x & (kWave - 1);
-    const int64_t j = k + 1 + (int64_t)blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
-    if (j >= d_out) return;
+    const int64_t c = k + 1 + (int64_t)blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+    if (c >= d_out) return;
+    const int j = (int)(k - k0);
     const double* v = A + k * d_in;  // v[k] = 1 (implicit), v[k+1:] stored
-    double* a = A + j * d_in;
-    double w = 0.0;
-    for (int64_t i = k + 1 + lane; i < d_in; i += kWave) w += v[i] * a[i];
-    w = wave_sum(w) + a[k];
-    w *= tau[k];
-    if (lane == 0) a[k] -= w;
-    double s = 0.0;
-    for (int64_t i = k + 1 + lane; i < d_in; i += kWave) {
-        const double t = a[i] - w * v[i];
-        a[i] = t;
-        s += t * t;
+    double* a = A + c * d_in;
+    double d = 0.0, d2 = 0.0;
+    int64_t i = k + 1 + lane;
+    for (; i + kWave < d_in; i += 2 * kWave) {
+        d += v[i] * a[i];
+        d2 += v[i + kWave] * a[i + kWave];
     }
+    if (i < d_in) d += v[i] * a[i];
+    const double akc = a[k];
+    d = wave_sum(d + d2) + akc;
+    double* Fc = F + c * kPanel;
+    double corr = 0.0, row = 0.0;
+    if (lane < j) {
+        const double f = Fc[lane];
+        corr = f * aux[lane];
+        row = A[(k0 + lane) * d_in + k] * f;
+    }
+    corr = wave_sum(corr);
+    row = wave_sum(row);
+    if (lane == 0) {
+        const double f = tau[k] * d + corr;
+        Fc[j] = f;
+        const double rkc = akc - row - f;
+        a[k] = rkc;
+        norm2[c] = fmax(norm2[c] - rkc * rkc, 0.0);
+    }
+}
+
+// Exact residual norms ||A_c[k:]||^2 of columns c >= k (one wave per column).
+__global__ __launch_bounds__(256) void qr_norms(const double* __restrict__ A, double* __restrict__ norm2, int64_t k,
+                                                int64_t d_out, int64_t d_in) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t c = k + (int64_t)blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+    if (c >= d_out) return;
+    const double* a = A + c * d_in;
+    double s = 0.0;
+    for (int64_t i = k + lane; i < d_in; i += kWave) s += a[i] * a[i];
     s = wave_sum(s);
-    if (lane == 0) norm2[j] = s;
+    if (lane == 0) norm2[c] = s;
+}
+
+// diag[k] = R[k][k] = A_k[k] for k < r.
+__global__ void extract_diag(const double* __restrict__ A, double* __restrict__ diag, int64_t r, int64_t d_in) {
+    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < r; k += (int64_t)gridDim.x * blockDim.x)
+        diag[k] = A[k * d_in + k];
 }
 
 // R11 in row-major form: RT[s][t] = A_t[s] for s <= t < r, 0 below.

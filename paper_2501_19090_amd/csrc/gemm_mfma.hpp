@@ -204,7 +204,8 @@ __device__ __forceinline__ void staged_store(const f32x16 (&acc)[TM][TN], int64_
             }
         }
         __syncthreads();
-        for (int q = threadIdx.x; q < R * G; q += NT) {
+        const int RC = (BM - r0) < R ? (BM - r0) : R;  // rows of this chunk inside the tile
+        for (int q = threadIdx.x; q < RC * G; q += NT) {
             const int rr = q / G, g = q % G;
             const int64_t m = m0 + r0 + rr, n = n0 + 8 * g;
             if (m >= e.M || n >= e.N) continue;

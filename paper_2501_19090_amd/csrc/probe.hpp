@@ -42,27 +42,17 @@ __global__ __launch_bounds__(256) void mfma_probe(int64_t iters, float seed, flo
     }
 }
 
-// Streams `bytes` (a multiple of 16) of a buffer with 16-byte loads, four in
-// flight per thread, and stores one word per workgroup (the XOR of what it
-// read) so the loads are kept.
+// Streams `n16` 16-byte words of a buffer, one load per thread per step of a
+// grid-stride loop; a word is stored only if the XOR of what a thread read
+// equals a fixed constant (which keeps the loads; the benchmark's zero-filled
+// buffer never matches).
 __global__ __launch_bounds__(256) void hbm_read_probe(const u32x4* __restrict__ buf, int64_t n16, uint32_t* sink) {
     uint32_t x = 0;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    for (; i + 3 * stride < n16; i += 4 * stride) {
-        const u32x4 v0 = buf[i], v1 = buf[i + stride], v2 = buf[i + 2 * stride], v3 = buf[i + 3 * stride];
-        x ^= v0[0] ^ v0[1] ^ v0[2] ^ v0[3] ^ v1[0] ^ v1[1] ^ v1[2] ^ v1[3];
-        x ^= v2[0] ^ v2[1] ^ v2[2] ^ v2[3] ^ v3[0] ^ v3[1] ^ v3[2] ^ v3[3];
-    }
-    for (; i < n16; i += stride) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += (int64_t)gridDim.x * blockDim.x) {
         const u32x4 v = buf[i];
         x ^= v[0] ^ v[1] ^ v[2] ^ v[3];
     }
-    __shared__ uint32_t red[4];
-    for (int o = 32; o > 0; o >>= 1) x ^= __shfl_xor(x, o);
-    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = x;
-    __syncthreads();
-    if (threadIdx.x == 0) sink[blockIdx.x] = red[0] ^ red[1] ^ red[2] ^ red[3];
+    if (x == 0x9E3779B9u) sink[blockIdx.x] = x;
 }
 
 }  // namespace pifa

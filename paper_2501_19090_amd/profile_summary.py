@@ -5,6 +5,7 @@
            <launch-name> <out.txt> <command...>
     python -m paper_2501_19090_amd.profile_summary steady <kernel_trace.csv> <N> <out.md> <kernel-substring>...
     python -m paper_2501_19090_amd.profile_summary counters <out.md> <title> <command> <dir> <kernel-substring>...
+    python -m paper_2501_19090_amd.profile_summary fullbench <bench_full.json> <out.md> <command...>
 
 `stats` turns a --kernel-trace --stats CSV into a short markdown table.
 `counters` appends to <out.md> a table of every counter a --pmc pass in <dir>
@@ -13,6 +14,10 @@ given substring.
 `steady` appends to <out.md> the average duration of the last N dispatches
 of each kernel whose name contains a given substring (the timed steps that
 follow the warm-up, as bench.py times them).
+`fullbench` turns the JSON report of `bench.py --full` into a markdown table
+(every configuration and batch size: PIFA, low-rank U V and dense times,
+speedups, TFLOP/s, GB/s and fractions of peak) with the source digest of the
+kernels it was measured on.
 `traffic` reads two --pmc passes (FETCH_SIZE, then WRITE_SIZE; KiB per
 dispatch), takes the average for the kernel whose name contains
 <kernel-substring>, and scales it by what the same counters read for the
@@ -54,7 +59,8 @@ def stats(csv_path: str, out_md: str, command: str) -> None:
 
 def steady(trace_csv: str, n: int, out_md: str, subs) -> None:
     rows = list(csv.DictReader(open(trace_csv)))
-    lines = ["", "Steady state: average of the last %d dispatches of each kernel (after the warm-up):" % n, "",
+    lines = ["", "Steady state: average of the last %d dispatches of each kernel (after the warm-up); forward "
+             "kernel digest `%s`:" % (n, build.forward_kernel_digest()), "",
              "| kernel | dispatches averaged | avg us |", "|---|---:|---:|"]
     for sub in subs:
         d = [(int(r["Start_Timestamp"]), int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
@@ -141,7 +147,8 @@ def traffic(fetch_dir, write_dir, kernel_sub, launch_name, out_txt, command):
         "dispatches": {"fetch": nf, "write": nw},
         "fetch_kib_raw": k_fetch, "write_kib_raw": k_write,
         "copy_bytes": COPY_BYTES, "copy_fetch_kib_raw": c_fetch, "copy_write_kib_raw": c_write,
-        "source_digest": build.source_digest(), "command": command,
+        "source_digest": build.source_digest(), "forward_kernel_digest": build.forward_kernel_digest(),
+        "command": command,
     }
     if None not in (k_fetch, k_write, c_fetch, c_write):
         f_scale = COPY_BYTES / (c_fetch * 1024.0)
@@ -156,6 +163,28 @@ def traffic(fetch_dir, write_dir, kernel_sub, launch_name, out_txt, command):
     print(json.dumps(rec, indent=1))
 
 
+def fullbench(json_path: str, out_md: str, command: str) -> None:
+    rows = json.load(open(json_path))
+    lines = ["# Every configuration: PIFA against the same-engine low-rank and dense layers", "",
+             "Command (run from the repository root on the GPU host):", "", "```", command, "```", "",
+             "Kernel source digest: `%s`.  Times are microseconds per forward: M <= 128 rows replay "
+             "HIP graphs over weight copies rotated past the 256 MB Infinity Cache; larger M are eager "
+             "launches after warm-up on the same copy.  x U V and x dense are the time ratios "
+             "(above 1: PIFA faster).  TFLOP/s uses PIFA's 2 M r (d_in + d_out - r) FLOPs, GB/s its "
+             "weights, indices, X and Y; fractions are of 2516.6 TFLOP/s and 8000 GB/s."
+             % rows[0].get("source_digest", build.source_digest()), "",
+             "| config | d_in -> d_out, r | M | PIFA us | U V us | dense us | x U V | x dense | TFLOP/s | "
+             "frac MFMA | GB/s | frac HBM |",
+             "|---|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
+    for r in rows:
+        lines.append("| %s | %d -> %d, %d | %d | %.1f | %.1f | %.1f | %.2f | %.2f | %.0f | %.3f | %.0f | %.3f |" % (
+            r["config"], r["d_in"], r["d_out"], r["r"], r["M"], r["pifa_us"], r["uv_us"], r["dense_us"],
+            r["speedup_vs_uv"], r["speedup_vs_dense"], r["pifa_tflops"], r["pifa_tflops"] / 2516.5824,
+            r["pifa_gbps"], r["pifa_gbps"] / 8000.0))
+    with open(out_md, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
 if __name__ == "__main__":
     mode = sys.argv[1]
     if mode == "stats":
@@ -164,6 +193,8 @@ if __name__ == "__main__":
         counters(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5], sys.argv[6:])
     elif mode == "steady":
         steady(sys.argv[2], int(sys.argv[3]), sys.argv[4], sys.argv[5:])
+    elif mode == "fullbench":
+        fullbench(sys.argv[2], sys.argv[3], " ".join(sys.argv[4:]))
     elif mode == "traffic":
         traffic(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5], sys.argv[6], " ".join(sys.argv[7:]))
     else:

@@ -29,9 +29,12 @@ def test_traffic_only_for_matching_sources(monkeypatch):
     path = os.path.join(ROOT, "profiles", "pifa_gemm1_xwp_attn4096_M4096_traffic.txt")
     with open(path) as f:
         rec = json.load(f)
-    monkeypatch.setattr(build, "source_digest", lambda: rec["source_digest"])
-    assert bench.traffic_from_profiles("pifa_gemm1_xwp") == rec["hbm_bytes_per_launch"]
-    monkeypatch.setattr(build, "source_digest", lambda: "0" * 16)
+    if "forward_kernel_digest" in rec:
+        monkeypatch.setattr(build, "forward_kernel_digest", lambda: rec["forward_kernel_digest"])
+        assert bench.traffic_from_profiles("pifa_gemm1_xwp") == rec["hbm_bytes_per_launch"]
+    else:  # a record that does not name the kernels' version is never used
+        assert bench.traffic_from_profiles("pifa_gemm1_xwp") is None
+    monkeypatch.setattr(build, "forward_kernel_digest", lambda: "0" * 16)
     assert bench.traffic_from_profiles("pifa_gemm1_xwp") is None
     assert bench.traffic_from_profiles("no_such_kernel") is None
 
