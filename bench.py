@@ -331,7 +331,7 @@ def measure_group(seed):
     return out
 
 
-def measure_backward(wl: Workload, M: int, iters: int = 10, warmup: int = 3):
+def measure_backward(wl: Workload, M: int, iters: int = 20, warmup: int = 30):
     """pifa_layer_backward at M rows: dX, dW_p and dC from X, the forward's Y
     and a random dY.  Useful FLOPs are twice the forward's (Sec. 3.3 cost for
     each of the two transposed products)."""
@@ -546,10 +546,13 @@ def main():
 
     if args.profile_run and args.profile_path == "forward" and args.profile_config != "B_attn_4096":
         cfg, lay, d_in, d_out, r, _, _, _ = inputs.CONFIGS[args.profile_config]
+        log("profile run: forming the %s layer" % args.profile_config)
         wl = Workload(d_in, d_out, r, inputs.config_seed(cfg, lay))
+        log("profile run: %s built on the GPU in %.0f ms" % (args.profile_config, wl.build_ms))
         M = args.profile_m
         wl.ensure_copies()
         wl.reserve(M)
+        log("profile run: %d weight copies ready" % len(wl.pifa_h))
         stream = torch.cuda.current_stream().cuda_stream
         x = torch.from_numpy(inputs.round_bf16(inputs.activations(M, d_in, 99))[0].view(np.int16)).cuda().view(
             torch.bfloat16)
