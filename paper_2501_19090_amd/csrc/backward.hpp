@@ -169,6 +169,9 @@ __global__ void zero_cols(bf16* __restrict__ p, int64_t rows, int64_t ld, int64_
 //   * writes bf16(G_p) transposed to gpt[j * ldt + m] for j < r (the A
 //     operand of dW_p = G_p^T X).
 struct GradPivotEpi {
+    // in a whole tile, gp is stored element-wise (store4_rows) and the
+    // transposed bf16 copy goes through LDS as 16-byte row pieces of gpt
+    static constexpr bool kTransposedPart = true;
     const bf16* G;
     int64_t ldg;
     const int32_t* piv;
@@ -200,6 +203,14 @@ struct GradPivotEpi {
         const float g = c.piv_ok ? v : 0.f;
         gp[m * r_pad + c.n] = g;
         if (c.piv_ok) reinterpret_cast<uint16_t*>(gpt)[c.n * ldt + m] = f32_to_bf16_bits(g);
+    }
+    // rows m .. m + 3 (m % 4 == 0) of column c, fp32 rows only (the
+    // transposed copy is written by the tile's staged transposed store)
+    __device__ __forceinline__ void store4_rows(int64_t m, const Col& c, const float (&v)[4]) const {
+        if (c.n >= r_pad || m >= M) return;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            if (m + e < M) gp[(m + e) * r_pad + c.n] = c.piv_ok ? v[e] : 0.f;
     }
     // rows m .. m + 3 (m % 4 == 0) of column c: the transposed copy is one
     // 8-byte store (ldt % 8 == 0)

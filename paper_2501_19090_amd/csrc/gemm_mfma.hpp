@@ -73,6 +73,17 @@ struct StagedEpiT<E, std::void_t<decltype(E::kStaged)>> {
     static constexpr bool value = true;
 };
 
+// An epilogue with kTransposedPart stores its rows element-wise
+// (store4_rows) and a bf16 transposed copy (gpt, ldt, r, M) through LDS.
+template <typename E, typename = void>
+struct TransposedPartEpiT {
+    static constexpr bool value = false;
+};
+template <typename E>
+struct TransposedPartEpiT<E, std::void_t<decltype(E::kTransposedPart)>> {
+    static constexpr bool value = true;
+};
+
 // An epilogue with kDual has a per-element part (y) and a staged part (ws).
 template <typename E, typename = void>
 struct DualEpiT {
@@ -220,6 +231,49 @@ __device__ __forceinline__ void staged_store(const f32x16 (&acc)[TM][TN], int64_
         }
     }
     if (over && e.overflow) atomicAdd(e.overflow, over);
+}
+
+// Store tile (m0, n0) transposed as bf16: out[n * ldt + m] = acc(m, n) for
+// n < nrows, m < ldt (zero for m >= M).  Chunks of C tile columns are written
+// to LDS as rows of BM values (pitch BM + 8), then stored 8 values of m per
+// 16-byte store (ldt a multiple of 8, out 16-byte aligned).
+template <int BM, int BN, int WM, int WN, int TM, int TN>
+__device__ __forceinline__ void staged_store_t(const f32x16 (&acc)[TM][TN], int64_t m0, int64_t n0, uint16_t* out,
+                                               int64_t ldt, int64_t nrows, int64_t M, char* smem, int lds_bytes) {
+    constexpr int NT = WM * WN * kWave;
+    constexpr int WTM = BM / WM, WTN = BN / WN;
+    constexpr int PT = BM + 8;  // LDS row pitch in elements
+    constexpr int G = BM / 8;   // 16-byte groups per row
+    const int C = (lds_bytes / (2 * PT)) < BN ? (lds_bytes / (2 * PT)) : BN;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const int wm = wave / WN, wn = wave % WN;
+    uint16_t* tile = reinterpret_cast<uint16_t*>(smem);
+    for (int c0 = 0; c0 < BN && n0 + c0 < nrows; c0 += C) {
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int nl = wn * WTN + j * 32 + (lane & 31) - c0;
+                if ((unsigned)nl < (unsigned)C) {
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) {
+                        const int ml = wm * WTM + i * 32 + 4 * (lane >> 5) + 8 * (v >> 2) + (v & 3);
+                        tile[nl * PT + ml] = m0 + ml < M ? f32_to_bf16_bits(acc[i][j][v]) : (uint16_t)0;
+                    }
+                }
+            }
+        }
+        __syncthreads();
+        const int CC = (BN - c0) < C ? (BN - c0) : C;  // tile columns of this chunk
+        for (int q = threadIdx.x; q < CC * G; q += NT) {
+            const int nn = q / G, g = q % G;
+            const int64_t n = n0 + c0 + nn, m = m0 + 8 * g;
+            if (n >= nrows || m >= ldt) continue;
+            *reinterpret_cast<u32x4*>(out + n * ldt + m) = *reinterpret_cast<const u32x4*>(tile + nn * PT + 8 * g);
+        }
+    }
 }
 
 // One output tile (tm, tn) over the K range [kbeg, kend); both operands are
@@ -394,6 +448,24 @@ __device__ __forceinline__ void gemm_nt_tile(const T* __restrict__ A, int64_t ld
 
     if constexpr (StagedEpiT<Epi>::value) {
         staged_store<BM, BN, WM, WN, TM, TN>(acc, m0, n0, epi, smem, LDS_BYTES);
+        return;
+    } else if constexpr (TransposedPartEpiT<Epi>::value) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const auto c = epi.col(n0 + wn * WTN + j * 32 + (lane & 31));
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                const int64_t mb = m0 + wm * WTM + i * 32 + 4 * (lane >> 5);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const float v4[4] = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                                         acc[i][j][4 * q + 3]};
+                    epi.store4_rows(mb + 8 * q, c, v4);
+                }
+            }
+        }
+        staged_store_t<BM, BN, WM, WN, TM, TN>(acc, m0, n0, reinterpret_cast<uint16_t*>(epi.gpt), epi.ldt, epi.r,
+                                               epi.M, smem, LDS_BYTES);
         return;
     } else if constexpr (DualEpiT<Epi>::value) {
 #pragma unroll
