@@ -273,6 +273,18 @@ GemmPlan gemm_plan(int64_t M, int64_t N, int64_t K, bool wide_ok, bool can_split
     if (cfg == kTile256x256) return {256, 256, {1, K}};
     if (cfg == kTile256x192) return {256, 192, {1, K}};
     if (cfg == kTile256x128) return {256, 128, {1, K}};
+    // at most 128 rows: split K over 64 x 64 tiles (4 waves), half the rows of
+    // the smallest 8-wave tile, so no tile computes masked rows at M <= 64 and
+    // twice the tiles need half the splits at M = 128, as long as each split
+    // stays at most 1024 deep (one wave per SIMD cannot hide a longer loop:
+    // the dense 4096^2 layer at M = 128 took 17.0 us with 2048-deep splits
+    // against 15.1 us on 128 x 64 tiles).  Attention layer, HIP-graph replay:
+    // PIFA M = 17 19.5 -> 18.0 us, M = 128 29.3 -> 26.5 us; dense M = 17-64
+    // 12.4-13.2 -> 11.0-12.1 us.
+    if (M <= 128 && can_split) {
+        const SplitPlan p = split_plan(ceil_div(M, 64) * ceil_div(N, 64), M, N, K);
+        if (p.splits > 1 && p.k_split <= 1024) return {64, 64, p};
+    }
     // too few tiles for the chip even at 128 x 128: split K, or, when that
     // does not pay and 128 x 128 tiles keep at most half the chip busy, take
     // 128 x 64 tiles if they fill it in one round (the rank sweep's 410-wide
@@ -327,7 +339,10 @@ hipError_t launch_gemm(int site, const T* A, int64_t lda, int64_t M, const T* B,
     } else {
         SplitEpi se{partials, M, N};
         const dim3 sgrid(grid.x, (unsigned)g.split.splits);
-        if (g.bn == 64)
+        if (g.bm == 64)
+            hipLaunchKernelGGL((gemm_nt_mfma<T, 64, 64, kGemmBK, 2, 2, BPACK, 2, SplitEpi>), sgrid,
+                               dim3(4 * kWave), 0, st, A, lda, M, B, ldb, N, K, g.split.k_split, se);
+        else if (g.bn == 64)
             hipLaunchKernelGGL((gemm_nt_mfma<T, 128, 64, kGemmBK, 4, 2, BPACK, 2, SplitEpi>), sgrid,
                                dim3(8 * kWave), 0, st, A, lda, M, B, ldb, N, K, g.split.k_split, se);
         else

@@ -179,15 +179,22 @@ def test_gemm_plan_of_measured_shapes(shape, wide, plan):
 
 
 def test_gemm_plan_splits_small_batches():
-    """Few rows: K is split over 128 x 64 tiles (half the splits 128 x 128
-    tiles would need for as many workgroups), with at most 16 splits and
-    partials no larger than the operands."""
+    """Few rows: K is split, over 64 x 64 tiles up to 128 rows and over
+    128 x 64 tiles above (half the splits 128 x 128 tiles would need for as
+    many workgroups), with at most 16 splits and partials no larger than the
+    operands."""
     for M in (17, 64, 128, 256):
         tm, tn, s = pifa.pifa_gemm_plan(M, 2048, 4096)
-        assert (tm, tn) == (128, 64) and 1 < s <= 16
+        assert (tm, tn) == ((64, 64) if M <= 128 else (128, 64)) and 1 < s <= 16
         assert s * M * 2048 * 4 <= (M + 2048) * 4096 * 2
-        assert ((M + 127) // 128) * (2048 // 64) * s <= 512
-    assert pifa.pifa_gemm_plan(128, 2048, 4096) == (128, 64, 8)
+        assert -(-M // tm) * (2048 // tn) * s <= 512
+    assert pifa.pifa_gemm_plan(32, 2048, 4096) == (64, 64, 8)
+    assert pifa.pifa_gemm_plan(128, 2048, 4096) == (64, 64, 4)
+    assert pifa.pifa_gemm_plan(128, 2048, 2048) == (64, 64, 4)
     assert pifa.pifa_gemm_plan(256, 2048, 4096) == (128, 64, 4)
+    # 64 x 64 tiles only while a split stays at most 1024 deep: the dense
+    # 4096^2 product at M = 128 keeps 128 x 64 tiles
+    assert pifa.pifa_gemm_plan(128, 4096, 4096) == (128, 64, 4)
+    assert pifa.pifa_gemm_plan(64, 4096, 4096) == (64, 64, 4)
     with pytest.raises(pifa.PifaError):
         pifa.pifa_gemm_plan(0, 2048, 4096)
