@@ -1436,10 +1436,6 @@ pifa_status pifa_layer_backward(pifa_handle h, const void* X, const void* Y, con
 
 }  // extern "C"
 
-extern "C" {
-
-}  // extern "C"
-
 // ===================================================================== reconstruction
 struct pifa_calib {
     int device = 0;
