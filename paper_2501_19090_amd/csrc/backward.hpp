@@ -7,10 +7,11 @@
 //   dX   = G_p W_p                    (M x d_in)
 //   dW_p = G_p^T X                    (r x d_in)
 //   dC   = G[:, I^c]^T Y_p            (n_np x r)
-// All four are products for the prefill GEMM (gemm_mfma.hpp), which wants
-// both operands K-contiguous; this file holds the data movement that puts
-// them in that form (gathers, tiled transposes, transposed weight packs) and
-// the epilogue of the G_p product.
+// All four are products for the prefill GEMM (gemm_mfma.hpp).  G_p and dX
+// take K-contiguous operands; dW_p and dC reduce over the activation rows
+// and read their operands K-major (rows of G_p, X, G[:, I^c], Y[:, I]).  This
+// file holds the gathers of G[:, I^c] and Y[:, I] as rows, the transposed
+// weight packs and the epilogue of the G_p product.
 //
 // Precision: G_p multiplies W_p in dX = G_p W_p with the same cancellation as
 // Y_p C^T in the forward (C rebuilds W_np from W_p): a bf16 G_p misses the
@@ -153,32 +154,23 @@ __global__ __launch_bounds__(256) void gather_tile(const bf16* __restrict__ in, 
     }
 }
 
-// Zero columns [c0, ld) of a rows x ld bf16 matrix.
-__global__ void zero_cols(bf16* __restrict__ p, int64_t rows, int64_t ld, int64_t c0) {
-    uint16_t* q = reinterpret_cast<uint16_t*>(p);
-    const int64_t w = ld - c0, total = rows * w;
-    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
-         e += (int64_t)gridDim.x * blockDim.x)
-        q[(e / w) * ld + c0 + e % w] = 0;
-}
-
-// Epilogue of G_p = G[:, I^c] C (+ G[:, I]): acc(m, j) for j < r_pad.
-//   * the accumulator starts from G[m, piv[j]] for j < r (init);
-//   * writes G_p in fp32 to gp[m * r_pad + j] (padding columns j >= r get
+// Epilogue of G_p = G[:, I^c] C (+ G[:, I]): acc(m, n) for n < r_pad.
+//   * the accumulator starts from G[m, piv[n]] for n < r (init);
+//   * writes G_p in fp32 to gp[m * r_pad + n] (padding columns n >= r get
 //     zeros), for the row-wise fp16 conversion;
-//   * writes bf16(G_p) transposed to gpt[j * ldt + m] for j < r (the A
-//     operand of dW_p = G_p^T X).
+//   * writes bf16(G_p) to gpb[m * r_pad + n] (zeros at n >= r): the K-major
+//     A operand of dW_p = G_p^T X.
+// In a whole tile the fp32 rows go out element by element (store4_rows) and
+// the bf16 rows through the staged 16-byte epilogue (staged()); the K-split
+// reduction uses store().
 struct GradPivotEpi {
-    // in a whole tile, gp is stored element-wise (store4_rows) and the
-    // transposed bf16 copy goes through LDS as 16-byte row pieces of gpt
-    static constexpr bool kTransposedPart = true;
+    static constexpr bool kRowsPlusStaged = true;
     const bf16* G;
     int64_t ldg;
     const int32_t* piv;
     int64_t r, r_pad;
     float* gp;
-    bf16* gpt;
-    int64_t ldt;
+    bf16* gpb;
     int64_t M;
 
     struct Col {
@@ -202,38 +194,19 @@ struct GradPivotEpi {
         if (m >= M || c.n >= r_pad) return;
         const float g = c.piv_ok ? v : 0.f;
         gp[m * r_pad + c.n] = g;
-        if (c.piv_ok) reinterpret_cast<uint16_t*>(gpt)[c.n * ldt + m] = f32_to_bf16_bits(g);
+        reinterpret_cast<uint16_t*>(gpb)[m * r_pad + c.n] = f32_to_bf16_bits(g);
     }
-    // rows m .. m + 3 (m % 4 == 0) of column c, fp32 rows only (the
-    // transposed copy is written by the tile's staged transposed store)
+    // rows m .. m + 3 (m % 4 == 0) of column c, fp32 rows only
     __device__ __forceinline__ void store4_rows(int64_t m, const Col& c, const float (&v)[4]) const {
         if (c.n >= r_pad || m >= M) return;
 #pragma unroll
         for (int e = 0; e < 4; ++e)
             if (m + e < M) gp[(m + e) * r_pad + c.n] = c.piv_ok ? v[e] : 0.f;
     }
-    // rows m .. m + 3 (m % 4 == 0) of column c: the transposed copy is one
-    // 8-byte store (ldt % 8 == 0)
-    __device__ __forceinline__ void store4(int64_t m, const Col& c, const float (&v)[4]) const {
-        if (c.n >= r_pad || m >= M) return;
-        uint16_t h[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const bool ok = m + e < M;
-            const float g = (c.piv_ok && ok) ? v[e] : 0.f;
-            if (ok) gp[(m + e) * r_pad + c.n] = g;
-            h[e] = f32_to_bf16_bits(g);
-        }
-        if (c.piv_ok) {
-            uint16_t* dst = reinterpret_cast<uint16_t*>(gpt) + c.n * ldt + m;
-            if (m + 4 <= M) {
-                *reinterpret_cast<uint64_t*>(dst) = __builtin_bit_cast(uint64_t, h);
-            } else {
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    if (m + e < M) dst[e] = h[e];
-            }
-        }
+    // the bf16 rows (the tile's padding columns n >= r hold zero products:
+    // C^T's padding rows and their starting values are zero)
+    __device__ __forceinline__ StagedEpi<bf16> staged() const {
+        return StagedEpi<bf16>{reinterpret_cast<uint16_t*>(gpb), r_pad, r_pad, 1.f, nullptr, M};
     }
 };
 

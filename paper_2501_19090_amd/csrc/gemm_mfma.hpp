@@ -17,6 +17,16 @@
 // masked lane is given an offset past the range), so any M, N and any K that
 // is a multiple of 8 work.  B is either
 // row-major (row stride ldb) or in the lane order of layout.hpp (BPACK).
+//
+// K-major operands (KM bit 0: A, bit 1: B) are stored K x M (K x N) with
+// row stride lda >= M rounded up to 8 (ldb likewise, 16-byte aligned rows):
+// the transposed products of the backward pass, whose
+// reduction runs over the activation rows.  Their tiles go to LDS as they
+// are loaded (BK rows of the tile's M or N extent) and the MFMA fragments
+// are read back with the transposing LDS read of gfx950 (ds_read_b64_tr_b16):
+// within each group of 16 lanes, lane R reads 4 elements of K row R / 4 at
+// column 4 (R % 4), and lane L receives the 4 elements of column L from those
+// 4 rows, so two such reads give a lane the 8 consecutive K values of its row.
 #pragma once
 
 #include <type_traits>
@@ -73,14 +83,14 @@ struct StagedEpiT<E, std::void_t<decltype(E::kStaged)>> {
     static constexpr bool value = true;
 };
 
-// An epilogue with kTransposedPart stores its rows element-wise
-// (store4_rows) and a bf16 transposed copy (gpt, ldt, r, M) through LDS.
+// An epilogue with kRowsPlusStaged stores one output element-wise
+// (store4_rows) and a second, contiguous one through LDS (staged()).
 template <typename E, typename = void>
-struct TransposedPartEpiT {
+struct RowsPlusStagedEpiT {
     static constexpr bool value = false;
 };
 template <typename E>
-struct TransposedPartEpiT<E, std::void_t<decltype(E::kTransposedPart)>> {
+struct RowsPlusStagedEpiT<E, std::void_t<decltype(E::kRowsPlusStaged)>> {
     static constexpr bool value = true;
 };
 
@@ -96,9 +106,32 @@ struct DualEpiT<E, std::void_t<decltype(E::kDual)>> {
 
 // LDS bytes of a BM x BN tile of T with K step BK: the double-buffered
 // operand tiles (the staged epilogues reuse them after the K loop).
-template <typename T, int BM, int BN, int BK>
+// A K-major tile is stored as BK rows of BM (BN) elements with a pitch of
+// BM + 32 (BN + 32): the 16 lanes of a transposing read cover 4 rows x 32
+// bytes, and that pitch puts the 4 rows on disjoint bank groups.
+template <int BM, int BK, bool KMAJ>
+constexpr int tile_elems() {
+    return KMAJ ? BK * (BM + 32) : BM * (BK + 8);
+}
+template <typename T, int BM, int BN, int BK, int KM = 0>
 constexpr int gemm_lds_bytes() {
-    return 2 * (BM + BN) * (BK + 8) * (int)sizeof(T);
+    return 2 * (tile_elems<BM, BK, (KM & 1) != 0>() + tile_elems<BN, BK, (KM & 2) != 0>()) * (int)sizeof(T);
+}
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+
+// 8 consecutive K values (k0 .. k0 + 7) of row r0 + lane % 32 of a K-major LDS
+// tile with pitch P (elements), for the 32x32x16 operand layout: lane l
+// holds row l % 32, K values 8 (l / 32) .. + 7 of the 16-deep step at k0.
+template <typename T, int P>
+__device__ __forceinline__ u32x4 frag_kmajor(const T* tile, int k0, int r0, int lane) {
+    const int g = lane >> 4, R = lane & 15;
+    const T* p = tile + (k0 + 8 * (g >> 1) + (R >> 2)) * P + r0 + 16 * (g & 1) + 4 * (R & 3);
+    typedef __attribute__((address_space(3))) v4i16 lds_v4;
+    const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4*)p);
+    const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4*)(p + 4 * P));
+    const uint2 a = __builtin_bit_cast(uint2, lo), b = __builtin_bit_cast(uint2, hi);
+    return u32x4{a.x, a.y, b.x, b.y};
 }
 
 template <typename T>
@@ -233,52 +266,9 @@ __device__ __forceinline__ void staged_store(const f32x16 (&acc)[TM][TN], int64_
     if (over && e.overflow) atomicAdd(e.overflow, over);
 }
 
-// Store tile (m0, n0) transposed as bf16: out[n * ldt + m] = acc(m, n) for
-// n < nrows, m < ldt (zero for m >= M).  Chunks of C tile columns are written
-// to LDS as rows of BM values (pitch BM + 8), then stored 8 values of m per
-// 16-byte store (ldt a multiple of 8, out 16-byte aligned).
-template <int BM, int BN, int WM, int WN, int TM, int TN>
-__device__ __forceinline__ void staged_store_t(const f32x16 (&acc)[TM][TN], int64_t m0, int64_t n0, uint16_t* out,
-                                               int64_t ldt, int64_t nrows, int64_t M, char* smem, int lds_bytes) {
-    constexpr int NT = WM * WN * kWave;
-    constexpr int WTM = BM / WM, WTN = BN / WN;
-    constexpr int PT = BM + 8;  // LDS row pitch in elements
-    constexpr int G = BM / 8;   // 16-byte groups per row
-    const int C = (lds_bytes / (2 * PT)) < BN ? (lds_bytes / (2 * PT)) : BN;
-    const int lane = threadIdx.x & (kWave - 1);
-    const int wave = threadIdx.x / kWave;
-    const int wm = wave / WN, wn = wave % WN;
-    uint16_t* tile = reinterpret_cast<uint16_t*>(smem);
-    for (int c0 = 0; c0 < BN && n0 + c0 < nrows; c0 += C) {
-        __syncthreads();
-#pragma unroll
-        for (int i = 0; i < TM; ++i) {
-#pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                const int nl = wn * WTN + j * 32 + (lane & 31) - c0;
-                if ((unsigned)nl < (unsigned)C) {
-#pragma unroll
-                    for (int v = 0; v < 16; ++v) {
-                        const int ml = wm * WTM + i * 32 + 4 * (lane >> 5) + 8 * (v >> 2) + (v & 3);
-                        tile[nl * PT + ml] = m0 + ml < M ? f32_to_bf16_bits(acc[i][j][v]) : (uint16_t)0;
-                    }
-                }
-            }
-        }
-        __syncthreads();
-        const int CC = (BN - c0) < C ? (BN - c0) : C;  // tile columns of this chunk
-        for (int q = threadIdx.x; q < CC * G; q += NT) {
-            const int nn = q / G, g = q % G;
-            const int64_t n = n0 + c0 + nn, m = m0 + 8 * g;
-            if (n >= nrows || m >= ldt) continue;
-            *reinterpret_cast<u32x4*>(out + n * ldt + m) = *reinterpret_cast<const u32x4*>(tile + nn * PT + 8 * g);
-        }
-    }
-}
-
 // One output tile (tm, tn) over the K range [kbeg, kend); both operands are
 // masked outside that range.
-template <typename T, int BM, int BN, int BK, int WM, int WN, bool BPACK, int PGR, typename Epi>
+template <typename T, int BM, int BN, int BK, int WM, int WN, bool BPACK, int PGR, typename Epi, int KM = 0>
 __device__ __forceinline__ void gemm_nt_tile(const T* __restrict__ A, int64_t lda, int64_t M,
                                              const T* __restrict__ B, int64_t ldb, int64_t N, int64_t K,
                                              int64_t kbeg, int64_t kend, int64_t tm, int64_t tn,
@@ -297,21 +287,31 @@ __device__ __forceinline__ void gemm_nt_tile(const T* __restrict__ A, int64_t ld
     static_assert(WTM % 32 == 0 && WTN % 32 == 0 && KK >= 2, "bad warp tile");
     static_assert(!BPACK || ((BK == 64 || BK == 128) && BN % kPackRows == 0), "bad packed tile");
     static_assert(PGR >= 1 && PGR <= 4, "prefetch depth");
+    constexpr bool AKM = (KM & 1) != 0, BKM = (KM & 2) != 0;
+    static_assert(!(BPACK && BKM), "a packed B is K-contiguous");
+    constexpr int PMA = BM + 32, PMB = BN + 32;  // K-major tile pitches
+    constexpr int AEL = tile_elems<BM, BK, AKM>(), BEL = tile_elems<BN, BK, BKM>();
 
-    constexpr int LDS_BYTES = gemm_lds_bytes<T, BM, BN, BK>();
+    constexpr int LDS_BYTES = gemm_lds_bytes<T, BM, BN, BK, KM>();
     __shared__ __attribute__((aligned(16))) char smem[LDS_BYTES];
-    T(*As)[BM * LDK] = reinterpret_cast<T(*)[BM * LDK]>(smem);
-    T(*Bs)[BN * LDK] = reinterpret_cast<T(*)[BN * LDK]>(smem + 2 * BM * LDK * sizeof(T));
+    T(*As)[AEL] = reinterpret_cast<T(*)[AEL]>(smem);
+    T(*Bs)[BEL] = reinterpret_cast<T(*)[BEL]>(smem + 2 * AEL * sizeof(T));
 
     const int64_t m0 = tm * BM, n0 = tn * BN;
     if constexpr (SkipEpi<Epi>::value) {
         if (epi.skip_tile(m0, n0, BM, BN)) return;
     }
 
-    const auto ars = make_rsrc31(A + m0 * lda, ((M - m0 - 1) * lda + K) * (int64_t)sizeof(T));
+    // K-major: element (k, m) at k * lda + m, with lda >= M rounded up to 8
+    // (the last row's final chunk lies inside the row pitch, so it is read
+    // whole: a range ending mid-chunk would zero the chunk's valid elements);
+    // elements at m >= M only feed output rows >= M, which are not stored
+    const auto ars = AKM ? make_rsrc31(A + m0, ((K - 1) * lda + round_up(M - m0, (int64_t)8)) * (int64_t)sizeof(T))
+                         : make_rsrc31(A + m0 * lda, ((M - m0 - 1) * lda + K) * (int64_t)sizeof(T));
     const int64_t KB = packed_kblocks(K);
     const auto brs = BPACK ? make_rsrc31(B + (n0 / kPackRows) * KB * (kPackChunks * 8),
                                          (packed_groups(N) - n0 / kPackRows) * KB * kPackChunks * 16)
+                     : BKM ? make_rsrc31(B + n0, ((K - 1) * ldb + round_up(N - n0, (int64_t)8)) * (int64_t)sizeof(T))
                            : make_rsrc31(B + n0 * ldb, ((N - n0 - 1) * ldb + K) * (int64_t)sizeof(T));
 
     const int tid = threadIdx.x;
@@ -327,11 +327,31 @@ __device__ __forceinline__ void gemm_nt_tile(const T* __restrict__ A, int64_t ld
     auto gload = [&](int64_t k0, Stage& R) {
 #pragma unroll
         for (int i = 0; i < A_CH; ++i) {
-            const int c = tid + i * NT, row = c / CPR;
-            const int64_t k = k0 + (c % CPR) * 8;
-            R.a[i] = load16(ars, k < kend ? (uint32_t)((row * lda + k) * (int64_t)sizeof(T)) : kMaskedOffset);
+            const int c = tid + i * NT;
+            if constexpr (AKM) {  // chunk: 8 consecutive rows m of K row k
+                // rows k >= kend get bit 31 (past every range) without a
+                // select: the per-chunk row makes the mask lane-dependent
+                const int64_t k = k0 + c / (BM / 8);
+                const int mc = c % (BM / 8);
+                const uint32_t off = (uint32_t)((k * lda + 8 * mc) * (int64_t)sizeof(T));
+                R.a[i] = load16(ars, off | ((uint32_t)(k >= kend) << 31));
+            } else {
+                const int row = c / CPR;
+                const int64_t k = k0 + (c % CPR) * 8;
+                R.a[i] = load16(ars, k < kend ? (uint32_t)((row * lda + k) * (int64_t)sizeof(T)) : kMaskedOffset);
+            }
         }
-        if constexpr (BPACK) {
+        if constexpr (BKM) {
+#pragma unroll
+            for (int i = 0; i < B_CH; ++i) {
+                const int c = tid + i * NT;
+                const int kr = c / (BN / 8), nc = c % (BN / 8);
+                const int64_t k = k0 + kr;
+                const uint32_t off = (uint32_t)((k * ldb + 8 * nc) * (int64_t)sizeof(T));
+                R.b[i] = load16(brs, off | ((uint32_t)(k >= kend) << 31));
+                R.blds[i] = kr * PMB + 8 * nc;
+            }
+        } else if constexpr (BPACK) {
             const int64_t blk = k0 / kPackCols;
             const int hsel = (int)((k0 % kPackCols) / BK);
 #pragma unroll
@@ -357,7 +377,10 @@ __device__ __forceinline__ void gemm_nt_tile(const T* __restrict__ A, int64_t ld
 #pragma unroll
         for (int i = 0; i < A_CH; ++i) {
             const int c = tid + i * NT;
-            *reinterpret_cast<u32x4*>(&As[buf][(c / CPR) * LDK + (c % CPR) * 8]) = R.a[i];
+            if constexpr (AKM)
+                *reinterpret_cast<u32x4*>(&As[buf][(c / (BM / 8)) * PMA + (c % (BM / 8)) * 8]) = R.a[i];
+            else
+                *reinterpret_cast<u32x4*>(&As[buf][(c / CPR) * LDK + (c % CPR) * 8]) = R.a[i];
         }
 #pragma unroll
         for (int i = 0; i < B_CH; ++i) *reinterpret_cast<u32x4*>(&Bs[buf][R.blds[i]]) = R.b[i];
@@ -386,12 +409,22 @@ __device__ __forceinline__ void gemm_nt_tile(const T* __restrict__ A, int64_t ld
     const int frag_row = lane & 31, frag_k = (lane >> 5) * 8;
     u32x4 fa[2][TM], fb[2][TN];
     auto lds_frag = [&](int buf, int kk, int slot) {
-        const T* as = &As[buf][(wm * WTM + frag_row) * LDK + frag_k + kk * 16];
-        const T* bs = &Bs[buf][(wn * WTN + frag_row) * LDK + frag_k + kk * 16];
+        if constexpr (AKM) {
 #pragma unroll
-        for (int i = 0; i < TM; ++i) fa[slot][i] = *reinterpret_cast<const u32x4*>(as + i * 32 * LDK);
+            for (int i = 0; i < TM; ++i) fa[slot][i] = frag_kmajor<T, PMA>(As[buf], kk * 16, wm * WTM + i * 32, lane);
+        } else {
+            const T* as = &As[buf][(wm * WTM + frag_row) * LDK + frag_k + kk * 16];
 #pragma unroll
-        for (int j = 0; j < TN; ++j) fb[slot][j] = *reinterpret_cast<const u32x4*>(bs + j * 32 * LDK);
+            for (int i = 0; i < TM; ++i) fa[slot][i] = *reinterpret_cast<const u32x4*>(as + i * 32 * LDK);
+        }
+        if constexpr (BKM) {
+#pragma unroll
+            for (int j = 0; j < TN; ++j) fb[slot][j] = frag_kmajor<T, PMB>(Bs[buf], kk * 16, wn * WTN + j * 32, lane);
+        } else {
+            const T* bs = &Bs[buf][(wn * WTN + frag_row) * LDK + frag_k + kk * 16];
+#pragma unroll
+            for (int j = 0; j < TN; ++j) fb[slot][j] = *reinterpret_cast<const u32x4*>(bs + j * 32 * LDK);
+        }
     };
 
     const int64_t nk = ceil_div(kend - kbeg, BK);
@@ -449,7 +482,7 @@ __device__ __forceinline__ void gemm_nt_tile(const T* __restrict__ A, int64_t ld
     if constexpr (StagedEpiT<Epi>::value) {
         staged_store<BM, BN, WM, WN, TM, TN>(acc, m0, n0, epi, smem, LDS_BYTES);
         return;
-    } else if constexpr (TransposedPartEpiT<Epi>::value) {
+    } else if constexpr (RowsPlusStagedEpiT<Epi>::value) {
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
             const auto c = epi.col(n0 + wn * WTN + j * 32 + (lane & 31));
@@ -464,8 +497,7 @@ __device__ __forceinline__ void gemm_nt_tile(const T* __restrict__ A, int64_t ld
                 }
             }
         }
-        staged_store_t<BM, BN, WM, WN, TM, TN>(acc, m0, n0, reinterpret_cast<uint16_t*>(epi.gpt), epi.ldt, epi.r,
-                                               epi.M, smem, LDS_BYTES);
+        staged_store<BM, BN, WM, WN, TM, TN>(acc, m0, n0, epi.staged(), smem, LDS_BYTES);
         return;
     } else if constexpr (DualEpiT<Epi>::value) {
 #pragma unroll
@@ -510,7 +542,7 @@ struct SplitEpi;
 // K splitting (partial products, Epi = SplitEpi): workgroup (tile,
 // blockIdx.y = s) reduces K range [s * k_split, min(K, (s + 1) * k_split));
 // k_split is a multiple of BK.  Every other epilogue covers all of K.
-template <typename T, int BM, int BN, int BK, int WM, int WN, bool BPACK, int PGR, typename Epi>
+template <typename T, int BM, int BN, int BK, int WM, int WN, bool BPACK, int PGR, typename Epi, int KM = 0>
 __global__ __launch_bounds__(WM* WN* kWave) void gemm_nt_mfma(const T* __restrict__ A, int64_t lda,
                                                              int64_t M, const T* __restrict__ B,
                                                              int64_t ldb, int64_t N, int64_t K,
@@ -520,12 +552,12 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_nt_mfma(const T* __restric
     if constexpr (std::is_same<Epi, SplitEpi>::value) {
         const int64_t kbeg = (int64_t)blockIdx.y * k_split;
         const int64_t kend = (kbeg + k_split) < K ? (kbeg + k_split) : K;
-        gemm_nt_tile<T, BM, BN, BK, WM, WN, BPACK, PGR, Epi>(A, lda, M, B, ldb, N, K, kbeg, kend, tm, tn, epi);
+        gemm_nt_tile<T, BM, BN, BK, WM, WN, BPACK, PGR, Epi, KM>(A, lda, M, B, ldb, N, K, kbeg, kend, tm, tn, epi);
     } else {
         // only the partial products of a split launch cover part of K; with
         // the whole range fixed at compile time the K loop's addressing is
         // simpler (measured about 3% faster on the GEMM1 shape)
-        gemm_nt_tile<T, BM, BN, BK, WM, WN, BPACK, PGR, Epi>(A, lda, M, B, ldb, N, K, 0, K, tm, tn, epi);
+        gemm_nt_tile<T, BM, BN, BK, WM, WN, BPACK, PGR, Epi, KM>(A, lda, M, B, ldb, N, K, 0, K, tm, tn, epi);
     }
 }
 

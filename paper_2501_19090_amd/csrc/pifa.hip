@@ -303,7 +303,7 @@ GemmPlan gemm_plan(int64_t M, int64_t N, int64_t K, bool wide_ok, bool can_split
     return {128, 128, p};
 }
 
-template <typename T, bool BPACK, typename Epi>
+template <typename T, bool BPACK, typename Epi, int KM = 0>
 hipError_t launch_gemm(int site, const T* A, int64_t lda, int64_t M, const T* B, int64_t ldb,
                        int64_t N, int64_t K, Epi epi, float* partials, hipStream_t st) {
     if (M == 0 || N == 0) return hipSuccess;
@@ -317,36 +317,36 @@ hipError_t launch_gemm(int site, const T* A, int64_t lda, int64_t M, const T* B,
     const dim3 grid((unsigned)(ceil_div(M, g.bm) * ceil_div(N, g.bn)));
     if (g.bm == 256 && g.bn == 256) {
         if constexpr (DualEpiT<Epi>::value)
-            hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 256, kGemmBK, 2, 4, BPACK, 1, ScatterEpi<bf16, kWsF16>>), grid,
+            hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 256, kGemmBK, 2, 4, BPACK, 1, ScatterEpi<bf16, kWsF16>, KM>), grid,
                                dim3(8 * kWave), 0, st, A, lda, M, B, ldb, N, K, K, epi.elementwise());
         else if constexpr (kWideOk)
-            hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 256, kGemmBK, 2, 4, BPACK, 1, Epi>), grid, dim3(8 * kWave), 0,
+            hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 256, kGemmBK, 2, 4, BPACK, 1, Epi, KM>), grid, dim3(8 * kWave), 0,
                                st, A, lda, M, B, ldb, N, K, K, epi);
     } else if (g.bm == 256 && g.bn == 192) {
         if constexpr (kWideOk)
-            hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 192, kGemmBK, 4, 2, BPACK, 2, Epi>), grid, dim3(8 * kWave), 0,
+            hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 192, kGemmBK, 4, 2, BPACK, 2, Epi, KM>), grid, dim3(8 * kWave), 0,
                                st, A, lda, M, B, ldb, N, K, K, epi);
     } else if (g.bm == 256) {
-        hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 128, kGemmBK, 4, 2, BPACK, 2, Epi>), grid, dim3(8 * kWave), 0, st,
+        hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 128, kGemmBK, 4, 2, BPACK, 2, Epi, KM>), grid, dim3(8 * kWave), 0, st,
                            A, lda, M, B, ldb, N, K, K, epi);
     } else if (g.split.splits == 1) {
         if (g.bn == 64)
-            hipLaunchKernelGGL((gemm_nt_mfma<T, 128, 64, kGemmBK, 4, 2, BPACK, 2, Epi>), grid, dim3(8 * kWave), 0,
+            hipLaunchKernelGGL((gemm_nt_mfma<T, 128, 64, kGemmBK, 4, 2, BPACK, 2, Epi, KM>), grid, dim3(8 * kWave), 0,
                                st, A, lda, M, B, ldb, N, K, K, epi);
         else
-            hipLaunchKernelGGL((gemm_nt_mfma<T, 128, 128, kGemmBK, 4, 2, BPACK, 2, Epi>), grid, dim3(8 * kWave), 0,
+            hipLaunchKernelGGL((gemm_nt_mfma<T, 128, 128, kGemmBK, 4, 2, BPACK, 2, Epi, KM>), grid, dim3(8 * kWave), 0,
                                st, A, lda, M, B, ldb, N, K, K, epi);
     } else {
         SplitEpi se{partials, M, N};
         const dim3 sgrid(grid.x, (unsigned)g.split.splits);
         if (g.bm == 64)
-            hipLaunchKernelGGL((gemm_nt_mfma<T, 64, 64, kGemmBK, 2, 2, BPACK, 2, SplitEpi>), sgrid,
+            hipLaunchKernelGGL((gemm_nt_mfma<T, 64, 64, kGemmBK, 2, 2, BPACK, 2, SplitEpi, KM>), sgrid,
                                dim3(4 * kWave), 0, st, A, lda, M, B, ldb, N, K, g.split.k_split, se);
         else if (g.bn == 64)
-            hipLaunchKernelGGL((gemm_nt_mfma<T, 128, 64, kGemmBK, 4, 2, BPACK, 2, SplitEpi>), sgrid,
+            hipLaunchKernelGGL((gemm_nt_mfma<T, 128, 64, kGemmBK, 4, 2, BPACK, 2, SplitEpi, KM>), sgrid,
                                dim3(8 * kWave), 0, st, A, lda, M, B, ldb, N, K, g.split.k_split, se);
         else
-            hipLaunchKernelGGL((gemm_nt_mfma<T, 128, 128, kGemmBK, 4, 2, BPACK, 2, SplitEpi>), sgrid,
+            hipLaunchKernelGGL((gemm_nt_mfma<T, 128, 128, kGemmBK, 4, 2, BPACK, 2, SplitEpi, KM>), sgrid,
                                dim3(8 * kWave), 0, st, A, lda, M, B, ldb, N, K, g.split.k_split, se);
         const int64_t work = M * ceil_div(N, 4);
         hipLaunchKernelGGL((split_reduce<Epi>), dim3((unsigned)std::min<int64_t>(ceil_div(work, 256), 65536)),
@@ -1365,47 +1365,37 @@ pifa_status pifa_layer_backward(pifa_handle h, const void* X, const void* Y, con
     pifa_status s = prepare_backward(h);
     if (s != PIFA_OK) return s;
 
-    const int64_t M_pad = round_up(M, (int64_t)8), ldc = round_up(n_np, (int64_t)8);
+    const int64_t ldc = round_up(n_np, (int64_t)8), ldy = round_up(r, (int64_t)8);
     // workspace regions, in 2-byte elements (each a multiple of 256 bytes)
-    const int64_t e_gic = align_elems(M * ldc), e_gict = align_elems(n_np * M_pad), e_ypt = align_elems(r * M_pad),
-                  e_xt = align_elems(d_in * M_pad), e_gp32 = align_elems(2 * M * r_pad),
-                  e_gp16 = align_elems(M * r_pad), e_inv = align_elems(2 * M), e_gpt = align_elems(r * M_pad);
-    const size_t part = std::max({split_bytes(M, r_pad, ldc), split_bytes(M, d_in, r_pad),
-                                  split_bytes(r, d_in, M_pad), split_bytes(n_np, r, M_pad)});
-    const size_t main_bytes = (size_t)(e_gic + e_gict + e_ypt + e_xt + e_gp32 + e_gp16 + e_inv + e_gpt) * 2;
+    const int64_t e_gic = align_elems(M * ldc), e_ypr = align_elems(M * ldy), e_gp32 = align_elems(2 * M * r_pad),
+                  e_gp16 = align_elems(M * r_pad), e_inv = align_elems(2 * M), e_gpb = align_elems(M * r_pad);
+    const size_t part = std::max({split_bytes(M, r_pad, ldc), split_bytes(M, d_in, r_pad), split_bytes(r, d_in, M),
+                                  split_bytes(n_np, r, M)});
+    const size_t main_bytes = (size_t)(e_gic + e_ypr + e_gp32 + e_gp16 + e_inv + e_gpb) * 2;
     s = h->bws.ensure(main_bytes + part, st);
     if (s != PIFA_OK) return s;
     bf16* gic = (bf16*)h->bws.ptr;
-    bf16* gict = gic + e_gic;
-    bf16* ypt = gict + e_gict;
-    bf16* xt = ypt + e_ypt;
-    float* gp32 = (float*)(xt + e_xt);
-    f16* gp16 = (f16*)(xt + e_xt + e_gp32);
-    float* inv = (float*)(xt + e_xt + e_gp32 + e_gp16);
-    bf16* gpt = xt + e_xt + e_gp32 + e_gp16 + e_inv;
+    bf16* ypr = gic + e_gic;
+    float* gp32 = (float*)(ypr + e_ypr);
+    f16* gp16 = (f16*)(ypr + e_ypr + e_gp32);
+    float* inv = (float*)(ypr + e_ypr + e_gp32 + e_gp16);
+    bf16* gpb = ypr + e_ypr + e_gp32 + e_gp16 + e_inv;
     float* partials = part ? (float*)((char*)h->bws.ptr + main_bytes) : nullptr;
     const bf16* G = (const bf16*)dY;
     hipError_t e = hipSuccess;
 
-    {  // operands in K-contiguous form: G[:, I^c] (rows and transposed), Y_p^T, X^T
+    {  // the gathered columns G[:, I^c] and Y[:, I] as rows
         TimedLaunch timed(kSiteBwdData, st);
-        if (n_np > 0 && (e = launch_gather(G, d_out, M, h->npiv, n_np, gic, ldc, dC ? gict : nullptr, M_pad, st)) !=
-                            hipSuccess)
+        if (n_np > 0 && (e = launch_gather(G, d_out, M, h->npiv, n_np, gic, ldc, nullptr, 0, st)) != hipSuccess)
             return PIFA_ERR_HIP;
         if (n_np > 0 && dC &&
-            (e = launch_gather((const bf16*)Y, d_out, M, h->piv, r, nullptr, 0, ypt, M_pad, st)) != hipSuccess)
-            return PIFA_ERR_HIP;
-        if (dW_p && (e = launch_gather((const bf16*)X, d_in, M, nullptr, d_in, nullptr, 0, xt, M_pad, st)) != hipSuccess)
+            (e = launch_gather((const bf16*)Y, d_out, M, h->piv, r, ypr, ldy, nullptr, 0, st)) != hipSuccess)
             return PIFA_ERR_HIP;
     }
-    // G_p = G[:, I^c] C + G[:, I] in fp32, and bf16(G_p)^T
+    // G_p = G[:, I^c] C + G[:, I] in fp32, and bf16(G_p)
     e = launch_gemm<bf16, true>(kSiteBwdGp, gic, ldc, M, (const bf16*)h->bwd_ct, 0, r_pad, ldc,
-                                GradPivotEpi{G, d_out, h->piv, r, r_pad, gp32, gpt, M_pad, M}, partials, st);
+                                GradPivotEpi{G, d_out, h->piv, r, r_pad, gp32, gpb, M}, partials, st);
     if (e != hipSuccess) return PIFA_ERR_HIP;
-    if (M_pad > M) {
-        hipLaunchKernelGGL(zero_cols, dim3(grid_for(r * (M_pad - M))), dim3(256), 0, st, gpt, r, M_pad, M);
-        if (hipGetLastError() != hipSuccess) return PIFA_ERR_HIP;
-    }
     if (dX) {  // dX = (G_p 2^s_m in fp16) (W_p^T 2^cw in fp16)^T 2^-(s_m + cw)
         {
             TimedLaunch timed(kSiteBwdRows, st);
@@ -1417,18 +1407,18 @@ pifa_status pifa_layer_backward(pifa_handle h, const void* X, const void* Y, con
                                    st);
         if (e != hipSuccess) return PIFA_ERR_HIP;
     }
+    // the transposed products reduce over the M activation rows: both
+    // operands are read K-major (rows of G_p, X, G[:, I^c], Y[:, I])
     if (dW_p) {  // dW_p = G_p^T X
-        e = launch_gemm<bf16, false>(kSiteBwdDwp, gpt, M_pad, r, xt, M_pad, d_in, M_pad,
-                                     make_epi<float, kWsNone>(dW_p, d_in, nullptr, d_in, 1.f, nullptr, 0, 0, 1.f,
-                                                              nullptr, r),
-                                     partials, st);
+        e = launch_gemm<bf16, false, ScatterEpi<float, kWsNone>, 3>(
+            kSiteBwdDwp, gpb, r_pad, r, (const bf16*)X, d_in, d_in, M,
+            make_epi<float, kWsNone>(dW_p, d_in, nullptr, d_in, 1.f, nullptr, 0, 0, 1.f, nullptr, r), partials, st);
         if (e != hipSuccess) return PIFA_ERR_HIP;
     }
     if (dC && n_np > 0) {  // dC = G[:, I^c]^T Y_p
-        e = launch_gemm<bf16, false>(kSiteBwdDc, gict, M_pad, n_np, ypt, M_pad, r, M_pad,
-                                     make_epi<float, kWsNone>(dC, r, nullptr, r, 1.f, nullptr, 0, 0, 1.f, nullptr,
-                                                              n_np),
-                                     partials, st);
+        e = launch_gemm<bf16, false, ScatterEpi<float, kWsNone>, 3>(
+            kSiteBwdDc, gic, ldc, n_np, ypr, ldy, r, M,
+            make_epi<float, kWsNone>(dC, r, nullptr, r, 1.f, nullptr, 0, 0, 1.f, nullptr, n_np), partials, st);
         if (e != hipSuccess) return PIFA_ERR_HIP;
     }
     return PIFA_OK;
