@@ -1579,6 +1579,24 @@ pifa_status pifa_calib_accumulate(pifa_calib_handle c, const void* X_o, const vo
     PIFA_ON_DEVICE(c->device);
     hipStream_t st = as_stream(stream);
     const int64_t n = c->n, Bp = round_up(B, (int64_t)8);
+    if (n % 8 == 0 && aligned16(X_o) && aligned16(X_u)) {
+        // the batches' rows are the products' K-major operands (K = tokens)
+        const size_t part = split_bytes(n, n, B);
+        pifa_status s = c->ws.ensure(part, st);
+        if (s != PIFA_OK) return s;
+        float* partials = part ? (float*)c->ws.ptr : nullptr;
+        const bf16* xu = (const bf16*)X_u;
+        const bf16* xo = (const bf16*)X_o;
+        // S is symmetric: only its lower tiles are accumulated (completed on read)
+        if (launch_gemm<bf16, false, AccF64Epi, 3>(kSiteCalibGram, xu, n, n, xu, n, n, B,
+                                                   AccF64Epi{c->S, n, n, n, true}, partials, st) != hipSuccess)
+            return PIFA_ERR_HIP;
+        if (launch_gemm<bf16, false, AccF64Epi, 3>(kSiteCalibGram, xo, n, n, xu, n, n, B,
+                                                   AccF64Epi{c->P, n, n, n, false}, partials, st) != hipSuccess)
+            return PIFA_ERR_HIP;
+        return PIFA_OK;
+    }
+    // unaligned rows: transposed copies of the batches, then K-contiguous products
     const int64_t e_t = align_elems(n * Bp);
     const size_t part = split_bytes(n, n, Bp);
     pifa_status s = c->ws.ensure((size_t)(2 * e_t) * 2 + part, st);

@@ -51,7 +51,9 @@ def _gpu_run(n, W, Vt, xo_st, xu_st, batches, lam, alpha):
         pifa.pifa_calib_destroy(h)
 
 
-@pytest.mark.parametrize("n,m,r,b,batches", [(256, 320, 64, 1500, 3), (136, 96, 40, 701, 2), (512, 1024, 200, 2048, 4)])
+# n = 100: rows that are not 16-byte multiples take the transposed-copy path
+@pytest.mark.parametrize("n,m,r,b,batches", [(256, 320, 64, 1500, 3), (136, 96, 40, 701, 2), (512, 1024, 200, 2048, 4),
+                                             (100, 80, 24, 500, 2)])
 def test_reconstruct_matches_oracle(n, m, r, b, batches):
     rng = np.random.default_rng(n + m)
     W = rng.standard_normal((m, n)) / np.sqrt(n)
