@@ -178,17 +178,23 @@ struct GradPivotEpi {
         int64_t src;
         bool piv_ok;
     };
+    // The loads below are unconditional, from clamped (valid) addresses, with
+    // the result selected afterwards: a load under a lane-dependent condition
+    // is compiled as a branch that waits for it, which serialised the 64
+    // starting-value loads of a lane (15 of the product's 63 us).
     __device__ __forceinline__ Col col(int64_t n) const {
         Col c;
         c.n = n;
         c.piv_ok = n < r;
-        c.src = c.piv_ok ? (int64_t)piv[n] : 0;
+        const int32_t p = piv[c.piv_ok ? n : 0];
+        c.src = c.piv_ok ? (int64_t)p : 0;
         return c;
     }
     // the product starts from G[m, piv[n]] (the G[:, I] term)
     __device__ __forceinline__ float init(int64_t m, const Col& c) const {
         const uint16_t* g16 = reinterpret_cast<const uint16_t*>(G);
-        return (c.piv_ok && m < M) ? bf16_bits_to_f32(g16[m * ldg + c.src]) : 0.f;
+        const float g = bf16_bits_to_f32(g16[(m < M ? m : 0) * ldg + c.src]);
+        return (c.piv_ok && m < M) ? g : 0.f;
     }
     __device__ __forceinline__ void store(int64_t m, const Col& c, float v) const {
         if (m >= M || c.n >= r_pad) return;

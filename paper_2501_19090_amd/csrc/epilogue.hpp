@@ -44,7 +44,15 @@ struct ScatterEpi {
         Col c;
         c.n = n;
         c.out_ok = n < n_out;
-        c.dst = c.out_ok ? (idx ? (int64_t)idx[n] : n) : 0;
+        // A load under a condition (the lane's, or idx == nullptr) becomes a
+        // branch whose join waits for it, so the index is read unconditionally
+        // through a buffer resource: a clamped offset, and an empty range
+        // (the load returns 0 without an access) when there is no map.
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<int32_t*>(idx), (short)0, idx ? (int)(n_out * 4) : 0, 0x00020000);
+        const int32_t v = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(rs, (int)((c.out_ok ? n : 0) * 4), 0, 0);
+        const int64_t d = idx ? (int64_t)v : n;
+        c.dst = c.out_ok ? d : 0;
         if (c.dst < 0) {  // a padding column of a grouped layer: no output
             c.out_ok = false;
             c.dst = 0;

@@ -391,11 +391,30 @@ __device__ __forceinline__ void gemm_nt_tile(const T* __restrict__ A, int64_t ld
     for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j) acc[i][j] = f32x16{};
+    // The epilogue's column descriptors (output index loads).  The epilogues
+    // that start from loaded values or write two outputs take them before the
+    // K loop on tiles with at most 4 accumulator blocks per wave, so the
+    // loads are in flight with the first tiles (the pivot product: 82.4 ->
+    // 80.4 us); the others take them after the loop (early, the non-pivot
+    // product took 1 us longer), as do the wider tiles, which have no
+    // registers to spare across the loop.
+    const auto& ecol_src = [&]() -> decltype(auto) {
+        if constexpr (DualEpiT<Epi>::value) return (epi.y);
+        else return (epi);
+    }();
+    using ECol = decltype(ecol_src.col(0));
+    constexpr bool kEarlyCols = InitEpi<Epi>::value || (DualEpiT<Epi>::value && TM * TN <= 4);
+    ECol ecols[TN];
+    auto fill_ecols = [&]() {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) ecols[j] = ecol_src.col(n0 + wn * WTN + j * 32 + (lane & 31));
+    };
+    if constexpr (kEarlyCols) fill_ecols();
     if constexpr (InitEpi<Epi>::value) {
         // 32x32 accumulator layout (see the epilogue below)
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
-            const auto c = epi.col(n0 + wn * WTN + j * 32 + (lane & 31));
+            const auto& c = ecols[j];
 #pragma unroll
             for (int i = 0; i < TM; ++i) {
                 const int64_t mb = m0 + wm * WTM + i * 32 + 4 * (lane >> 5);
@@ -479,13 +498,14 @@ __device__ __forceinline__ void gemm_nt_tile(const T* __restrict__ A, int64_t ld
     for (int u = 0; u < PGR - 1; ++u)
         if (kt + u < nk) body(kt + u, S[(u + 1) % PGR]);
 
+    if constexpr (!kEarlyCols) fill_ecols();
     if constexpr (StagedEpiT<Epi>::value) {
         staged_store<BM, BN, WM, WN, TM, TN>(acc, m0, n0, epi, smem, LDS_BYTES);
         return;
     } else if constexpr (RowsPlusStagedEpiT<Epi>::value) {
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
-            const auto c = epi.col(n0 + wn * WTN + j * 32 + (lane & 31));
+            const auto& c = ecols[j];
 #pragma unroll
             for (int i = 0; i < TM; ++i) {
                 const int64_t mb = m0 + wm * WTM + i * 32 + 4 * (lane >> 5);
@@ -502,7 +522,7 @@ __device__ __forceinline__ void gemm_nt_tile(const T* __restrict__ A, int64_t ld
     } else if constexpr (DualEpiT<Epi>::value) {
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
-            const auto c = epi.y.col(n0 + wn * WTN + j * 32 + (lane & 31));
+            const auto& c = ecols[j];
 #pragma unroll
             for (int i = 0; i < TM; ++i) {
                 const int64_t mb = m0 + wm * WTM + i * 32 + 4 * (lane >> 5);
@@ -517,7 +537,7 @@ __device__ __forceinline__ void gemm_nt_tile(const T* __restrict__ A, int64_t ld
     // 8*(v/4) + 4*(lane/32) + (v%4) for v = 0..15.
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
-        const auto c = epi.col(n0 + wn * WTN + j * 32 + (lane & 31));
+        const auto& c = ecols[j];
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
             const int64_t mb = m0 + wm * WTM + i * 32 + 4 * (lane >> 5);
