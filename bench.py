@@ -643,9 +643,14 @@ def main():
     # ---- the clock the matrix cores hold right after that load, and the
     # sustained MFMA-only rate at it (no memory traffic)
     probe_tflops, sclk_mhz = pifa.pifa_probe_mfma(20000)
+    # and on operands that change with every MFMA, as a GEMM's do: matrix-core
+    # power follows the toggling operand bits, so under the board's power
+    # limit this is the rate (and clock) a GEMM on random data can approach
+    probe_rand_tflops, sclk_rand_mhz = pifa.pifa_probe_mfma_random(40000)
     log("prefill M=%d: %.1f us/step (%.1f with per-launch events), %.1f TFLOP/s; kernels %s; "
-        "MFMA-only %.0f TFLOP/s at %.0f MHz"
-        % (M, 1e3 * ms_step, 1e3 * ms_step_instrumented, value, kern, probe_tflops, sclk_mhz))
+        "MFMA-only %.0f TFLOP/s at %.0f MHz (constant operands), %.0f TFLOP/s at %.0f MHz (random operands)"
+        % (M, 1e3 * ms_step, 1e3 * ms_step_instrumented, value, kern, probe_tflops, sclk_mhz,
+           probe_rand_tflops, sclk_rand_mhz))
 
     def kernel_roof(site, flops):
         n, ms = kern[site]
@@ -656,7 +661,10 @@ def main():
 
     g1 = kernel_roof("pifa_gemm1_xwp", 2.0 * M * r * d_in)
     g2 = kernel_roof("pifa_gemm2_ypc", 2.0 * M * r * (d_out - r))
-    peak_at_clock = PEAK_BF16_TFLOPS * sclk_mhz / PEAK_SCLK_MHZ
+    # the clock a GEMM on random data holds is the random-operand probe's
+    # (an instrumented copy of the kernels read 1896 MHz inside GEMM1 where
+    # that probe read 1906), not the constant-operand probe's
+    peak_at_clock = PEAK_BF16_TFLOPS * sclk_rand_mhz / PEAK_SCLK_MHZ
     traffic = traffic_from_profiles("pifa_gemm1_xwp")
     roofline = {"bound": "mfma", "kernel": "pifa_gemm1_xwp (X W_p^T, bf16 MFMA, pivot-column epilogue)",
                 "achieved": g1["achieved"], "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": g1["frac"],
@@ -665,12 +673,16 @@ def main():
                 "gemm2": dict(g2, kernel="pifa_gemm2_ypc (Y_p C^T, fp16 MFMA, non-pivot epilogue)"),
                 "layer": {"us": 1e3 * ms_step, "achieved": value, "frac": value / PEAK_BF16_TFLOPS},
                 "sclk_mhz": sclk_mhz,
+                "sclk_mhz_random_operands": sclk_rand_mhz,
                 "frac_at_measured_clock": g1["achieved"] / peak_at_clock,
                 "mfma_only_tflops": probe_tflops,
+                "mfma_only_random_operands": {"tflops": probe_rand_tflops, "sclk_mhz": sclk_rand_mhz,
+                                              "gemm1_frac_of_it": g1["achieved"] / probe_rand_tflops},
                 "timing": "HIP events around every launch on its stream, over K instrumented steps run "
                           "right after the K timed steps on settled clocks (%.1f us/step with the events); "
-                          "sclk from shader-clock / real-time counters of an MFMA-only kernel run right "
-                          "after them" % (1e3 * ms_step_instrumented)}
+                          "sclk from shader-clock / real-time counters of MFMA-only kernels run right "
+                          "after them (constant operands, then random operands that change with every "
+                          "MFMA)" % (1e3 * ms_step_instrumented)}
     kernels = {k: {"launches": n, "avg_us": 1e3 * v / n} for k, (n, v) in kern.items()}
 
     # ---- the decode case
@@ -689,7 +701,9 @@ def main():
     del buf
     torch.cuda.empty_cache()
     peak_check = {"mfma_only_tflops": probe_tflops, "sclk_mhz_under_mfma": sclk_mhz,
-                  "peak_bf16_tflops_at_that_clock": peak_at_clock, "hbm_read_gbps": hbm_read,
+                  "mfma_only_random_operands_tflops": probe_rand_tflops,
+                  "sclk_mhz_under_mfma_random_operands": sclk_rand_mhz,
+                  "peak_bf16_tflops_at_random_operand_clock": peak_at_clock, "hbm_read_gbps": hbm_read,
                   "what": "MFMA-only kernel (2048 x 4 waves of independent 32x32x16 bf16 MFMAs) and "
                           "grid-stride streaming reads of a zero-filled 1 GiB buffer (best of 3 grid sizes, "
                           "5 reads each), on this GPU in this run"}

@@ -394,6 +394,13 @@ pifa_status pifa_profile_read(const char** names, int64_t* launches, double* tot
  * FLOP rate; *sclk_mhz is the shader clock the loop ran at, averaged over
  * the workgroups (shader-clock cycles over real-time-clock ticks).
  *
+ * pifa_probe_mfma_random: the same on operands that change with every MFMA
+ * (each wave cycles through 8 register sets of random bf16 values; `iters`
+ * is rounded up to a multiple of 8).  Matrix-core power grows with the
+ * operand bits that toggle, so under the board's power limit this rate and
+ * clock are what a GEMM on real data can approach, while pifa_probe_mfma's
+ * constant operands give the rate at the unthrottled clock.
+ *
  * pifa_probe_hbm_read: `reps` back-to-back reads of the device buffer `buf`
  * (`bytes` a multiple of 16, 16-byte aligned; larger than the 256 MB
  * Infinity Cache to measure HBM) with 16-byte loads in a grid-stride loop;
@@ -404,6 +411,7 @@ pifa_status pifa_profile_read(const char** names, int64_t* launches, double* tot
  * a launch or event fails.
  */
 pifa_status pifa_probe_mfma(int64_t iters, double* tflops, double* sclk_mhz, void* stream);
+pifa_status pifa_probe_mfma_random(int64_t iters, double* tflops, double* sclk_mhz, void* stream);
 pifa_status pifa_probe_hbm_read(const void* buf, int64_t bytes, int reps, double* gbps, void* stream);
 
 #ifdef __cplusplus

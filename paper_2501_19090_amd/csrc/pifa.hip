@@ -2102,8 +2102,11 @@ struct DevBuf {
 
 }  // namespace
 
-pifa_status pifa_probe_mfma(int64_t iters, double* tflops, double* sclk_mhz, void* stream) {
+namespace {
+
+pifa_status probe_mfma(bool random, int64_t iters, double* tflops, double* sclk_mhz, void* stream) {
     if (iters < 1 || !tflops || !sclk_mhz) return PIFA_ERR_INVALID_ARG;
+    if (random) iters = round_up(iters, 8);
     hipStream_t st = as_stream(stream);
     constexpr unsigned kGrid = 2048, kThreads = 256;
     DevBuf clocks, sink;
@@ -2120,8 +2123,12 @@ pifa_status pifa_probe_mfma(int64_t iters, double* tflops, double* sclk_mhz, voi
         return PIFA_ERR_HIP;
     }
     auto run = [&]() {
-        hipLaunchKernelGGL(mfma_probe, dim3(kGrid), dim3(kThreads), 0, st, iters, 0.0f, (float*)sink.p,
-                           (uint64_t*)clocks.p);
+        if (random)
+            hipLaunchKernelGGL(mfma_probe_random, dim3(kGrid), dim3(kThreads), 0, st, iters, 0.0f, (float*)sink.p,
+                               (uint64_t*)clocks.p);
+        else
+            hipLaunchKernelGGL(mfma_probe, dim3(kGrid), dim3(kThreads), 0, st, iters, 0.0f, (float*)sink.p,
+                               (uint64_t*)clocks.p);
         return hipGetLastError();
     };
     float ms = 0.f;
@@ -2144,6 +2151,16 @@ pifa_status pifa_probe_mfma(int64_t iters, double* tflops, double* sclk_mhz, voi
     }
     *sclk_mhz = n ? mhz / n : 0.0;
     return PIFA_OK;
+}
+
+}  // namespace
+
+pifa_status pifa_probe_mfma(int64_t iters, double* tflops, double* sclk_mhz, void* stream) {
+    return probe_mfma(false, iters, tflops, sclk_mhz, stream);
+}
+
+pifa_status pifa_probe_mfma_random(int64_t iters, double* tflops, double* sclk_mhz, void* stream) {
+    return probe_mfma(true, iters, tflops, sclk_mhz, stream);
 }
 
 pifa_status pifa_probe_hbm_read(const void* buf, int64_t bytes, int reps, double* gbps, void* stream) {

@@ -42,6 +42,57 @@ __global__ __launch_bounds__(256) void mfma_probe(int64_t iters, float seed, flo
     }
 }
 
+// The same loop on operands that change with every MFMA, as a GEMM's do:
+// each wave holds 8 register sets of random bf16 values (random sign and
+// mantissa, magnitudes in [0.5, 1)) and each MFMA of a round of 8 takes a
+// different pair.  Matrix-core power depends on how many operand bits toggle,
+// so under the board's power limit this loop runs at a lower clock than
+// mfma_probe's constant operands; the pair of rates brackets what a GEMM on
+// real data can reach.  `iters` is a multiple of 8.
+__device__ __forceinline__ uint32_t probe_mix(uint32_t x) {
+    x ^= x >> 16;
+    x *= 0x7FEB352Du;
+    x ^= x >> 15;
+    x *= 0x846CA68Bu;
+    x ^= x >> 16;
+    return x;
+}
+
+__global__ __launch_bounds__(256) void mfma_probe_random(int64_t iters, float seed, float* sink, uint64_t* clocks) {
+    const uint32_t base = (uint32_t)(blockIdx.x * 256 + threadIdx.x) * 64u ^ __builtin_bit_cast(uint32_t, seed);
+    u32x4 a[8], b[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            a[q][w] = (probe_mix(base + 8 * q + w) & 0x807F807Fu) | 0x3F003F00u;
+            b[q][w] = (probe_mix(base + 8 * q + w + 4) & 0x807F807Fu) | 0x3F003F00u;
+        }
+    }
+    f32x16 c0{}, c1{}, c2{}, c3{};
+    const uint64_t cyc0 = __builtin_amdgcn_s_memtime();
+    const uint64_t rt0 = __builtin_amdgcn_s_memrealtime();
+    for (int64_t i = 0; i < iters; i += 8) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            c0 = Mfma<bf16>::mma32(a[q], b[q], c0);
+            c1 = Mfma<bf16>::mma32(b[(q + 1) & 7], a[(q + 3) & 7], c1);
+            c2 = Mfma<bf16>::mma32(a[(q + 5) & 7], b[(q + 2) & 7], c2);
+            c3 = Mfma<bf16>::mma32(b[(q + 6) & 7], a[(q + 7) & 7], c3);
+        }
+    }
+    float s = 0.f;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) s += c0[v] + c1[v] + c2[v] + c3[v];
+    const uint64_t cyc1 = __builtin_amdgcn_s_memtime();
+    const uint64_t rt1 = __builtin_amdgcn_s_memrealtime();
+    if (s == seed) sink[blockIdx.x] = s;
+    if (threadIdx.x == 0) {
+        clocks[2 * blockIdx.x] = cyc1 - cyc0;
+        clocks[2 * blockIdx.x + 1] = rt1 - rt0;
+    }
+}
+
 // Streams `n16` 16-byte words of a buffer, one load per thread per step of a
 // grid-stride loop; a word is stored only if the XOR of what a thread read
 // equals a fixed constant (which keeps the loads; the benchmark's zero-filled

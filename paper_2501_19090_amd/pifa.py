@@ -92,6 +92,7 @@ _SIGNATURES = {
     "pifa_calib_reconstruct": (_st, [_vp, _vp, _i64, _vp, _i64, ctypes.c_double, ctypes.c_double, _vp, _vp, _vp]),
     "pifa_build_f64": (_st, [_vp, pifa_dims, _vp, _vp, _i32p, _i32p, ctypes.POINTER(ctypes.c_double), _vp]),
     "pifa_probe_mfma": (_st, [_i64, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double), _vp]),
+    "pifa_probe_mfma_random": (_st, [_i64, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double), _vp]),
     "pifa_probe_hbm_read": (_st, [_vp, _i64, ctypes.c_int, ctypes.POINTER(ctypes.c_double), _vp]),
     "pifa_profile_enable": (_st, [ctypes.c_int]),
     "pifa_profile_reset": (_st, []),
@@ -571,6 +572,15 @@ def pifa_probe_mfma(iters: int = 20000, stream=None):
     tf, mhz = ctypes.c_double(), ctypes.c_double()
     _check("pifa_probe_mfma", lib().pifa_probe_mfma(int(iters), ctypes.byref(tf), ctypes.byref(mhz),
                                                     _stream(stream)))
+    return tf.value, mhz.value
+
+
+def pifa_probe_mfma_random(iters: int = 20000, stream=None):
+    """(dense bf16 MFMA TFLOP/s, shader clock in MHz) of an MFMA-only kernel
+    whose operands change with every MFMA (random bf16 values)."""
+    tf, mhz = ctypes.c_double(), ctypes.c_double()
+    _check("pifa_probe_mfma_random", lib().pifa_probe_mfma_random(int(iters), ctypes.byref(tf), ctypes.byref(mhz),
+                                                                  _stream(stream)))
     return tf.value, mhz.value
 
 
