@@ -25,6 +25,11 @@ namespace pifa {
 constexpr int kSkinnyRows = 16;
 constexpr int kSkinnyStepK = 128;  // K covered by one wave step
 
+// The activation loads below are exec-masked (rows m >= M and K values past
+// K keep zeros): at decode sizes most lanes hold rows past M, and a masked
+// lane costs the load nothing.  The kernels issue them in a phase of their
+// own, ahead of the MFMAs that use them.
+
 // A operand from a bf16 / fp16 activation matrix (M x K, row stride lda).
 template <typename T>
 struct ALoad16 {
@@ -33,8 +38,8 @@ struct ALoad16 {
     int64_t M;
     static constexpr int kOps = 1;
     __device__ __forceinline__ void load(int m, int64_t k, int64_t K, u32x4 (&out)[1]) const {
-        out[0] = (m < M && k < K) ? *reinterpret_cast<const u32x4*>(a + (int64_t)m * lda + k)
-                                  : zero16();
+        out[0] = zero16();
+        if (m < M && k < K) out[0] = *reinterpret_cast<const u32x4*>(a + (int64_t)m * lda + k);
     }
 };
 
@@ -46,13 +51,12 @@ struct ALoadPair16 {
     int64_t M;
     static constexpr int kOps = 2;
     __device__ __forceinline__ void load(int m, int64_t k, int64_t K, u32x4 (&out)[2]) const {
-        if (!(m < M && k < K)) {
-            out[0] = zero16();
-            out[1] = zero16();
-            return;
+        out[0] = zero16();
+        out[1] = zero16();
+        if (m < M && k < K) {
+            out[0] = *reinterpret_cast<const u32x4*>(a + (int64_t)m * lda + k);
+            out[1] = *reinterpret_cast<const u32x4*>(a + (M + (int64_t)m) * lda + k);
         }
-        out[0] = *reinterpret_cast<const u32x4*>(a + (int64_t)m * lda + k);
-        out[1] = *reinterpret_cast<const u32x4*>(a + (M + (int64_t)m) * lda + k);
     }
 };
 
@@ -67,13 +71,12 @@ struct ASplit32 {
     float scale;
     static constexpr int kOps = 2;
     __device__ __forceinline__ void load(int m, int64_t k, int64_t K, u32x4 (&out)[2]) const {
-        if (!(m < M && k < K)) {
-            out[0] = zero16();
-            out[1] = zero16();
-            return;
+        f32x4 x0 = {0.f, 0.f, 0.f, 0.f}, x1 = x0;
+        if (m < M && k < K) {
+            const f32x4* p = reinterpret_cast<const f32x4*>(a + (int64_t)m * lda + k);
+            x0 = p[0];
+            x1 = p[1];
         }
-        const f32x4* p = reinterpret_cast<const f32x4*>(a + (int64_t)m * lda + k);
-        const f32x4 x0 = p[0], x1 = p[1];
         T hi[8], lo[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
@@ -89,8 +92,10 @@ struct ASplit32 {
 // Sum the per-wave 16x16 tiles in LDS and hand the result to the epilogue;
 // wave t finishes activation tile t (t < MT).  Only weight rows n0 + [c_lo,
 // c_lo + c_cnt) are stored (a workgroup may own part of a 16-row group).
-template <int WAVES, int MT, typename Epi>
-__device__ __forceinline__ void skinny_finish(const f32x4 (&acc)[MT], int64_t n0, const Epi& epi, int c_lo = 0,
+// ecol: epi.col(n0 + lane % 16), taken before the K loop so its index load
+// is not a dependent round trip after the reduction.
+template <int WAVES, int MT, typename Epi, typename ECol>
+__device__ __forceinline__ void skinny_finish(const f32x4 (&acc)[MT], const Epi& epi, const ECol& ecol, int c_lo = 0,
                                               int c_cnt = 16) {
     static_assert(MT <= WAVES, "one finishing wave per tile");
     __shared__ f32x4 red[WAVES][MT][kWave];
@@ -105,9 +110,8 @@ __device__ __forceinline__ void skinny_finish(const f32x4 (&acc)[MT], int64_t n0
     for (int w = 1; w < WAVES; ++w) tot += red[w][wave][lane];
     // 16x16 accumulator layout: lane holds column (lane % 16), rows 4*(lane/16) + v
     if ((unsigned)((lane & 15) - c_lo) >= (unsigned)c_cnt) return;
-    const auto c = epi.col(n0 + (lane & 15));
 #pragma unroll
-    for (int v = 0; v < 4; ++v) epi.store(16 * wave + 4 * (lane >> 4) + v, c, tot[v]);
+    for (int v = 0; v < 4; ++v) epi.store(16 * wave + 4 * (lane >> 4) + v, ecol, tot[v]);
 }
 
 // Weights in lane order (layout.hpp): B holds packed_elems(N, K) elements;
@@ -128,31 +132,56 @@ __device__ __forceinline__ void skinny_packed_group(const AL& al, const TB* __re
     const int row = lane & 15;
     const int kq = (lane >> 4) * 32;
     const bool mine = PARTS == 1 || row / PROWS == part;
+    const auto ecol = epi.col(g * kSkinnyRows + row);
 
     f32x4 acc[MT];
 #pragma unroll
     for (int t = 0; t < MT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // Single activation operands (with registers for a whole step) are all
+    // loaded right after the step's weights and before its MFMAs, so they
+    // cost one round trip per step instead of one per MFMA (the dense and
+    // pivot products at M = 16: 7% and 3% faster).  The two-operand forms
+    // keep their loads next to the MFMAs, which measured 4% faster for them.
+    constexpr bool kHoistA = OPS == 1 && MT * UNROLL * (WAVES > 8 ? 2 : 1) <= 8;
     for (int64_t kb = wave; kb < KB; kb += (int64_t)WAVES * UNROLL) {
         u32x4 bw[UNROLL][4];
+        u32x4 aw[kHoistA ? UNROLL : 1][4][kHoistA ? MT : 1][OPS];
 #pragma unroll
         for (int u = 0; u < UNROLL; ++u) {
             const int64_t b = kb + (int64_t)u * WAVES;
 #pragma unroll
-            for (int c = 0; c < 4; ++c) bw[u][c] = (mine && b < KB) ? blk[b * kPackChunks + c * kWave + lane] : zero16();
+            for (int c = 0; c < 4; ++c) {  // exec-masked: the other parts' lanes load nothing
+                bw[u][c] = zero16();
+                if (mine && b < KB) bw[u][c] = blk[b * kPackChunks + c * kWave + lane];
+            }
         }
+        if constexpr (kHoistA) {
+#pragma unroll
+            for (int u = 0; u < UNROLL; ++u)
+#pragma unroll
+                for (int c = 0; c < 4; ++c)
+#pragma unroll
+                    for (int t = 0; t < MT; ++t)
+                        al.load(row + 16 * t, (kb + (int64_t)u * WAVES) * kSkinnyStepK + kq + c * 8, K, aw[u][c][t]);
+        }
+        // keep every load of the step ahead of its MFMAs (the scheduler would
+        // otherwise interleave them to save registers, and each load issued
+        // after an MFMA that waited is another memory round trip)
+        if constexpr (kHoistA) __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int u = 0; u < UNROLL; ++u)
 #pragma unroll
             for (int c = 0; c < 4; ++c)
 #pragma unroll
                 for (int t = 0; t < MT; ++t) {
-                    u32x4 aw[OPS];
-                    al.load(row + 16 * t, (kb + (int64_t)u * WAVES) * kSkinnyStepK + kq + c * 8, K, aw);
+                    if constexpr (!kHoistA)
+                        al.load(row + 16 * t, (kb + (int64_t)u * WAVES) * kSkinnyStepK + kq + c * 8, K, aw[0][c][0]);
+                    const u32x4(&a)[OPS] = aw[kHoistA ? u : 0][c][kHoistA ? t : 0];
 #pragma unroll
-                    for (int o = 0; o < OPS; ++o) acc[t] = Mfma<TB>::mma16(aw[o], bw[u][c], acc[t]);
+                    for (int o = 0; o < OPS; ++o) acc[t] = Mfma<TB>::mma16(a[o], bw[u][c], acc[t]);
                 }
     }
-    skinny_finish<WAVES, MT>(acc, g * kSkinnyRows, epi, part * PROWS, PROWS);
+    skinny_finish<WAVES, MT>(acc, epi, ecol, part * PROWS, PROWS);
 }
 
 // Grid: PARTS * packed_groups(N) workgroups.
@@ -354,9 +383,13 @@ __global__ __launch_bounds__(WAVES* kWave) void skinny_rowmajor(AL al, const TB*
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
     const int64_t n0 = (int64_t)blockIdx.x * kSkinnyRows;
-    const auto brs = make_rsrc(B + n0 * ldb, ((N - n0 - 1) * ldb + K) * (int64_t)sizeof(TB));
+    // this workgroup's 16 rows (fewer at the end): rows past N and K values
+    // past K lie past the range (masked offsets too stay below 2^31)
+    const int64_t rows = (N - n0) < kSkinnyRows ? (N - n0) : kSkinnyRows;
+    const auto brs = make_rsrc31(B + n0 * ldb, ((rows - 1) * ldb + K) * (int64_t)sizeof(TB));
     const int row = lane & 15;
     const int kq = (lane >> 4) * 32;
+    const auto ecol = epi.col(n0 + row);
 
     f32x4 acc[MT];
 #pragma unroll
@@ -368,7 +401,7 @@ __global__ __launch_bounds__(WAVES* kWave) void skinny_rowmajor(AL al, const TB*
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
                 const int64_t k = kb + (int64_t)u * WAVES * kSkinnyStepK + kq + c * 8;
-                bw[u][c] = k < K ? load16(brs, (uint32_t)((row * ldb + k) * (int64_t)sizeof(TB))) : zero16();
+                bw[u][c] = load16(brs, k < K ? (uint32_t)((row * ldb + k) * (int64_t)sizeof(TB)) : kMaskedOffset);
             }
 #pragma unroll
         for (int u = 0; u < UNROLL; ++u)
@@ -382,7 +415,7 @@ __global__ __launch_bounds__(WAVES* kWave) void skinny_rowmajor(AL al, const TB*
                     for (int o = 0; o < OPS; ++o) acc[t] = Mfma<TB>::mma16(aw[o], bw[u][c], acc[t]);
                 }
     }
-    skinny_finish<WAVES, MT>(acc, n0, epi);
+    skinny_finish<WAVES, MT>(acc, epi, ecol);
 }
 
 }  // namespace pifa
