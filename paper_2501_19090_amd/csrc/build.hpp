@@ -20,9 +20,41 @@ namespace pifa {
 
 constexpr int kBuildThreads = 1024;
 
-__device__ __forceinline__ double wave_sum(double v) {
-    for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off);
-    return v;
+// Cross-lane moves on the VALU (DPP) instead of the LDS crossbar that
+// __shfl_xor uses.  dpp<CTRL, ROWS>(x, old): lane l gets x from the lane CTRL
+// names; lanes of rows outside the ROWS mask get old.  Controls used:
+// quad_perm [1,0,3,2] (0xB1) and [2,3,0,1] (0x4E), row_ror:4 (0x124) and
+// :8 (0x128), row_bcast:15 (0x142) and :31 (0x143).
+template <int CTRL, int ROWS = 0xF>
+__device__ __forceinline__ uint32_t dpp32(uint32_t x, uint32_t old) {
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)x, CTRL, ROWS, 0xF, false);
+}
+template <int CTRL, int ROWS = 0xF>
+__device__ __forceinline__ double dpp64(double x, double old) {
+    const uint2 u = __builtin_bit_cast(uint2, x), o = __builtin_bit_cast(uint2, old);
+    const uint2 r = {dpp32<CTRL, ROWS>(u.x, o.x), dpp32<CTRL, ROWS>(u.y, o.y)};
+    return __builtin_bit_cast(double, r);
+}
+__device__ __forceinline__ double lane63(double x) {
+    const uint2 u = __builtin_bit_cast(uint2, x);
+    const uint2 r = {(uint32_t)__builtin_amdgcn_readlane((int)u.x, 63), (uint32_t)__builtin_amdgcn_readlane((int)u.y, 63)};
+    return __builtin_bit_cast(double, r);
+}
+
+// The sum of x over the wave's 64 lanes (every lane active), returned to
+// every lane: a butterfly within each quad and each row of 16 lanes, then the
+// rows folded into lane 63.  A fixed order, so the result is deterministic,
+// and equal inputs give equal sums.  (About 4x faster than the same
+// reduction through __shfl_xor, which moves doubles through the LDS
+// crossbar: the 17 sums of a pivot step took 22 K of its 49 K cycles.)
+__device__ __forceinline__ double wave_sum(double x) {
+    x += dpp64<0xB1>(x, 0.0);
+    x += dpp64<0x4E>(x, 0.0);
+    x += dpp64<0x124>(x, 0.0);
+    x += dpp64<0x128>(x, 0.0);
+    x += dpp64<0x142, 0xA>(x, 0.0);  // rows 1 and 3 add rows 0 and 2
+    x += dpp64<0x143, 0xC>(x, 0.0);  // rows 2 and 3 add rows 0 + 1
+    return lane63(x);
 }
 
 // A (d_out columns of length d_in) = W' rows; norm2[j] = ||A_j||^2; perm[j] = j.
@@ -64,6 +96,69 @@ __global__ __launch_bounds__(256) void qr_init(const double* __restrict__ W, dou
 // step.
 constexpr int kPanel = 16;
 
+// The pivot of step k, for a workgroup of kBuildThreads threads (all of them
+// call it): the column c in [k, d_out) of largest norm2[c], ties to the
+// lowest original index perm[c].  The comparison is a total order, so the
+// result is exact whatever the reduction order.
+__device__ __forceinline__ int64_t block_pivot(const double* __restrict__ norm2, const int32_t* __restrict__ perm,
+                                               int64_t k, int64_t d_out, double* s_val, int64_t* s_idx,
+                                               int32_t* s_key) {
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    double bv = -1.0;
+    int64_t bi = -1;
+    int32_t bk = INT32_MAX;
+    for (int64_t c = k + tid; c < d_out; c += kBuildThreads) {
+        const double v = norm2[c];
+        const int32_t key = perm[c];
+        if (v > bv || (v == bv && key < bk)) {
+            bv = v;
+            bi = c;
+            bk = key;
+        }
+    }
+    {   // the wave's best (value, key, index), on the VALU; a total order
+        // (larger value, then smaller key), so the result is exact
+        int32_t bi32 = (int32_t)bi;
+        auto take = [&](double ov, int32_t ok, int32_t oi) {
+            if (ov > bv || (ov == bv && ok < bk)) {
+                bv = ov;
+                bk = ok;
+                bi32 = oi;
+            }
+        };
+#define PIFA_ARGMAX_STEP(CTRL, ROWS)                                                                 \
+    take(dpp64<CTRL, ROWS>(bv, bv), (int32_t)dpp32<CTRL, ROWS>((uint32_t)bk, (uint32_t)bk), \
+         (int32_t)dpp32<CTRL, ROWS>((uint32_t)bi32, (uint32_t)bi32))
+        PIFA_ARGMAX_STEP(0xB1, 0xF);
+        PIFA_ARGMAX_STEP(0x4E, 0xF);
+        PIFA_ARGMAX_STEP(0x124, 0xF);
+        PIFA_ARGMAX_STEP(0x128, 0xF);
+        PIFA_ARGMAX_STEP(0x142, 0xA);
+        PIFA_ARGMAX_STEP(0x143, 0xC);
+#undef PIFA_ARGMAX_STEP
+        bv = lane63(bv);
+        bk = __builtin_amdgcn_readlane(bk, 63);
+        bi = (int64_t)__builtin_amdgcn_readlane(bi32, 63);
+    }
+    if (lane == 0) {
+        s_val[wave] = bv;
+        s_idx[wave] = bi;
+        s_key[wave] = bk;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        for (int w = 1; w < kBuildThreads / kWave; ++w)
+            if (s_val[w] > bv || (s_val[w] == bv && s_key[w] < bk)) {
+                bv = s_val[w];
+                bi = s_idx[w];
+                bk = s_key[w];
+            }
+        s_idx[0] = bi;
+    }
+    __syncthreads();
+    return s_idx[0];
+}
+
 // Step k = k0 + j, part 1 (a single workgroup of kBuildThreads threads):
 //   * pivot: the column of largest (downdated) residual norm, ties to the
 //     lowest original index; swap it into position k (A columns, F rows,
@@ -85,46 +180,7 @@ __global__ __launch_bounds__(kBuildThreads) void qr_panel_pivot(double* __restri
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
     const int j = (int)(k - k0);
 
-    // argmax of norm2[k..d_out), ties to the lowest original index perm[]
-    double bv = -1.0;
-    int64_t bi = -1;
-    int32_t bk = INT32_MAX;
-    for (int64_t c = k + tid; c < d_out; c += kBuildThreads) {
-        const double v = norm2[c];
-        const int32_t key = perm[c];
-        if (v > bv || (v == bv && key < bk)) {
-            bv = v;
-            bi = c;
-            bk = key;
-        }
-    }
-    for (int off = kWave / 2; off > 0; off >>= 1) {
-        const double ov = __shfl_xor(bv, off);
-        const int64_t oi = __shfl_xor(bi, off);
-        const int32_t ok = __shfl_xor(bk, off);
-        if (ov > bv || (ov == bv && ok < bk)) {
-            bv = ov;
-            bi = oi;
-            bk = ok;
-        }
-    }
-    if (lane == 0) {
-        s_val[wave] = bv;
-        s_idx[wave] = bi;
-        s_key[wave] = bk;
-    }
-    __syncthreads();
-    if (tid == 0) {
-        for (int w = 1; w < kBuildThreads / kWave; ++w)
-            if (s_val[w] > bv || (s_val[w] == bv && s_key[w] < bk)) {
-                bv = s_val[w];
-                bi = s_idx[w];
-                bk = s_key[w];
-            }
-        s_idx[0] = bi;
-    }
-    __syncthreads();
-    const int64_t p = s_idx[0];
+    const int64_t p = block_pivot(norm2, perm, k, d_out, s_val, s_idx, s_key);
 
     // swap columns k and p, with their F rows, norms and original indices
     if (p != k) {
@@ -219,6 +275,126 @@ __global__ __launch_bounds__(kBuildThreads) void qr_panel_pivot(double* __restri
     }
 }
 
+// qr_panel_pivot with fewer dependent memory round trips, for columns of at
+// most kPivotLdsRows rows (longer columns take qr_panel_pivot): the pivot
+// column is read where it is (position p) in the same pass that moves the old
+// column k there and brings the pivot column up to date; the updated rows
+// wait in LDS (dynamic, (d_in - k) doubles) until they are scaled into the
+// reflector, and alpha = x[k] is read from there.  The arithmetic and its
+// order are those of qr_panel_pivot, so the results are bit-identical.
+// (64 KB of dynamic LDS at most.)
+constexpr int64_t kPivotLdsRows = 8192;
+
+__global__ __launch_bounds__(kBuildThreads) void qr_panel_pivot_lds(double* __restrict__ A, double* __restrict__ norm2,
+                                                                    int32_t* __restrict__ perm, double* __restrict__ F,
+                                                                    double* __restrict__ tau, double* __restrict__ aux,
+                                                                    int* __restrict__ status, int64_t k, int64_t k0,
+                                                                    int64_t d_out, int64_t d_in) {
+    __shared__ double s_val[kBuildThreads / kWave];
+    __shared__ int64_t s_idx[kBuildThreads / kWave];
+    __shared__ int32_t s_key[kBuildThreads / kWave];
+    __shared__ double fk[kPanel];
+    extern __shared__ double pcol[];  // rows [k, d_in) of the updated pivot column
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    const int j = (int)(k - k0);
+
+    const int64_t p = block_pivot(norm2, perm, k, d_out, s_val, s_idx, s_key);
+
+    // columns k and p trade F rows, norms and original indices; fk is the
+    // pivot column's F row
+    if (tid < kPanel) {
+        const double fp = tid < j ? F[p * kPanel + tid] : 0.0;
+        fk[tid] = fp;
+        if (p != k && tid < j) {
+            const double fo = F[k * kPanel + tid];
+            F[k * kPanel + tid] = fp;
+            F[p * kPanel + tid] = fo;
+        }
+    }
+    if (tid == 0 && p != k) {
+        const int32_t tp = perm[k];
+        perm[k] = perm[p];
+        perm[p] = tp;
+        const double tn = norm2[k];
+        norm2[k] = norm2[p];
+        norm2[p] = tn;
+    }
+    double* x = A + k * d_in;
+    double* ap = A + p * d_in;
+    if (p != k) {  // rows above k (entries of R) swap as they are
+        for (int64_t i = tid; i < k; i += kBuildThreads) {
+            const double t = x[i];
+            x[i] = ap[i];
+            ap[i] = t;
+        }
+    }
+    __syncthreads();  // fk
+
+    // one pass over rows [k, d_in): the pivot column after the panel's
+    // reflections, x[i] = a_p[i] - V[i, 0:j] fk (to LDS), its squared norm
+    // and dot[t] = sum_{i > k} V[i, t] x[i]; the old column k moves to p
+    double s = 0.0;
+    double dot[kPanel];
+#pragma unroll
+    for (int t = 0; t < kPanel; ++t) dot[t] = 0.0;
+    for (int64_t i = k + tid; i < d_in; i += kBuildThreads) {
+        double vrow[kPanel];
+#pragma unroll
+        for (int t = 0; t < kPanel; ++t) vrow[t] = t < j ? A[(k0 + t) * d_in + i] : 0.0;
+        double v = ap[i];
+        if (p != k) ap[i] = x[i];
+#pragma unroll
+        for (int t = 0; t < kPanel; ++t) v -= vrow[t] * fk[t];  // zero past j
+        pcol[i - k] = v;
+        s += v * v;
+        if (i > k) {
+#pragma unroll
+            for (int t = 0; t < kPanel; ++t) dot[t] += vrow[t] * v;
+        }
+    }
+    __shared__ double s_dot[kBuildThreads / kWave][kPanel + 1];
+    s = wave_sum(s);
+#pragma unroll
+    for (int t = 0; t < kPanel; ++t) {
+        const double d = wave_sum(dot[t]);
+        if (lane == 0) s_dot[wave][t] = d;
+    }
+    if (lane == 0) s_val[wave] = s;
+    __syncthreads();
+    if (tid == 0) {
+        double t = 0.0;
+        for (int w = 0; w < kBuildThreads / kWave; ++w) t += s_val[w];
+        s_val[0] = t;
+    }
+    if (tid < j) {
+        double d = 0.0;
+        for (int w = 0; w < kBuildThreads / kWave; ++w) d += s_dot[w][tid];
+        s_dot[0][tid] = d;
+    }
+    __syncthreads();
+    const double xnorm = sqrt(s_val[0]);
+    const double alpha = pcol[0];
+    if (xnorm == 0.0) {
+        for (int64_t i = k + tid; i < d_in; i += kBuildThreads) x[i] = pcol[i - k];
+        if (tid == 0) {
+            status[0] = 1;
+            tau[k] = 0.0;
+        }
+        if (tid < j) aux[tid] = 0.0;
+        return;
+    }
+    const double beta = -copysign(xnorm, alpha);
+    const double tk = (beta - alpha) / beta;
+    const double inv = 1.0 / (alpha - beta);
+    for (int64_t i = k + 1 + tid; i < d_in; i += kBuildThreads) x[i] = pcol[i - k] * inv;
+    // aux[t] = -tau_k V[k:, t]^T v_k = -tau_k (V[k, t] + inv * dot[t]), v_k[k] = 1
+    if (tid < j) aux[tid] = -tk * (A[(k0 + tid) * d_in + k] + inv * s_dot[0][tid]);
+    if (tid == 0) {
+        x[k] = beta;
+        tau[k] = tk;
+    }
+}
+
 // Step k = k0 + j, part 2: one wave per trailing column c > k, read only
 // except for three values per column:
 //   F[c, j]  = tau_k a_c^T v_k + F[c, 0:j] aux[0:j]  (a_c as of the panel start)
@@ -234,15 +410,41 @@ __global__ __launch_bounds__(256) void qr_panel_gemv(double* __restrict__ A, dou
     const int j = (int)(k - k0);
     const double* v = A + k * d_in;  // v[k] = 1 (implicit), v[k+1:] stored
     double* a = A + c * d_in;
-    double d = 0.0, d2 = 0.0;
-    int64_t i = k + 1 + lane;
-    for (; i + kWave < d_in; i += 2 * kWave) {
-        d += v[i] * a[i];
-        d2 += v[i + kWave] * a[i + kWave];
+    double d;
+    if ((d_in & 1) == 0) {
+        // 16-byte loads of rows [s2, d_in), s2 = k + 1 rounded up to even,
+        // four pairs in flight per lane (clamped indices, masked products: no
+        // branch per load); row k + 1 on its own when it is odd.  The order
+        // depends only on k, so equal columns give equal sums.
+        const int64_t s = k + 1, s2 = s + (s & 1), n2 = d_in / 2;
+        const double2* v2 = reinterpret_cast<const double2*>(v);
+        const double2* a2 = reinterpret_cast<const double2*>(a);
+        double acc[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
+        for (int64_t q = s2 / 2 + lane; q < n2; q += 4 * kWave) {
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int64_t qu = q + u * kWave;
+                const bool ok = qu < n2;
+                const int64_t qc = ok ? qu : n2 - 1;
+                const double2 vv = v2[qc], aa = a2[qc];
+                acc[2 * u] += ok ? vv.x * aa.x : 0.0;
+                acc[2 * u + 1] += ok ? vv.y * aa.y : 0.0;
+            }
+        }
+        d = ((acc[0] + acc[1]) + (acc[2] + acc[3])) + ((acc[4] + acc[5]) + (acc[6] + acc[7]));
+        if (lane == 0 && (s & 1) && s < d_in) d += v[s] * a[s];
+    } else {
+        double d1 = 0.0, d2 = 0.0;
+        int64_t i = k + 1 + lane;
+        for (; i + kWave < d_in; i += 2 * kWave) {
+            d1 += v[i] * a[i];
+            d2 += v[i + kWave] * a[i + kWave];
+        }
+        if (i < d_in) d1 += v[i] * a[i];
+        d = d1 + d2;
     }
-    if (i < d_in) d += v[i] * a[i];
     const double akc = a[k];
-    d = wave_sum(d + d2) + akc;
+    d = wave_sum(d) + akc;
     double* Fc = F + c * kPanel;
     double corr = 0.0, row = 0.0;
     if (lane < j) {
@@ -292,93 +494,52 @@ __global__ void extract_r11(const double* __restrict__ A, double* __restrict__ R
 
 // C (n_np x r) with C R11^T = R12^T, i.e. for each row q of C:
 //   sum_{t >= s} R11[s][t] c[t] = b[s],  b[s] = A_{r+q}[s]   (s < r),
-// solved from the last unknown up in blocks of 64.  Workgroup = 64 rows of
-// C, 256 threads; for each block: b' = b - C[:, after] R11[block, after]^T
-// (4 x 4 outputs per thread through LDS), then a 64 x 64 triangular solve.
-constexpr int kSolveRows = 64;
+// solved from the last unknown up in blocks of kSolveBlock unknowns,
+// right-looking: X = the right-hand sides (coeff_rhs); for each block, from
+// the last, coeff_block_solve finds the block's unknowns of every row by
+// substitution against R11's diagonal block, and one fp64 MFMA GEMM (gemm64)
+// subtracts their contribution from the right-hand sides of all earlier
+// unknowns.  The GEMMs carry the n_np r^2 FLOPs over the whole chip, where a
+// left-looking solve with one workgroup per 64 rows of C kept n_np / 64
+// workgroups busy (32 at 4096 x 4096, r = 2048).
 constexpr int kSolveBlock = 64;
-constexpr int kSolveK = 16;
 
-__global__ __launch_bounds__(256) void coeff_solve(const double* __restrict__ A,
-                                                   const double* __restrict__ RT,
-                                                   double* __restrict__ C, int64_t r, int64_t n_np,
-                                                   int64_t d_in) {
-    __shared__ double sC[kSolveK][kSolveRows + 1];
-    __shared__ double sR[kSolveK][kSolveBlock + 1];
-    __shared__ double sB[kSolveRows][kSolveBlock + 1];
+__global__ void coeff_rhs(const double* __restrict__ A, double* __restrict__ X, int64_t r, int64_t n_np,
+                          int64_t d_in) {
+    const int64_t total = n_np * r;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t q = e / r, s = e % r;
+        X[e] = A[(r + q) * d_in + s];
+    }
+}
+
+// Unknowns [s0, s0 + nb) of rows [64 b, 64 b + 64) of X, in place: thread t
+// substitutes row 64 b + t against the diagonal block of R11 (upper
+// triangular, row-major in RT with row stride r).
+__global__ __launch_bounds__(kSolveBlock) void coeff_block_solve(const double* __restrict__ RT, double* __restrict__ X,
+                                                                  int64_t r, int64_t n_np, int64_t s0, int nb) {
     __shared__ double sD[kSolveBlock][kSolveBlock + 1];
+    __shared__ double sB[kSolveBlock][kSolveBlock + 1];
     const int tid = threadIdx.x;
-    const int tx = tid % 16, ty = tid / 16;  // 4 x 4 outputs: rows ty*4.., cols tx*4..
-    const int64_t q0 = (int64_t)blockIdx.x * kSolveRows;
-
-    const int64_t nblk = ceil_div(r, kSolveBlock);
-    for (int64_t blk = nblk - 1; blk >= 0; --blk) {
-        const int64_t s0 = blk * kSolveBlock;
-        const int64_t s1 = (s0 + kSolveBlock) < r ? (s0 + kSolveBlock) : r;
-        const int nb = (int)(s1 - s0);
-        // right-hand sides b[q][s] = A_{r+q}[s]
-        double acc[4][4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int jj = 0; jj < 4; ++jj) acc[i][jj] = 0.0;
-        // acc[q][s] = sum_{t >= s1} C[q][t] * R11[s][t]
-        for (int64_t t0 = s1; t0 < r; t0 += kSolveK) {
-            for (int e = tid; e < kSolveK * kSolveRows; e += 256) {
-                const int kk = e % kSolveK, row = e / kSolveK;
-                const int64_t q = q0 + row, t = t0 + kk;
-                sC[kk][row] = (q < n_np && t < r) ? C[q * r + t] : 0.0;
-            }
-            for (int e = tid; e < kSolveK * kSolveBlock; e += 256) {
-                const int kk = e % kSolveK, col = e / kSolveK;
-                const int64_t s = s0 + col, t = t0 + kk;
-                sR[kk][col] = (s < s1 && t < r) ? RT[s * r + t] : 0.0;
-            }
-            __syncthreads();
-#pragma unroll
-            for (int kk = 0; kk < kSolveK; ++kk) {
-                double a[4], b[4];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) a[i] = sC[kk][ty * 4 + i];
-#pragma unroll
-                for (int jj = 0; jj < 4; ++jj) b[jj] = sR[kk][tx * 4 + jj];
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-#pragma unroll
-                    for (int jj = 0; jj < 4; ++jj) acc[i][jj] = fma(a[i], b[jj], acc[i][jj]);
-            }
-            __syncthreads();
-        }
-        // b' = b - acc into LDS, plus the diagonal block of R11
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int jj = 0; jj < 4; ++jj) {
-                const int row = ty * 4 + i, col = tx * 4 + jj;
-                const int64_t q = q0 + row, s = s0 + col;
-                sB[row][col] = (q < n_np && s < s1) ? A[(r + q) * d_in + s] - acc[i][jj] : 0.0;
-            }
-        for (int e = tid; e < kSolveBlock * kSolveBlock; e += 256) {
-            const int a = e / kSolveBlock, b = e % kSolveBlock;
-            sD[a][b] = (a < nb && b < nb) ? RT[(s0 + a) * r + s0 + b] : 0.0;
-        }
-        __syncthreads();
-        // back substitution inside the block: thread `row` owns one row of C
-        if (tid < kSolveRows) {
-            const int row = tid;
-            for (int a = nb - 1; a >= 0; --a) {
-                double v = sB[row][a];
-                for (int b = a + 1; b < nb; ++b) v -= sD[a][b] * sB[row][b];
-                sB[row][a] = v / sD[a][a];
-            }
-        }
-        __syncthreads();
-        for (int e = tid; e < kSolveRows * kSolveBlock; e += 256) {
-            const int row = e / kSolveBlock, col = e % kSolveBlock;
-            const int64_t q = q0 + row, s = s0 + col;
-            if (q < n_np && s < s1) C[q * r + s] = sB[row][col];
-        }
-        __syncthreads();
+    const int64_t q0 = (int64_t)blockIdx.x * kSolveBlock;
+    for (int e = tid; e < kSolveBlock * kSolveBlock; e += kSolveBlock) {
+        const int a = e / kSolveBlock, b = e % kSolveBlock;
+        sD[a][b] = (a < nb && b < nb) ? RT[(s0 + a) * r + s0 + b] : 0.0;
+        const int64_t q = q0 + a;
+        sB[a][b] = (q < n_np && b < nb) ? X[q * r + s0 + b] : 0.0;
+    }
+    __syncthreads();
+    for (int a = nb - 1; a >= 0; --a) {
+        double v = sB[tid][a];
+        for (int b = a + 1; b < nb; ++b) v -= sD[a][b] * sB[tid][b];
+        sB[tid][a] = v / sD[a][a];
+    }
+    __syncthreads();
+    for (int e = tid; e < kSolveBlock * kSolveBlock; e += kSolveBlock) {
+        const int row = e / kSolveBlock, col = e % kSolveBlock;
+        const int64_t q = q0 + row;
+        if (q < n_np && col < nb) X[q * r + s0 + col] = sB[row][col];
     }
 }
 

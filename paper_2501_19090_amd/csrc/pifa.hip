@@ -1909,8 +1909,14 @@ pifa_status pifa_build_f64(const double* W, pifa_dims dims, double* W_p, double*
     for (int64_t k0 = 0; k0 < r; k0 += kPanel) {
         const int64_t nb = std::min<int64_t>(kPanel, r - k0);
         for (int64_t k = k0; k < k0 + nb; ++k) {
-            hipLaunchKernelGGL(qr_panel_pivot, dim3(1), dim3(kBuildThreads), 0, st, dA, dn, dperm, dF,
-                               (double*)tau.p, (double*)aux.p, (int*)status.p, k, k0, d_out, d_in);
+            // columns of up to kPivotLdsRows rows keep the updated pivot
+            // column in LDS (fewer dependent memory round trips, bit-identical)
+            if (d_in <= kPivotLdsRows)
+                hipLaunchKernelGGL(qr_panel_pivot_lds, dim3(1), dim3(kBuildThreads), (size_t)(d_in - k) * 8, st, dA, dn,
+                                   dperm, dF, (double*)tau.p, (double*)aux.p, (int*)status.p, k, k0, d_out, d_in);
+            else
+                hipLaunchKernelGGL(qr_panel_pivot, dim3(1), dim3(kBuildThreads), 0, st, dA, dn, dperm, dF,
+                                   (double*)tau.p, (double*)aux.p, (int*)status.p, k, k0, d_out, d_in);
             if (k + 1 < d_out)
                 hipLaunchKernelGGL(qr_panel_gemv, dim3((unsigned)ceil_div(d_out - k - 1, 4)), dim3(256), 0, st, dA, dn,
                                    dF, (const double*)tau.p, (const double*)aux.p, k, k0, d_out, d_in);
@@ -1981,8 +1987,19 @@ pifa_status pifa_build_f64(const double* W, pifa_dims dims, double* W_p, double*
         if (!alloc(RT, (size_t)r * r * 8) || !alloc(Csel, (size_t)n_np * r * 8)) return PIFA_ERR_OOM;
         hipLaunchKernelGGL(extract_r11, dim3(grid_for(r * r)), dim3(256), 0, st, (const double*)dA, (double*)RT.p, r,
                            d_in);
-        hipLaunchKernelGGL(coeff_solve, dim3((unsigned)ceil_div(n_np, kSolveRows)), dim3(256), 0, st,
-                           (const double*)dA, (const double*)RT.p, (double*)Csel.p, r, n_np, d_in);
+        // C R11^T = R12^T, right-looking blocks of kSolveBlock unknowns (build.hpp)
+        double* X = (double*)Csel.p;
+        const double* R11 = (const double*)RT.p;
+        hipLaunchKernelGGL(coeff_rhs, dim3(grid_for(n_np * r)), dim3(256), 0, st, (const double*)dA, X, r, n_np, d_in);
+        for (int64_t s0 = (ceil_div(r, (int64_t)kSolveBlock) - 1) * kSolveBlock; s0 >= 0; s0 -= kSolveBlock) {
+            const int nb = (int)std::min<int64_t>(kSolveBlock, r - s0);
+            hipLaunchKernelGGL(coeff_block_solve, dim3((unsigned)ceil_div(n_np, (int64_t)kSolveBlock)),
+                               dim3(kSolveBlock), 0, st, R11, X, r, n_np, s0, nb);
+            // X[:, 0:s0] -= X[:, s0:s0+nb] R11[0:s0, s0:s0+nb]^T
+            if (s0 > 0 && gemm64_launch(st, n_np, s0, nb, -1.0, X + s0, r, 1, R11 + s0, 1, r, 1.0, X, r, 1) !=
+                              hipSuccess)
+                return PIFA_ERR_HIP;
+        }
         hipLaunchKernelGGL(gather_coeffs, dim3(grid_for(n_np * r)), dim3(256), 0, st, (const double*)Csel.p,
                            didx + r + n_np, didx + r + 2 * n_np, C, n_np, r);
     }

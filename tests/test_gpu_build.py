@@ -36,7 +36,9 @@ def _gpu_build(W, r):
 
 @pytest.mark.parametrize("d_out,d_in,r", [(64, 48, 16), (48, 64, 16), (96, 96, 1), (32, 48, 32), (256, 256, 128),
                                           (333, 200, 150), (1024, 1024, 512), (2752, 1024, 512),
-                                          (1024, 2752, 512), (4096, 4096, 2048)])
+                                          (1024, 2752, 512), (4096, 4096, 2048),
+                                          # columns longer than the LDS-held pivot column (8192 rows)
+                                          (96, 9000, 48), (40, 8193, 40)])
 def test_build_matches_oracle(d_out, d_in, r):
     U, V = inputs.lowrank_factors(d_out, d_in, r, seed=d_out + r)
     W = U @ V
