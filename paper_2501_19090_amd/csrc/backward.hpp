@@ -116,14 +116,23 @@ __global__ __launch_bounds__(256) void gather_tile(const bf16* __restrict__ in, 
             for (int e = 0; e < 8; ++e) tile[mm][j8 + e] = v[e];
         }
     } else {
+        // every load is unconditional (clamped row, a valid column): under a
+        // lane condition each would be a branch whose join waits for it, one
+        // memory round trip per element
         const int jj = tid % kTrTile;
         const int64_t j = j0 + jj;
         const int64_t cj = j < ncols ? (idx ? (int64_t)idx[j] : j) : 0;
+        constexpr int kPer = kTrTile * kTrTile / 256;
+        uint16_t v[kPer];
 #pragma unroll
-        for (int i = 0; i < kTrTile * kTrTile / 256; ++i) {
+        for (int i = 0; i < kPer; ++i) {
+            const int64_t m = m0 + tid / kTrTile + 4 * i;
+            v[i] = src[(m < M ? m : M - 1) * ld_in + cj];
+        }
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {
             const int mm = tid / kTrTile + 4 * i;
-            const int64_t m = m0 + mm;
-            tile[mm][jj] = (m < M && j < ncols) ? src[m * ld_in + cj] : (uint16_t)0;
+            tile[mm][jj] = (m0 + mm < M && j < ncols) ? v[i] : (uint16_t)0;
         }
     }
     __syncthreads();
