@@ -96,6 +96,21 @@ __global__ __launch_bounds__(256) void qr_init(const double* __restrict__ W, dou
 // step.
 constexpr int kPanel = 16;
 
+// One step of a wave argmax over (value v, key k, index i): take the partner
+// lane's triple (dpp64 / dpp32 with control CTRL, rows ROWS; lanes outside
+// ROWS see their own) if its value is larger, or equal with a smaller key.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ void argmax_step(double& v, int32_t& k, int32_t& i) {
+    const double ov = dpp64<CTRL, ROWS>(v, v);
+    const int32_t ok = (int32_t)dpp32<CTRL, ROWS>((uint32_t)k, (uint32_t)k);
+    const int32_t oi = (int32_t)dpp32<CTRL, ROWS>((uint32_t)i, (uint32_t)i);
+    if (ov > v || (ov == v && ok < k)) {
+        v = ov;
+        k = ok;
+        i = oi;
+    }
+}
+
 // The pivot of step k, for a workgroup of kBuildThreads threads (all of them
 // call it): the column c in [k, d_out) of largest norm2[c], ties to the
 // lowest original index perm[c].  The comparison is a total order, so the
@@ -119,23 +134,12 @@ __device__ __forceinline__ int64_t block_pivot(const double* __restrict__ norm2,
     {   // the wave's best (value, key, index), on the VALU; a total order
         // (larger value, then smaller key), so the result is exact
         int32_t bi32 = (int32_t)bi;
-        auto take = [&](double ov, int32_t ok, int32_t oi) {
-            if (ov > bv || (ov == bv && ok < bk)) {
-                bv = ov;
-                bk = ok;
-                bi32 = oi;
-            }
-        };
-#define PIFA_ARGMAX_STEP(CTRL, ROWS)                                                                 \
-    take(dpp64<CTRL, ROWS>(bv, bv), (int32_t)dpp32<CTRL, ROWS>((uint32_t)bk, (uint32_t)bk), \
-         (int32_t)dpp32<CTRL, ROWS>((uint32_t)bi32, (uint32_t)bi32))
-        PIFA_ARGMAX_STEP(0xB1, 0xF);
-        PIFA_ARGMAX_STEP(0x4E, 0xF);
-        PIFA_ARGMAX_STEP(0x124, 0xF);
-        PIFA_ARGMAX_STEP(0x128, 0xF);
-        PIFA_ARGMAX_STEP(0x142, 0xA);
-        PIFA_ARGMAX_STEP(0x143, 0xC);
-#undef PIFA_ARGMAX_STEP
+        argmax_step<0xB1, 0xF>(bv, bk, bi32);
+        argmax_step<0x4E, 0xF>(bv, bk, bi32);
+        argmax_step<0x124, 0xF>(bv, bk, bi32);
+        argmax_step<0x128, 0xF>(bv, bk, bi32);
+        argmax_step<0x142, 0xA>(bv, bk, bi32);
+        argmax_step<0x143, 0xC>(bv, bk, bi32);
         bv = lane63(bv);
         bk = __builtin_amdgcn_readlane(bk, 63);
         bi = (int64_t)__builtin_amdgcn_readlane(bi32, 63);
