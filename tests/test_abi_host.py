@@ -182,7 +182,8 @@ def test_gemm_plan_splits_small_batches():
     """Few rows: K is split, over 64 x 64 tiles up to 128 rows and over
     128 x 64 tiles above (half the splits 128 x 128 tiles would need for as
     many workgroups), with at most 16 splits and partials no larger than the
-    operands."""
+    operands; a product at most 2048 deep whose 64 x 64 tiles fill half the
+    chip or more is not split."""
     for M in (17, 64, 128, 256):
         tm, tn, s = pifa.pifa_gemm_plan(M, 2048, 4096)
         assert (tm, tn) == ((64, 64) if M <= 128 else (128, 64)) and 1 < s <= 16
@@ -192,6 +193,11 @@ def test_gemm_plan_splits_small_batches():
     assert pifa.pifa_gemm_plan(128, 2048, 4096) == (64, 64, 4)
     assert pifa.pifa_gemm_plan(128, 2048, 2048) == (64, 64, 4)
     assert pifa.pifa_gemm_plan(256, 2048, 4096) == (128, 64, 4)
+    # at most 2048 deep, with 64 x 64 tiles filling half the chip or more: no split
+    assert pifa.pifa_gemm_plan(256, 2048, 2048) == (64, 64, 1)
+    assert pifa.pifa_gemm_plan(512, 2048, 2048) == (64, 64, 1)
+    assert pifa.pifa_gemm_plan(256, 4096, 2048) == (64, 64, 1)
+    assert pifa.pifa_gemm_plan(192, 2048, 2048)[2] > 1
     # 64 x 64 tiles only while a split stays at most 1024 deep: the dense
     # 4096^2 product at M = 128 keeps 128 x 64 tiles
     assert pifa.pifa_gemm_plan(128, 4096, 4096) == (128, 64, 4)
