@@ -109,6 +109,24 @@ class Workload:
         self.uv_h = [self._new_uv()]
         self.dense_h = [self._new_dense()]
 
+    def warm_build_ms(self):
+        """Times a second pifa_build_f64 of the same W' in this process (the
+        first call also pays one-time costs: code-object loading, first device
+        allocations); returns (ms, whether it selected the same pivot set)."""
+        torch, pifa = self.torch, self.pifa
+        from paper_2501_19090_amd import inputs
+        U, V = inputs.lowrank_factors(self.d_out, self.d_in, self.r, self.seed)
+        W64 = torch.from_numpy(U @ V).to("cuda:0")
+        del U, V
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        piv, _, Wp, C, _ = pifa.pifa_build_f64(W64, self.r)
+        torch.cuda.synchronize()
+        ms = 1e3 * (time.perf_counter() - t0)
+        del W64, Wp, C
+        torch.cuda.empty_cache()
+        return ms, bool(np.array_equal(piv, self.piv))
+
     def _new_pifa(self):
         return self.pifa.pifa_layer_create(self.wp, self.c, self.piv, self.npiv, (self.d_in, self.d_out, self.r))
 
@@ -718,9 +736,12 @@ def main():
     log("reconstruct:", json.dumps(reconstruct))
     grouped = measure_group(inputs.config_seed(2))
     log("grouped:", json.dumps(grouped))
-    build = {"ms": wl.build_ms, "report": wl.build_report,
+    warm_ms, warm_same = wl.warm_build_ms()
+    build = {"ms": wl.build_ms, "ms_second_call": warm_ms, "second_call_same_pivots": warm_same,
+             "report": wl.build_report,
              "what": "pifa_build_f64 of the 4096x4096 rank-2048 W' on the GPU (fp64 QR with column pivoting "
-                     "+ coefficient solve)"}
+                     "+ coefficient solve); ms: the first call in the process (one-time costs included), "
+                     "ms_second_call: the same build again"}
     wl.close()
 
     out = {
