@@ -137,7 +137,8 @@ struct StagedEpi {
 // The pivot product's epilogue of a bf16 prefill: the pivot outputs go to
 // their columns of Y element by element (scatter), and the fp16 hand-off,
 // a contiguous M x ldws matrix, is staged in LDS and written with 16-byte
-// stores.  col / store serve the K-split reduction, element by element.
+// stores (on the 128-row tiles; the 256-row tiles take elementwise()).
+// col / store serve the K-split reduction, element by element.
 struct PivotHandoffEpi {
     static constexpr bool kDual = true;
     ScatterEpi<bf16, kWsNone> y;
@@ -152,9 +153,8 @@ struct PivotHandoffEpi {
         y.store(m, c.y, v);
         ws.store(m, c.ws, v);
     }
-    // the same outputs with the hand-off written element by element (for
-    // tiles whose registers cannot hold the staging on top of 128
-    // accumulators per lane)
+    // the same outputs with the hand-off written element by element (the
+    // 256-row tiles: faster there than staging it through LDS)
     __host__ ScatterEpi<bf16, kWsF16> elementwise() const {
         ScatterEpi<bf16, kWsF16> e;
         e.out = y.out;

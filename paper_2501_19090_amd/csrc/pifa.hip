@@ -330,12 +330,25 @@ hipError_t launch_gemm(int site, const T* A, int64_t lda, int64_t M, const T* B,
             hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 256, kGemmBK, 2, 4, BPACK, 1, Epi, KM>), grid, dim3(8 * kWave), 0,
                                st, A, lda, M, B, ldb, N, K, K, epi);
     } else if (g.bm == 256 && g.bn == 192) {
-        if constexpr (kWideOk)
+        // the 256-row tiles write the pivot product's fp16 hand-off element by
+        // element: staged through LDS it cost more than its stores save (M =
+        // 4096, three alternating passes, us per launch: attention layer,
+        // 256 x 128 tiles, 80.1-81.2 -> 76.3-76.4; r = 70% of 4096, 256 x 192
+        // tiles, 103.9-104.2 -> 100.0-100.4).  The 128-row tiles keep it
+        // staged (1-2 us faster there).
+        if constexpr (DualEpiT<Epi>::value)
+            hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 192, kGemmBK, 4, 2, BPACK, 2, ScatterEpi<bf16, kWsF16>, KM>), grid,
+                               dim3(8 * kWave), 0, st, A, lda, M, B, ldb, N, K, K, epi.elementwise());
+        else if constexpr (kWideOk)
             hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 192, kGemmBK, 4, 2, BPACK, 2, Epi, KM>), grid, dim3(8 * kWave), 0,
                                st, A, lda, M, B, ldb, N, K, K, epi);
     } else if (g.bm == 256) {
-        hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 128, kGemmBK, 4, 2, BPACK, 2, Epi, KM>), grid, dim3(8 * kWave), 0, st,
-                           A, lda, M, B, ldb, N, K, K, epi);
+        if constexpr (DualEpiT<Epi>::value)
+            hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 128, kGemmBK, 4, 2, BPACK, 2, ScatterEpi<bf16, kWsF16>, KM>), grid,
+                               dim3(8 * kWave), 0, st, A, lda, M, B, ldb, N, K, K, epi.elementwise());
+        else
+            hipLaunchKernelGGL((gemm_nt_mfma<T, 256, 128, kGemmBK, 4, 2, BPACK, 2, Epi, KM>), grid, dim3(8 * kWave), 0,
+                               st, A, lda, M, B, ldb, N, K, K, epi);
     } else if (g.split.splits == 1) {
         if (g.bm == 64)
             hipLaunchKernelGGL((gemm_nt_mfma<T, 64, 64, kGemmBK, 2, 2, BPACK, 2, Epi, KM>), grid, dim3(4 * kWave), 0,
