@@ -67,8 +67,9 @@ def steady(trace_csv: str, n: int, out_md: str, subs) -> None:
              for r in rows if sub in r["Kernel_Name"]]
         d.sort()
         last = [x for _, x in d[-n:]]
-        if last:
-            lines.append("| `%s` | %d | %.2f |" % (_short(sub), len(last), sum(last) / len(last) / 1e3))
+        if not last:
+            raise SystemExit("steady: no dispatch of a kernel matching %r" % sub)
+        lines.append("| `%s` | %d | %.2f |" % (_short(sub), len(last), sum(last) / len(last) / 1e3))
     with open(out_md, "a") as f:
         f.write("\n".join(lines) + "\n")
 
@@ -138,6 +139,8 @@ def traffic(fetch_dir, write_dir, kernel_sub, launch_name, out_txt, command):
     write = _counter(write_dir, "WRITE_SIZE")
     k_fetch, nf = _avg(fetch, lambda n: kernel_sub in n)
     k_write, nw = _avg(write, lambda n: kernel_sub in n)
+    if not nf or not nw:
+        raise SystemExit("traffic: no dispatch of a kernel matching %r (FETCH %d, WRITE %d)" % (kernel_sub, nf, nw))
     is_copy = _is_copy
     # the calibration copy is the largest copy dispatch in the run
     c_fetch = max((x for n, x in fetch if is_copy(n)), default=None)
