@@ -578,6 +578,21 @@ __device__ __forceinline__ void gemm_nt_tile(const T* __restrict__ A, int64_t ld
         }
         staged_store<BM, BN, WM, WN, TM, TN>(acc, m0, n0, epi.ws, smem, LDS_BYTES);
         return;
+    } else if constexpr (std::is_same<Epi, ScatterEpi<bf16, kWsNone>>::value && BM == 256) {
+        // the wider tiles of the non-pivot product: rows outer, so that the
+        // stores of one group of rows go out across all column blocks in turn
+        // (M = 4096, three alternating passes, us per launch: the MLP up
+        // projection's 256 x 192 tiles 167.5-169.9 -> 164.1-165.3, the
+        // r = 10% layer's 256 x 256 tiles 31.1-31.4 -> 28.9-29.6)
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            const int64_t mb = m0 + wm * WTM + i * 32 + 4 * (lane >> 5);
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+#pragma unroll
+                for (int j = 0; j < TN; ++j) epi.store(mb + 8 * (v >> 2) + (v & 3), ecols[j], acc[i][j][v]);
+            }
+        }
     } else {
     // 32x32 accumulator layout: lane holds column (lane % 32) and rows
     // 8*(v/4) + 4*(lane/32) + (v%4) for v = 0..15.
